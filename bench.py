@@ -1,0 +1,278 @@
+"""Throughput of the tiled dense contraction on one MI355X.
+
+A step is one launch of the contraction on the headline workload: the fp32
+matmul M = N = K = 4096 (row-major, uniform [-1, 1) inputs from a fixed seed,
+already resident in HBM).  ``value`` is its TFLOP/s (2*M*N*K per launch over
+the HIP-event time of exactly ``--steps`` launches, after ``--warmup``
+untimed ones).  The same line also reports, timed the same way, the bf16
+matmul 8192^3 (fp32 accumulate and output) and the fp32 conv2d 32x64x56x56
+-> 64, 3x3, stride 1, pad 1 as an implicit GEMM, each with its fraction of
+the MI355X matrix-core peak, and the fp64 CPU oracle timed on the host cores
+on a bounded sample of the headline workload (``cpu_baseline``), which also
+checks sampled outputs of every timed launch against the oracle.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only fp32,bf16,conv]
+                       [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import xtc_inputs as xi  # noqa: E402
+
+METRIC = "matmul TFLOP/s (fp32, bf16) and % of MI355X MFMA peak at 1 GPU"
+# MI355X published dense matrix peaks (TFLOP/s) and HBM bandwidth.
+PEAK = {"f32": 157.3, "bf16": 2516.6}
+HBM_GBS = 8000.0
+KERNEL_SOURCES = {
+    "f32": ["gemm_f32.hip", "mfma_f32.h", "tile_map.h"],
+    "bf16": ["gemm_bf16.hip", "tile_map.h"],
+    "conv": ["conv2d_f32.hip", "mfma_f32.h", "tile_map.h"],
+}
+
+
+def kernel_hash(kind: str) -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kind]:
+        h.update(open(os.path.join(ROOT, "paper_2512_16512_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kind: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when there is none for this kernel source (the counters were taken
+    on a different version of the kernel)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(workload)
+    except (ValueError, OSError):
+        return None
+    if not rec or rec.get("kernel_hash") != kernel_hash(kind):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def to_dev(arr):
+    import torch
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(arr)).cuda()
+
+
+def time_launches(fn, steps: int, warmup: int):
+    """Run ``warmup`` untimed launches, then time exactly ``steps`` launches
+    between two HIP events recorded on the launch stream (torch's current
+    stream), with a device synchronisation on both sides.  Returns ms per
+    launch."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        fn()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def run_matmul(cfg, steps, warmup):
+    import torch
+    import paper_2512_16512_amd as xtc
+    A, B = xi.matmul_inputs(cfg)
+    a, b = to_dev(A), to_dev(B)
+    c = torch.empty((cfg["M"], cfg["N"]), dtype=torch.float32, device="cuda")
+    code = xtc.XTC_F32 if cfg["dtype"] == "f32" else xtc.XTC_BF16
+    sched = xtc.xtc_default_schedule(xtc.XTC_OP_MATMUL, code, cfg["M"], cfg["N"], cfg["K"])
+    ms = time_launches(lambda: xtc.matmul(a, b, out=c, sched=sched), steps, warmup)
+    flops = 2.0 * cfg["M"] * cfg["N"] * cfg["K"]
+    elt = 4 if cfg["dtype"] == "f32" else 2
+    alg_bytes = elt * (cfg["M"] * cfg["K"] + cfg["K"] * cfg["N"]) + 4 * cfg["M"] * cfg["N"]
+    i, j = xi.sample_indices_matmul(xi.seed(cfg["index"], 3), cfg["M"], cfg["N"], cfg["check"])
+    sampled = c[torch.from_numpy(i).cuda(), torch.from_numpy(j).cuda()].cpu().numpy()
+    return dict(ms=ms, flops=flops, alg_bytes=alg_bytes, sched=repr(sched), A=A, B=B, I=i, J=j,
+                sampled=sampled)
+
+
+def run_conv(cfg, steps, warmup):
+    import torch
+    import paper_2512_16512_amd as xtc
+    X, W = xi.conv_inputs(cfg)
+    xd, wd = to_dev(X), to_dev(W)
+    OH, OW = xi.conv_out_hw(cfg["H"], cfg["W"], cfg["R"], cfg["S"], cfg["stride"], cfg["stride"],
+                            cfg["pad"], cfg["pad"])
+    y = torch.empty((cfg["N"], cfg["OC"], OH, OW), dtype=torch.float32, device="cuda")
+    Mg, Ng, Kg = cfg["OC"], cfg["N"] * OH * OW, cfg["C"] * cfg["R"] * cfg["S"]
+    sched = xtc.xtc_default_schedule(xtc.XTC_OP_CONV2D, xtc.XTC_F32, Mg, Ng, Kg)
+    ms = time_launches(lambda: xtc.conv2d_nchw(xd, wd, cfg["stride"], cfg["pad"], out=y, sched=sched),
+                       steps, warmup)
+    F = xi.sample_indices_flat(xi.seed(cfg["index"], 3), y.numel(), cfg["check"])
+    sampled = y.reshape(-1)[torch.from_numpy(F).cuda()].cpu().numpy()
+    alg_bytes = 4 * (X.size + W.size + y.numel())
+    return dict(ms=ms, flops=2.0 * Mg * Ng * Kg, alg_bytes=alg_bytes, sched=repr(sched), X=X, W=W,
+                F=F, sampled=sampled, gemm=(Mg, Ng, Kg))
+
+
+def summary(kind, cfg, r, workload):
+    tflops = r["flops"] / (r["ms"] * 1e-3) / 1e12
+    traffic = measured_traffic(kind, workload)
+    return {
+        "workload": workload,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "ms_per_launch": round(r["ms"], 4),
+        "frac_of_peak": round(tflops / PEAK["bf16" if kind == "bf16" else "f32"], 4),
+        "schedule": r["sched"],
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(tflops, 2),
+            "peak": PEAK["bf16" if kind == "bf16" else "f32"],
+            "unit": "TFLOP/s",
+            "frac": round(tflops / PEAK["bf16" if kind == "bf16" else "f32"], 4),
+            "traffic": traffic,
+            "alg_bytes": r["alg_bytes"],
+            "alg_hbm_GBps": round(r["alg_bytes"] / (r["ms"] * 1e-3) / 1e9, 1),
+        },
+    }
+
+
+def cpu_baseline_leg(results, budget_s: float):
+    """The fp64 oracle on the host cores: (1) a bounded sample of the
+    headline workload -- leading row slabs of the fp32 4096^3 product, run
+    until ``budget_s`` seconds have elapsed or every row is done -- reported
+    in TFLOP/s; (2) the sampled parity check of every timed launch."""
+    import oracle
+    out = {}
+    if "fp32" in results:
+        r = results["fp32"]
+        A, B = r["A"], r["B"]
+        M, K = A.shape
+        N = B.shape[1]
+        rows, t0 = 0, time.perf_counter()
+        slab = 128
+        while rows < M and time.perf_counter() - t0 < budget_s:
+            oracle.matmul(A, B, rows=(rows, min(M, rows + slab)))
+            rows = min(M, rows + slab)
+        dt = time.perf_counter() - t0
+        out["cpu_baseline"] = {
+            "value": round(2.0 * rows * N * K / dt / 1e12, 6),
+            "unit": "TFLOP/s",
+            "cores": oracle.max_threads(),
+            "kind": "oracle",
+            "sample": "fp64 oracle (i-k-j loop, OpenMP over rows) on the first %d of %d rows of "
+                      "the fp32 %dx%dx%d matmul, %.1f s wall" % (rows, M, M, N, K, dt),
+            "cpu_model": _cpu_model(),
+        }
+    parity = {}
+    for kind, r in results.items():
+        if kind == "conv":
+            ref = oracle.conv2d_sampled(r["X"], r["W"], r["F"], stride=1, pad=1)
+            tol = 1e-5
+        else:
+            ref = oracle.matmul_sampled(r["A"], r["B"], r["I"], r["J"])
+            tol = 1e-5 if kind == "fp32" else 1e-2
+        err = oracle.rel_fro(r["sampled"], ref)
+        parity[kind] = {"rel_fro": float("%.3e" % err), "tol": tol, "samples": int(len(ref)),
+                        "ok": bool(err <= tol)}
+    out["parity"] = parity
+    return out
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--only", default="fp32,bf16,conv")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the contraction is benchmarked on a single "
+              "MI355X and no multi-GPU path is built (--gpus must be 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU (torch.cuda.is_available() is False)", file=sys.stderr)
+        sys.exit(1)
+    import paper_2512_16512_amd  # noqa: F401  (fails loudly if libxtc.so is missing)
+
+    kinds = [k.strip() for k in args.only.split(",") if k.strip()]
+    results, summaries = {}, {}
+    if "fp32" in kinds:
+        cfg = xi.CONFIGS[2]
+        results["fp32"] = run_matmul(cfg, args.steps, args.warmup)
+        summaries["fp32"] = summary("f32", cfg, results["fp32"], "matmul_f32_4096x4096x4096")
+        print("# fp32 4096^3: %.4f ms/launch" % results["fp32"]["ms"], file=sys.stderr, flush=True)
+    if "bf16" in kinds:
+        cfg = xi.CONFIGS[3]
+        results["bf16"] = run_matmul(cfg, args.steps, args.warmup)
+        summaries["bf16"] = summary("bf16", cfg, results["bf16"], "matmul_bf16_8192x8192x8192")
+        print("# bf16 8192^3: %.4f ms/launch" % results["bf16"]["ms"], file=sys.stderr, flush=True)
+    if "conv" in kinds:
+        cfg = xi.CONFIGS[4]
+        results["conv"] = run_conv(cfg, args.steps, args.warmup)
+        summaries["conv"] = summary("conv", cfg, results["conv"], "conv2d_f32_n32c64h56w56_oc64_r3s3")
+        print("# conv: %.4f ms/launch" % results["conv"]["ms"], file=sys.stderr, flush=True)
+
+    head_kind = "fp32" if "fp32" in summaries else kinds[0]
+    head = summaries[head_kind]
+    line = {
+        "metric": METRIC,
+        "value": head["value"],
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_launch"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if head_kind != "bf16" else "bf16",
+        "data": "synthetic: splitmix64 uniform [-1,1) inputs from fixed seeds, resident in HBM",
+        "config": {
+            "workload": head["workload"],
+            "M": 4096, "N": 4096, "K": 4096, "layout": "row-major A[M,K], B[K,N], C[M,N]",
+            "schedule": head["schedule"],
+            "device": torch.cuda.get_device_name(0),
+        },
+        "roofline": head["roofline"],
+        "frac_of_peak": head["frac_of_peak"],
+        "also": {k: v for k, v in summaries.items() if k != head_kind},
+    }
+    if not args.no_cpu_baseline:
+        extra = cpu_baseline_leg(results, args.cpu_budget)
+        if "cpu_baseline" in extra:
+            line["cpu_baseline"] = extra["cpu_baseline"]
+        line["parity"] = extra["parity"]
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

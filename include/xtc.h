@@ -1,0 +1,197 @@
+/*
+ * xtc.h -- C ABI of libxtc.so, the MI355X (gfx950) tiled dense contraction.
+ *
+ * One function per operator, inputs before outputs, every tensor a raw
+ * pointer to contiguous memory (the paper's module ABI, Sec. 4.1, "Module":
+ * a function named after the operator that takes the operator's inputs and
+ * outputs as contiguous raw pointers).  The schedule is an explicit struct so
+ * that schedules can be swept: its fields are the GPU forms of the paper's
+ * scheduling primitives (Sec. 3.2, Table 1): strip-mine/tile (block_*,
+ * wave_*), vectorize (mfma_*), pack with padding (lds_stages, lds_pad),
+ * unroll (unroll_k), parallelize (the workgroup grid) and interchange of the
+ * parallel tile loops (raster, xcd_remap).
+ *
+ * Plain C: no HIP header is needed to use it.  The stream is an opaque
+ * hipStream_t passed as void* (NULL = the null stream).
+ *
+ * Common rules for every entry point
+ * ----------------------------------
+ * - Tensor pointers are DEVICE pointers, allocated and owned by the caller.
+ *   The library allocates nothing, keeps no pointer after it returns and
+ *   holds no mutable global state except a thread-local last HIP error code.
+ * - Outputs must not overlap inputs (the paper declares its operands
+ *   noalias, Fig. 5).  This is not checked.
+ * - Every argument and schedule check happens on the host BEFORE any HIP
+ *   call, so invalid calls return an error without touching the device.
+ * - Kernels are enqueued on `stream`; calls are asynchronous and never
+ *   synchronise.  Faults during execution surface at the caller's next
+ *   synchronisation on that stream, not in the return value.
+ * - The return value is the only error channel.
+ * - Element offsets are 32-bit inside the kernels: every operand's span
+ *   (bytes from its first to its last addressed element) must be < 2^31,
+ *   else XTC_ERR_TOO_LARGE.
+ */
+#ifndef XTC_H
+#define XTC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element types.  XTC_BF16: inputs are bf16 bit patterns (uint16), products
+ * are exact in fp32, accumulation and output are fp32. */
+typedef enum { XTC_F32 = 0, XTC_BF16 = 1 } xtc_dtype;
+
+typedef enum { XTC_OP_MATMUL = 0, XTC_OP_CONV2D = 1 } xtc_op;
+
+typedef enum {
+    XTC_OK = 0,
+    XTC_ERR_NULL_POINTER = 1,         /* a tensor or output pointer is NULL   */
+    XTC_ERR_BAD_SHAPE = 2,            /* negative or inconsistent extents     */
+    XTC_ERR_BAD_LEADING_DIM = 3,      /* lda < K, ldb < N or ldc < N          */
+    XTC_ERR_BAD_DTYPE = 4,            /* unknown dtype, or not supported here */
+    XTC_ERR_BAD_SCHEDULE = 5,         /* illegal field values / combination   */
+    XTC_ERR_UNSUPPORTED_SCHEDULE = 6, /* legal but not among compiled ones    */
+    XTC_ERR_TOO_LARGE = 7,            /* an operand span is >= 2^31 bytes     */
+    XTC_ERR_HIP = 8                   /* a HIP call failed (see below)        */
+} xtc_status;
+
+/*
+ * Schedule of one contraction C[M,N] = A[M,K] B[K,N] (for conv2d the implicit
+ * GEMM: M = OC, N = batch*OH*OW, K = C*R*S; see xtc_conv2d_nchw).
+ *
+ *  size          sizeof(xtc_sched) as known to the caller (ABI versioning).
+ *  block_m/n/k   workgroup tile: the outer strip-mine of M and N (one
+ *                workgroup per tile, parallelized over the CUs) and the
+ *                K-step staged in LDS per pipeline stage.
+ *  wave_m/n      tile of one 64-lane wavefront inside the workgroup tile
+ *                (second strip-mine level); the workgroup has
+ *                (block_m/wave_m)*(block_n/wave_n) waves.
+ *  mfma_m/n/k    matrix-core instruction tile (the vectorize primitive):
+ *                fp32: 32x32x2 or 16x16x4; bf16: 32x32x16 or 16x16x32.
+ *  lds_stages    LDS buffers per operand (pack + software pipelining): 2.
+ *  lds_pad       LDS row padding in elements (pack with padding against bank
+ *                conflicts); -1 selects an XOR-swizzled layout instead.
+ *  unroll_k      MFMA k-steps unrolled per LDS stage (0 = the whole stage).
+ *  raster        order of the parallel tile loops (interchange): 0 row-major
+ *                (N fastest), 1 column-major (M fastest), g >= 2 grouped:
+ *                bands of g tile-rows, walked column by column.
+ *  xcd_remap     1: renumber workgroups so that each of the 8 XCDs (which
+ *                receive workgroups round-robin and each own an L2) works on
+ *                one contiguous band of the tile order; 0: hardware order.
+ *
+ * block_*, wave_*, mfma_*, lds_stages, lds_pad and unroll_k select a compiled
+ * kernel instance; raster and xcd_remap are run-time choices valid for all.
+ */
+typedef struct {
+    int32_t size;
+    int32_t block_m, block_n, block_k;
+    int32_t wave_m, wave_n;
+    int32_t mfma_m, mfma_n, mfma_k;
+    int32_t lds_stages;
+    int32_t lds_pad;
+    int32_t unroll_k;
+    int32_t raster;
+    int32_t xcd_remap;
+} xtc_sched;
+
+/*
+ * xtc_matmul -- C = A * B  (paper Sec. 3.1, Fig. 2: C[i][j] accumulates
+ * A[i][k]*B[k][j] over k; here C is overwritten, i.e. accumulation starts
+ * from zero).
+ *
+ *  M, N, K   extents, >= 0.  M == 0 or N == 0: no-op returning XTC_OK.
+ *            K == 0: C[0:M, 0:N] is set to zero.
+ *  A         device, row-major M x K with row stride lda >= max(K,1)
+ *            (elements); fp32 (XTC_F32) or bf16 bits (XTC_BF16).
+ *  B         device, row-major K x N with row stride ldb >= max(N,1).
+ *  C         device, fp32, row-major M x N with row stride ldc >= max(N,1).
+ *            Only C[i*ldc + j] for i < M, j < N is written; columns
+ *            N <= j < ldc are never touched.
+ *  dtype     XTC_F32 or XTC_BF16 (applies to A and B; C is always fp32).
+ *  sched     NULL selects xtc_default_schedule(); otherwise must pass
+ *            xtc_sched_check().
+ *  stream    hipStream_t or NULL.
+ * Errors: XTC_ERR_NULL_POINTER (A, B or C NULL while M, N > 0),
+ * XTC_ERR_BAD_SHAPE (negative extent), XTC_ERR_BAD_LEADING_DIM,
+ * XTC_ERR_BAD_DTYPE, XTC_ERR_BAD_SCHEDULE, XTC_ERR_UNSUPPORTED_SCHEDULE,
+ * XTC_ERR_TOO_LARGE, XTC_ERR_HIP (launch failed).
+ */
+xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K,
+                      const void *A, int64_t lda,
+                      const void *B, int64_t ldb,
+                      float *C, int64_t ldc,
+                      xtc_dtype dtype, const xtc_sched *sched, void *stream);
+
+/*
+ * xtc_conv2d_nchw -- 2-D convolution (the paper's conv2d operator, Sec. 3.1)
+ * read as zero-padded cross-correlation without dilation, groups or bias:
+ *   Y[n][oc][oh][ow] = sum_{ic<C, kh<R, kw<S}
+ *        X[n][ic][oh*stride_h - pad_h + kh][ow*stride_w - pad_w + kw]
+ *        * Wt[oc][ic][kh][kw],
+ * input positions outside [0,H) x [0,W) contributing zero, with
+ *   OH = (H + 2*pad_h - R)/stride_h + 1,  OW = (W + 2*pad_w - S)/stride_w + 1.
+ * Computed as an implicit GEMM (no im2col buffer): M = OC, N = N*OH*OW,
+ * K = C*R*S with k = (ic*R + kh)*S + kw.
+ *
+ *  X    device, NCHW contiguous fp32.      Wt  device, OIHW contiguous fp32.
+ *  Y    device, N x OC x OH x OW contiguous fp32 (overwritten).
+ *  N, C, H, W, OC, R, S >= 1 except that N == 0 or OC == 0 is a no-op;
+ *  stride >= 1, pad >= 0, OH >= 1 and OW >= 1, else XTC_ERR_BAD_SHAPE.
+ *  dtype must be XTC_F32 (else XTC_ERR_BAD_DTYPE).
+ *  sched NULL selects the default conv schedule.
+ * Errors as for xtc_matmul; XTC_ERR_TOO_LARGE also when C*R*S exceeds the
+ * kernel's k-offset table capacity (xtc_conv_max_k()).
+ */
+xtc_status xtc_conv2d_nchw(int64_t N, int64_t C, int64_t H, int64_t W,
+                           int64_t OC, int64_t R, int64_t S,
+                           int64_t stride_h, int64_t stride_w,
+                           int64_t pad_h, int64_t pad_w,
+                           const void *X, const void *Wt, float *Y,
+                           xtc_dtype dtype, const xtc_sched *sched, void *stream);
+
+/*
+ * xtc_default_schedule -- the schedule used when sched == NULL, chosen from
+ * the problem shape (the paper's default_schedule of an exploration
+ * strategy, Sec. 5.2).  For op == XTC_OP_CONV2D pass the implicit-GEMM
+ * extents.  Pure host function.  Errors: XTC_ERR_NULL_POINTER (out NULL),
+ * XTC_ERR_BAD_DTYPE, XTC_ERR_BAD_SHAPE.
+ */
+xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dtype,
+                                int64_t M, int64_t N, int64_t K, xtc_sched *out);
+
+/*
+ * xtc_sched_check -- XTC_OK if `s` can run op/dtype: its fields are legal
+ * (XTC_ERR_BAD_SCHEDULE otherwise) and they name a compiled instance
+ * (XTC_ERR_UNSUPPORTED_SCHEDULE otherwise).  Pure host function.
+ */
+xtc_status xtc_sched_check(xtc_op op, xtc_dtype dtype, const xtc_sched *s);
+
+/*
+ * xtc_sched_list -- writes up to `cap` compiled schedules for op/dtype into
+ * `out` (raster = 0, xcd_remap = 1) and returns how many exist in total
+ * (call with cap = 0 to size the array).  Returns -1 for an unknown
+ * op/dtype.  Pure host function.
+ */
+int32_t xtc_sched_list(xtc_op op, xtc_dtype dtype, xtc_sched *out, int32_t cap);
+
+/* Static description of a status code. */
+const char *xtc_status_str(xtc_status s);
+
+/* hipError_t value of the last failed HIP call made by this thread inside
+ * the library (0 if none). */
+int32_t xtc_last_hip_error(void);
+
+/* Largest C*R*S accepted by xtc_conv2d_nchw. */
+int64_t xtc_conv_max_k(void);
+
+/* Library version: major*10000 + minor*100 + patch. */
+int32_t xtc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XTC_H */

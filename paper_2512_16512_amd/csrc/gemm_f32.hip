@@ -1,0 +1,213 @@
+// fp32 GEMM on the gfx950 matrix cores: C[M,N] = A[M,K] * B[K,N], row-major,
+// fp32 in, fp32 accumulate, fp32 out (C overwritten).
+//
+// How the paper's scheduling primitives (Sec. 3.2) appear here:
+//  - strip-mine / tile + parallelize: one workgroup per BM x BN tile of C,
+//    the tile grid spread over the CUs (tile_map.h for the order);
+//  - second tiling level: each 64-lane wave owns a WM x WN sub-tile;
+//  - vectorize: the innermost tile is one MFMA instruction tile
+//    (32x32x2 or 16x16x4 fp32), accumulators stay in registers
+//    (bufferize: they are written to C once, at the end);
+//  - pack (with padding): each K-step of A (BM x BK) and B (BK x BN) is
+//    copied to LDS in padded rows, double-buffered so that the global loads
+//    of step t+1 overlap the matrix-core work of step t;
+//  - split: the last K-step and the edge tiles use predicated loads that
+//    zero-fill outside the matrix, and predicated stores.
+//
+// Operand fragments.  An fp32 MFMA of shape MIxMIxKG takes, per lane, one
+// A value (row lane%MI, k-group lane/MI) and one B value (column lane%MI,
+// k-group lane/MI).  Any assignment of the K-step's k values to
+// (instruction, k-group) works as long as A and B agree; here lane group g
+// of instruction s takes k = kk + 4g + s, so one ds_read_b128 per lane
+// fetches the A values of four consecutive instructions from a k-contiguous
+// LDS row, and B (n-contiguous in LDS) is read with conflict-free
+// ds_read_b32 (lanes of one group read consecutive columns).
+#include "mfma_f32.h"
+#include "tile_map.h"
+#include "xtc_internal.h"
+
+namespace xtc {
+namespace {
+
+template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD, bool VEC>
+struct GemmF32Cfg {
+    static constexpr int NWM = BM / WM, NWN = BN / WN;
+    static constexpr int NT = NWM * NWN * 64;
+    static constexpr int TM = WM / MI, TN = WN / MI;
+    typedef F32Mfma<MI> MF;
+    static constexpr int KG = MF::KG;
+    static constexpr int KCH = 4 * KG;                 // k consumed per A fragment read
+    static constexpr int AS = BK + PAD;                // A tile LDS row stride (floats)
+    static constexpr int BS = BN + (MI == 32 ? 8 : 4); // B tile LDS row stride (floats)
+    static constexpr int W = VEC ? 4 : 1;              // elements per global load
+    static constexpr int A_CPR = BK / W;               // loads per A tile row
+    static constexpr int B_CPR = BN / W;               // loads per B tile row
+    static constexpr int A_LOADS = BM * BK / (W * NT);
+    static constexpr int B_LOADS = BK * BN / (W * NT);
+    typedef typename VecF32<W>::t vec_t;
+    static_assert(BM % WM == 0 && BN % WN == 0, "wave tile must divide the block tile");
+    static_assert(WM % MI == 0 && WN % MI == 0, "MFMA tile must divide the wave tile");
+    static_assert(BK % KCH == 0, "block_k must be a multiple of the fragment k-chunk");
+    static_assert(A_LOADS * W * NT == BM * BK, "A tile must split evenly over threads");
+    static_assert(B_LOADS * W * NT == BK * BN, "B tile must split evenly over threads");
+    static_assert(PAD % 4 == 0, "A padding must keep 16-byte alignment");
+};
+
+template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD, bool VEC>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+gemm_f32_kernel(GemmArgs p) {
+    typedef GemmF32Cfg<BM, BN, BK, WM, WN, MI, PAD, VEC> G;
+    typedef typename G::MF MF;
+    typedef typename G::vec_t vec_t;
+    constexpr int W = G::W;
+
+    __shared__ __attribute__((aligned(16))) float As[2][BM * G::AS];
+    __shared__ __attribute__((aligned(16))) float Bs[2][BK * G::BS];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / G::NWN, wn = wave % G::NWN;
+    const int lrow = lane % MI, lgrp = lane / MI;
+
+    const int M = p.M, N = p.N, K = p.K;
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const float *__restrict__ A = static_cast<const float *>(p.A);
+    const float *__restrict__ B = static_cast<const float *>(p.B);
+    const int lda = p.lda, ldb = p.ldb;
+
+    vec_t ra[G::A_LOADS], rb[G::B_LOADS];
+
+    // Global -> registers for K-step kt (zero-filled outside the matrix).
+    auto load_tiles = [&](int kt) {
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int i = 0; i < G::A_LOADS; ++i) {
+            const int idx = tid + i * G::NT;
+            const int r = idx / G::A_CPR, c = (idx % G::A_CPR) * W;
+            const int gm = m0 + r, gk = k0 + c;
+            const int valid = gm < M ? K - gk : 0;
+            ra[i] = load_pred<W>(A + (gm < M ? gm : 0) * lda + (valid > 0 ? gk : 0), valid);
+        }
+#pragma unroll
+        for (int i = 0; i < G::B_LOADS; ++i) {
+            const int idx = tid + i * G::NT;
+            const int r = idx / G::B_CPR, c = (idx % G::B_CPR) * W;
+            const int gk = k0 + r, gn = n0 + c;
+            const int valid = gk < K ? N - gn : 0;
+            rb[i] = load_pred<W>(B + (gk < K ? gk : 0) * ldb + (valid > 0 ? gn : 0), valid);
+        }
+    };
+
+    // Registers -> LDS stage `st`.
+    auto store_tiles = [&](int st) {
+#pragma unroll
+        for (int i = 0; i < G::A_LOADS; ++i) {
+            const int idx = tid + i * G::NT;
+            const int r = idx / G::A_CPR, c = (idx % G::A_CPR) * W;
+            *reinterpret_cast<vec_t *>(&As[st][r * G::AS + c]) = ra[i];
+        }
+#pragma unroll
+        for (int i = 0; i < G::B_LOADS; ++i) {
+            const int idx = tid + i * G::NT;
+            const int r = idx / G::B_CPR, c = (idx % G::B_CPR) * W;
+            *reinterpret_cast<vec_t *>(&Bs[st][r * G::BS + c]) = rb[i];
+        }
+    };
+
+    typename MF::acc_t acc[G::TM][G::TN];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[i][j][r] = 0.f;
+
+    const int KT = (K + BK - 1) / BK;
+    if (KT > 0) {
+        load_tiles(0);
+        store_tiles(0);
+        __syncthreads();
+    }
+    for (int kt = 0; kt < KT; ++kt) {
+        const int cur = kt & 1;
+        const bool has_next = kt + 1 < KT;
+        if (has_next) load_tiles(kt + 1);
+
+        const float *as = &As[cur][(wm * WM + lrow) * G::AS + 4 * lgrp];
+        const float *bs = &Bs[cur][(4 * lgrp) * G::BS + wn * WN + lrow];
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += G::KCH) {
+            f32x4 a[G::TM];
+            float b[G::TN][4];
+#pragma unroll
+            for (int i = 0; i < G::TM; ++i)
+                a[i] = *reinterpret_cast<const f32x4 *>(as + i * MI * G::AS + kk);
+#pragma unroll
+            for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+                for (int s = 0; s < 4; ++s) b[j][s] = bs[(kk + s) * G::BS + j * MI];
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < G::TN; ++j) acc[i][j] = MF::mma(a[i][s], b[j][s], acc[i][j]);
+        }
+
+        if (has_next) store_tiles(cur ^ 1);
+        __syncthreads();
+    }
+
+    // Epilogue: accumulators -> C, masked on the edges.
+    float *__restrict__ C = p.C;
+    const int ldc = p.ldc;
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j) {
+            const int col = n0 + wn * WN + j * MI + lrow;
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
+                if (row < M && col < N) C[row * ldc + col] = acc[i][j][r];
+            }
+        }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD, bool VEC>
+hipError_t launch_f32(const GemmArgs &a, hipStream_t s) {
+    typedef GemmF32Cfg<BM, BN, BK, WM, WN, MI, PAD, VEC> G;
+    const unsigned tiles = (unsigned)(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
+    GemmArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&gemm_f32_kernel<BM, BN, BK, WM, WN, MI, PAD, VEC>),
+                           dim3(tiles), dim3(G::NT), kargs, 0, s);
+}
+
+#define XTC_F32_INSTANCE(BM, BN, BK, WM, WN, MI, PAD)                                         \
+    GemmInstance {                                                                            \
+        make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 2 : 4), 2, PAD, 0),                 \
+            &launch_f32<BM, BN, BK, WM, WN, MI, PAD, true>,                                   \
+            &launch_f32<BM, BN, BK, WM, WN, MI, PAD, false>                                   \
+    }
+
+const GemmInstance kF32Instances[] = {
+    XTC_F32_INSTANCE(128, 128, 32, 64, 64, 32, 4),   // default for large problems
+    XTC_F32_INSTANCE(128, 128, 16, 64, 64, 32, 4),
+    XTC_F32_INSTANCE(64, 64, 32, 32, 32, 32, 4),     // small problems: more tiles
+    XTC_F32_INSTANCE(128, 128, 32, 64, 64, 16, 4),   // 16x16x4 instruction tile
+    XTC_F32_INSTANCE(256, 128, 16, 128, 64, 32, 4),
+};
+
+}  // namespace
+
+const GemmInstance *gemm_f32_instances(int *count) {
+    *count = (int)(sizeof(kF32Instances) / sizeof(kF32Instances[0]));
+    return kF32Instances;
+}
+
+}  // namespace xtc

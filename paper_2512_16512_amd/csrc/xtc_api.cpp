@@ -1,0 +1,254 @@
+// Host side of the C ABI declared in include/xtc.h: argument and schedule
+// validation (before any HIP call), compiled-instance lookup, default
+// schedules and the launch on the caller's stream.
+#include <string.h>
+
+#include "xtc_internal.h"
+
+namespace {
+
+using namespace xtc;
+
+thread_local int32_t g_last_hip_error = 0;
+
+constexpr int64_t kMaxSpan = (int64_t(1) << 31) - 1;  // bytes; kernels use 32-bit offsets
+constexpr int kLdsBytes = 160 * 1024;                  // LDS per CU on gfx950
+
+// Bytes from the first to one past the last addressed element of a
+// rows x cols row-major operand with row stride ld (0 if empty).
+int64_t span_bytes(int64_t rows, int64_t cols, int64_t ld, int64_t elt) {
+    if (rows <= 0 || cols <= 0) return 0;
+    return ((rows - 1) * ld + cols) * elt;
+}
+
+bool same_instance(const xtc_sched &a, const xtc_sched &b) {
+    return a.block_m == b.block_m && a.block_n == b.block_n && a.block_k == b.block_k &&
+           a.wave_m == b.wave_m && a.wave_n == b.wave_n && a.mfma_m == b.mfma_m &&
+           a.mfma_n == b.mfma_n && a.mfma_k == b.mfma_k && a.lds_stages == b.lds_stages &&
+           a.lds_pad == b.lds_pad && (a.unroll_k == b.unroll_k || a.unroll_k == 0 || b.unroll_k == 0);
+}
+
+bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+// Structural legality of a schedule for op/dtype, independent of whether it
+// was compiled.
+xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
+    if (s.size != (int32_t)sizeof(xtc_sched)) return XTC_ERR_BAD_SCHEDULE;
+    if (!pow2(s.block_m) || !pow2(s.block_n) || !pow2(s.block_k) || !pow2(s.wave_m) ||
+        !pow2(s.wave_n))
+        return XTC_ERR_BAD_SCHEDULE;
+    if (s.block_m % s.wave_m || s.block_n % s.wave_n) return XTC_ERR_BAD_SCHEDULE;
+    const int waves = (s.block_m / s.wave_m) * (s.block_n / s.wave_n);
+    if (waves < 1 || waves > 16) return XTC_ERR_BAD_SCHEDULE;  // <= 1024 threads
+    // instruction tiles the matrix cores offer for this dtype
+    if (s.mfma_m != s.mfma_n) return XTC_ERR_BAD_SCHEDULE;
+    if (dt == XTC_F32) {
+        if (!((s.mfma_m == 32 && s.mfma_k == 2) || (s.mfma_m == 16 && s.mfma_k == 4)))
+            return XTC_ERR_BAD_SCHEDULE;
+    } else {
+        if (!((s.mfma_m == 32 && s.mfma_k == 16) || (s.mfma_m == 16 && s.mfma_k == 32)))
+            return XTC_ERR_BAD_SCHEDULE;
+    }
+    if (s.wave_m % s.mfma_m || s.wave_n % s.mfma_n) return XTC_ERR_BAD_SCHEDULE;
+    const int kchunk = dt == XTC_F32 ? 4 * (64 / s.mfma_m) : s.mfma_k;
+    if (s.block_k % kchunk) return XTC_ERR_BAD_SCHEDULE;
+    if (s.lds_stages < 1 || s.lds_stages > 4) return XTC_ERR_BAD_SCHEDULE;
+    if (s.lds_pad < -1 || s.lds_pad > 64) return XTC_ERR_BAD_SCHEDULE;
+    if (s.unroll_k < 0) return XTC_ERR_BAD_SCHEDULE;
+    if (s.raster < 0 || s.xcd_remap < 0 || s.xcd_remap > 1) return XTC_ERR_BAD_SCHEDULE;
+    // LDS budget of the staged tiles
+    const int elt = dt == XTC_F32 ? 4 : 2;
+    const int pad = s.lds_pad > 0 ? s.lds_pad : 0;
+    const int64_t lds = (int64_t)s.lds_stages * elt *
+                        ((int64_t)s.block_m * (s.block_k + pad) + (int64_t)s.block_n * (s.block_k + 8));
+    if (lds > kLdsBytes) return XTC_ERR_BAD_SCHEDULE;
+    if (op == XTC_OP_CONV2D && dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
+    return XTC_OK;
+}
+
+const GemmInstance *find_gemm(xtc_dtype dt, const xtc_sched &s) {
+    int n = 0;
+    const GemmInstance *tab = dt == XTC_F32 ? gemm_f32_instances(&n) : gemm_bf16_instances(&n);
+    for (int i = 0; i < n; ++i)
+        if (same_instance(tab[i].sched, s)) return &tab[i];
+    return nullptr;
+}
+
+const ConvInstance *find_conv(const xtc_sched &s) {
+    int n = 0;
+    const ConvInstance *tab = conv2d_f32_instances(&n);
+    for (int i = 0; i < n; ++i)
+        if (same_instance(tab[i].sched, s)) return &tab[i];
+    return nullptr;
+}
+
+xtc_status hip_status(hipError_t e) {
+    if (e == hipSuccess) return XTC_OK;
+    g_last_hip_error = (int32_t)e;
+    return XTC_ERR_HIP;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char *xtc_status_str(xtc_status s) {
+    switch (s) {
+        case XTC_OK: return "ok";
+        case XTC_ERR_NULL_POINTER: return "null pointer";
+        case XTC_ERR_BAD_SHAPE: return "bad shape";
+        case XTC_ERR_BAD_LEADING_DIM: return "bad leading dimension";
+        case XTC_ERR_BAD_DTYPE: return "bad or unsupported dtype";
+        case XTC_ERR_BAD_SCHEDULE: return "illegal schedule";
+        case XTC_ERR_UNSUPPORTED_SCHEDULE: return "schedule not among the compiled instances";
+        case XTC_ERR_TOO_LARGE: return "operand too large for 32-bit offsets";
+        case XTC_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+int32_t xtc_last_hip_error(void) { return g_last_hip_error; }
+
+int64_t xtc_conv_max_k(void) { return kConvMaxK; }
+
+int32_t xtc_version(void) { return 100; }
+
+xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, int64_t K,
+                                xtc_sched *out) {
+    if (!out) return XTC_ERR_NULL_POINTER;
+    if (dt != XTC_F32 && dt != XTC_BF16) return XTC_ERR_BAD_DTYPE;
+    if (op != XTC_OP_MATMUL && op != XTC_OP_CONV2D) return XTC_ERR_BAD_SHAPE;
+    if (M < 0 || N < 0 || K < 0) return XTC_ERR_BAD_SHAPE;
+    const int64_t cus = 256;
+    auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
+    if (op == XTC_OP_CONV2D) {
+        if (dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
+        *out = make_sched(64, 128, 32, 32, 64, 32, 32, 2, 2, 4, 0);
+        if (M > 64) *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, 4, 0);
+        out->raster = 0;
+        return XTC_OK;
+    }
+    if (dt == XTC_F32) {
+        // Large tiles once they still give at least one tile per CU.
+        if (tiles(128, 128) >= cus)
+            *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, 4, 0);
+        else
+            *out = make_sched(64, 64, 32, 32, 32, 32, 32, 2, 2, 4, 0);
+    } else {
+        if (tiles(256, 256) >= cus)
+            *out = make_sched(256, 256, 64, 128, 64, 32, 32, 16, 2, 8, 0);
+        else if (tiles(128, 128) >= cus)
+            *out = make_sched(128, 128, 64, 64, 64, 32, 32, 16, 2, 8, 0);
+        else
+            *out = make_sched(64, 64, 64, 32, 32, 32, 32, 16, 2, 8, 0);
+    }
+    out->raster = tiles(out->block_m, out->block_n) >= 64 ? 8 : 0;
+    return XTC_OK;
+}
+
+xtc_status xtc_sched_check(xtc_op op, xtc_dtype dt, const xtc_sched *s) {
+    if (!s) return XTC_ERR_NULL_POINTER;
+    if (dt != XTC_F32 && dt != XTC_BF16) return XTC_ERR_BAD_DTYPE;
+    if (op != XTC_OP_MATMUL && op != XTC_OP_CONV2D) return XTC_ERR_BAD_SCHEDULE;
+    const xtc_status st = legal(op, dt, *s);
+    if (st != XTC_OK) return st;
+    if (op == XTC_OP_MATMUL) return find_gemm(dt, *s) ? XTC_OK : XTC_ERR_UNSUPPORTED_SCHEDULE;
+    return find_conv(*s) ? XTC_OK : XTC_ERR_UNSUPPORTED_SCHEDULE;
+}
+
+int32_t xtc_sched_list(xtc_op op, xtc_dtype dt, xtc_sched *out, int32_t cap) {
+    int n = 0;
+    if (op == XTC_OP_MATMUL && dt == XTC_F32) {
+        const GemmInstance *t = gemm_f32_instances(&n);
+        for (int i = 0; i < n && i < cap && out; ++i) out[i] = t[i].sched;
+    } else if (op == XTC_OP_MATMUL && dt == XTC_BF16) {
+        const GemmInstance *t = gemm_bf16_instances(&n);
+        for (int i = 0; i < n && i < cap && out; ++i) out[i] = t[i].sched;
+    } else if (op == XTC_OP_CONV2D && dt == XTC_F32) {
+        const ConvInstance *t = conv2d_f32_instances(&n);
+        for (int i = 0; i < n && i < cap && out; ++i) out[i] = t[i].sched;
+    } else {
+        return -1;
+    }
+    return n;
+}
+
+xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
+                      int64_t ldb, float *C, int64_t ldc, xtc_dtype dtype, const xtc_sched *sched,
+                      void *stream) {
+    if (dtype != XTC_F32 && dtype != XTC_BF16) return XTC_ERR_BAD_DTYPE;
+    if (M < 0 || N < 0 || K < 0) return XTC_ERR_BAD_SHAPE;
+    if (lda < (K > 1 ? K : 1) || ldb < (N > 1 ? N : 1) || ldc < (N > 1 ? N : 1))
+        return XTC_ERR_BAD_LEADING_DIM;
+    xtc_sched s;
+    if (sched) {
+        const xtc_status st = xtc_sched_check(XTC_OP_MATMUL, dtype, sched);
+        if (st != XTC_OK) return st;
+        s = *sched;
+    } else {
+        xtc_default_schedule(XTC_OP_MATMUL, dtype, M, N, K, &s);
+    }
+    if (M == 0 || N == 0) return XTC_OK;
+    if (!C || (K > 0 && (!A || !B))) return XTC_ERR_NULL_POINTER;
+    const int64_t elt = dtype == XTC_F32 ? 4 : 2;
+    if (span_bytes(M, K, lda, elt) > kMaxSpan || span_bytes(K, N, ldb, elt) > kMaxSpan ||
+        span_bytes(M, N, ldc, 4) > kMaxSpan || lda > kMaxSpan / elt || ldb > kMaxSpan / elt ||
+        ldc > kMaxSpan / 4)
+        return XTC_ERR_TOO_LARGE;
+    const GemmInstance *inst = find_gemm(dtype, s);
+    if (!inst) return XTC_ERR_UNSUPPORTED_SCHEDULE;
+
+    GemmArgs a;
+    a.M = (int)M; a.N = (int)N; a.K = (int)K;
+    a.A = A; a.lda = (int)lda; a.B = B; a.ldb = (int)ldb; a.C = C; a.ldc = (int)ldc;
+    a.raster = s.raster; a.xcd_remap = s.xcd_remap;
+    const bool vec = K == 0 || (aligned16(A) && aligned16(B) && (lda * elt) % 16 == 0 &&
+                                (ldb * elt) % 16 == 0);
+    const GemmLaunch fn = vec ? inst->vec_launch : inst->any_launch;
+    return hip_status(fn(a, static_cast<hipStream_t>(stream)));
+}
+
+xtc_status xtc_conv2d_nchw(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int64_t R,
+                           int64_t S, int64_t stride_h, int64_t stride_w, int64_t pad_h,
+                           int64_t pad_w, const void *X, const void *Wt, float *Y, xtc_dtype dtype,
+                           const xtc_sched *sched, void *stream) {
+    if (dtype != XTC_F32 && dtype != XTC_BF16) return XTC_ERR_BAD_DTYPE;
+    if (dtype != XTC_F32) return XTC_ERR_BAD_DTYPE;
+    if (N < 0 || OC < 0 || C < 1 || H < 1 || W < 1 || R < 1 || S < 1 || stride_h < 1 ||
+        stride_w < 1 || pad_h < 0 || pad_w < 0)
+        return XTC_ERR_BAD_SHAPE;
+    if (H + 2 * pad_h < R || W + 2 * pad_w < S) return XTC_ERR_BAD_SHAPE;
+    const int64_t OH = (H + 2 * pad_h - R) / stride_h + 1;
+    const int64_t OW = (W + 2 * pad_w - S) / stride_w + 1;
+    const int64_t Mg = OC, Ng = N * OH * OW, Kg = C * R * S;
+    xtc_sched s;
+    if (sched) {
+        const xtc_status st = xtc_sched_check(XTC_OP_CONV2D, dtype, sched);
+        if (st != XTC_OK) return st;
+        s = *sched;
+    } else {
+        xtc_default_schedule(XTC_OP_CONV2D, dtype, Mg, Ng, Kg, &s);
+    }
+    if (N == 0 || OC == 0) return XTC_OK;
+    if (!X || !Wt || !Y) return XTC_ERR_NULL_POINTER;
+    if (N * C * H * W * 4 > kMaxSpan || OC * Kg * 4 > kMaxSpan || N * OC * OH * OW * 4 > kMaxSpan)
+        return XTC_ERR_TOO_LARGE;
+    if (Kg > kConvMaxK) return XTC_ERR_TOO_LARGE;
+    const ConvInstance *inst = find_conv(s);
+    if (!inst) return XTC_ERR_UNSUPPORTED_SCHEDULE;
+
+    ConvArgs a;
+    a.Nb = (int)N; a.C = (int)C; a.H = (int)H; a.W = (int)W; a.OC = (int)OC;
+    a.R = (int)R; a.S = (int)S;
+    a.sh = (int)stride_h; a.sw = (int)stride_w; a.ph = (int)pad_h; a.pw = (int)pad_w;
+    a.OH = (int)OH; a.OW = (int)OW;
+    a.X = static_cast<const float *>(X);
+    a.Wt = static_cast<const float *>(Wt);
+    a.Y = Y;
+    a.raster = s.raster; a.xcd_remap = s.xcd_remap;
+    return hip_status(inst->launch(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,76 @@
+// Internal interface between the host API (xtc_api.cpp) and the kernel
+// families (gemm_f32.hip, gemm_bf16.hip, conv2d_f32.hip).  Not installed.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/xtc.h"
+
+namespace xtc {
+
+// Arguments of one matmul launch.  Offsets are in elements and fit in
+// 32 bits (checked on the host).
+struct GemmArgs {
+    int M, N, K;
+    const void *A;
+    int lda;
+    const void *B;
+    int ldb;
+    float *C;
+    int ldc;
+    int raster;     // 0 row-major, 1 column-major, g >= 2 grouped by g tile-rows
+    int xcd_remap;  // 1: give each XCD a contiguous band of the tile order
+};
+
+// Arguments of one conv2d launch (implicit GEMM: M = OC, N = Nb*OH*OW,
+// K = C*R*S, k = (ic*R + kh)*S + kw).
+struct ConvArgs {
+    int Nb, C, H, W, OC, R, S;
+    int sh, sw, ph, pw;
+    int OH, OW;
+    const float *X;
+    const float *Wt;
+    float *Y;
+    int raster;
+    int xcd_remap;
+};
+
+using GemmLaunch = hipError_t (*)(const GemmArgs &, hipStream_t);
+using ConvLaunch = hipError_t (*)(const ConvArgs &, hipStream_t);
+
+// One compiled kernel instance.  `vec_launch` requires 16-byte aligned
+// operand rows (base pointers and leading dimensions); `any_launch` has no
+// alignment requirement.
+struct GemmInstance {
+    xtc_sched sched;
+    GemmLaunch vec_launch;
+    GemmLaunch any_launch;
+};
+
+struct ConvInstance {
+    xtc_sched sched;
+    ConvLaunch launch;
+};
+
+const GemmInstance *gemm_f32_instances(int *count);
+const GemmInstance *gemm_bf16_instances(int *count);
+const ConvInstance *conv2d_f32_instances(int *count);
+
+// Largest implicit-GEMM K the conv kernels' LDS k-offset table holds.
+constexpr int kConvMaxK = 4096;
+
+// Fills the fields of a schedule descriptor.
+inline xtc_sched make_sched(int bm, int bn, int bk, int wm, int wn, int mm, int mn, int mk,
+                            int stages, int pad, int unroll) {
+    xtc_sched s;
+    s.size = (int32_t)sizeof(xtc_sched);
+    s.block_m = bm; s.block_n = bn; s.block_k = bk;
+    s.wave_m = wm; s.wave_n = wn;
+    s.mfma_m = mm; s.mfma_n = mn; s.mfma_k = mk;
+    s.lds_stages = stages; s.lds_pad = pad; s.unroll_k = unroll;
+    s.raster = 0; s.xcd_remap = 1;
+    return s;
+}
+
+}  // namespace xtc

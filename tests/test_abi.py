@@ -1,0 +1,165 @@
+"""C ABI of libxtc.so on the CPU: the library loads without a GPU, exports
+every function include/xtc.h declares, and rejects every invalid call with the
+documented status before touching the device (all checks below use NULL or
+dummy pointers, which a kernel would fault on, so a wrong OK would show)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "xtc.h")
+
+
+@pytest.fixture(scope="module")
+def x():
+    import paper_2512_16512_amd as mod
+    return mod
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(xtc_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_declares_the_abi():
+    names = _declared_functions()
+    for n in ("xtc_matmul", "xtc_conv2d_nchw", "xtc_default_schedule", "xtc_sched_check",
+              "xtc_sched_list", "xtc_status_str"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(x):
+    lib = ctypes.CDLL(x.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), "libxtc.so does not export %s" % name
+    assert sorted(x.EXPORTS) == _declared_functions()
+
+
+def test_sched_struct_size_matches_header(x):
+    src = open(HEADER).read()
+    body = re.search(r"typedef struct \{(.*?)\} xtc_sched;", src, re.S).group(1)
+    n_fields = len(re.findall(r"\b[a-z_]+\b(?=[,;])", re.sub(r"/\*.*?\*/", "", body, flags=re.S)))
+    assert ctypes.sizeof(x.Sched) == 4 * n_fields
+
+
+def test_status_strings(x):
+    for st in range(0, 9):
+        s = x.xtc_status_str(st)
+        assert s and s != "unknown status"
+    assert x.xtc_status_str(99) == "unknown status"
+
+
+BAD = 0x10  # a dummy non-NULL pointer: dereferencing it would fault
+
+
+@pytest.mark.parametrize("args,expected", [
+    ((-1, 4, 4, BAD, 4, BAD, 4, BAD, 4, 0), 2),          # negative M
+    ((4, -1, 4, BAD, 4, BAD, 4, BAD, 4, 0), 2),          # negative N
+    ((4, 4, -1, BAD, 4, BAD, 4, BAD, 4, 0), 2),          # negative K
+    ((4, 4, 8, BAD, 7, BAD, 4, BAD, 4, 0), 3),           # lda < K
+    ((4, 8, 4, BAD, 4, BAD, 7, BAD, 8, 0), 3),           # ldb < N
+    ((4, 8, 4, BAD, 4, BAD, 8, BAD, 7, 0), 3),           # ldc < N
+    ((4, 4, 4, BAD, 4, BAD, 4, BAD, 4, 7), 4),           # unknown dtype
+    ((4, 4, 4, 0, 4, BAD, 4, BAD, 4, 0), 1),             # A NULL
+    ((4, 4, 4, BAD, 4, 0, 4, BAD, 4, 0), 1),             # B NULL
+    ((4, 4, 4, BAD, 4, BAD, 4, 0, 4, 0), 1),             # C NULL
+    ((1 << 16, 1 << 15, 1 << 15, BAD, 1 << 15, BAD, 1 << 15, BAD, 1 << 15, 0), 7),  # span >= 2^31
+    ((3, 3, 1 << 30, BAD, 1 << 30, BAD, 3, BAD, 3, 1), 7),
+])
+def test_matmul_validation(x, args, expected):
+    assert x.xtc_matmul(*args) == expected
+
+
+def test_matmul_empty_is_noop(x):
+    # M == 0 or N == 0 returns OK without any device work (NULL pointers allowed)
+    assert x.xtc_matmul(0, 5, 5, 0, 5, 0, 5, 0, 5, 0) == 0
+    assert x.xtc_matmul(5, 0, 5, 0, 5, 0, 1, 0, 1, 1) == 0
+
+
+@pytest.mark.parametrize("args,expected", [
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 1), 4),     # bf16 conv not offered
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 5), 4),     # unknown dtype
+    ((1, 0, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 0), 2),     # C = 0
+    ((1, 3, 8, 8, 4, 3, 3, 0, 1, 1, 1, BAD, BAD, BAD, 0), 2),     # stride 0
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, -1, 1, BAD, BAD, BAD, 0), 2),    # negative pad
+    ((1, 3, 2, 2, 4, 5, 5, 1, 1, 0, 0, BAD, BAD, BAD, 0), 2),     # kernel larger than input
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, 0, BAD, BAD, 0), 1),       # X NULL
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, 0, BAD, 0), 1),       # W NULL
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, 0, 0), 1),       # Y NULL
+    ((1, 1024, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 0), 7),  # C*R*S > table capacity
+])
+def test_conv_validation(x, args, expected):
+    assert x.xtc_conv2d_nchw(*args) == expected
+
+
+def test_conv_empty_is_noop(x):
+    assert x.xtc_conv2d_nchw(0, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, 0, 0, 0, 0) == 0
+    assert x.xtc_conv2d_nchw(2, 3, 8, 8, 0, 3, 3, 1, 1, 1, 1, 0, 0, 0, 0) == 0
+
+
+def test_sched_list_and_check(x):
+    for op, dt in ((0, 0), (0, 1), (1, 0)):
+        lst = x.xtc_sched_list(op, dt)
+        assert len(lst) >= 3
+        for s in lst:
+            assert x.xtc_sched_check(op, dt, s) == 0
+            for r in (0, 1, 4, 8):           # raster and xcd remap are run-time choices
+                s2 = x.Sched(**s.as_dict())
+                s2.raster = r
+                s2.xcd_remap = r & 1
+                assert x.xtc_sched_check(op, dt, s2) == 0
+    assert x.xtc_sched_list(1, 1) == []
+
+
+def _base(x, dt=0):
+    return x.Sched(**x.xtc_sched_list(0, dt)[0].as_dict())
+
+
+@pytest.mark.parametrize("field,value", [
+    ("block_m", 96), ("block_n", 0), ("wave_m", 256), ("mfma_m", 8), ("mfma_k", 16),
+    ("lds_stages", 0), ("lds_pad", -2), ("raster", -1), ("xcd_remap", 2), ("block_k", 4),
+    ("size", 12),
+])
+def test_sched_illegal_fields(x, field, value):
+    s = _base(x)
+    setattr(s, field, value)
+    assert x.xtc_sched_check(0, 0, s) == 5
+    # and the same schedule is refused by the entry point before any device work
+    assert x.xtc_matmul(4, 4, 4, BAD, 4, BAD, 4, BAD, 4, 0, s) == 5
+
+
+def test_sched_legal_but_not_compiled(x):
+    s = _base(x)
+    s.block_m, s.block_n, s.wave_m, s.wave_n = 64, 128, 32, 64
+    assert x.xtc_sched_check(0, 0, s) == 6
+    assert x.xtc_matmul(4, 4, 4, BAD, 4, BAD, 4, BAD, 4, 0, s) == 6
+
+
+def test_sched_lds_budget(x):
+    s = _base(x, 1)
+    s.block_m = s.block_n = 512
+    s.wave_m, s.wave_n = 128, 128
+    assert x.xtc_sched_check(0, 1, s) == 5
+
+
+def test_bf16_schedule_rejected_for_f32(x):
+    s = _base(x, 1)
+    assert x.xtc_sched_check(0, 0, s) == 5
+
+
+def test_default_schedules_are_compiled(x):
+    for (op, dt, M, N, K) in [(0, 0, 4096, 4096, 4096), (0, 0, 256, 256, 256), (0, 0, 1, 1, 1),
+                              (0, 1, 8192, 8192, 8192), (0, 1, 100, 100, 100), (0, 1, 2048, 2048, 64),
+                              (1, 0, 64, 100352, 576), (1, 0, 256, 1000, 2304)]:
+        s = x.xtc_default_schedule(op, dt, M, N, K)
+        assert x.xtc_sched_check(op, dt, s) == 0, (op, dt, M, N, K, s)
+    with pytest.raises(x.XtcError):
+        x.xtc_default_schedule(1, 1, 64, 64, 64)
+
+
+def test_no_hip_error_recorded_by_validation(x):
+    assert x.xtc_last_hip_error() == 0
+    assert x.xtc_conv_max_k() >= 576

@@ -1,0 +1,291 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Exact cases (small-integer inputs, identity, all-ones, rank-1, conv delta)
+must match bit for bit; random uniform inputs must be within the relative
+Frobenius tolerance (1e-5 fp32, 1e-2 bf16 inputs) over every output, or over
+4096 seeded sampled outputs at the full benchmark sizes (the same default
+schedule and launch that bench.py times).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import xtc_inputs as xi
+from _helpers import assert_parity, say, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def x():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2512_16512_amd as mod  # raises ImportError if libxtc.so is missing
+    return mod
+
+
+def _bits(a):
+    return xi.f32_to_bf16_bits(a)
+
+
+def _prep(A, B, dtype):
+    """Host operands for the oracle and the device, for dtype f32 / bf16."""
+    if dtype == "bf16":
+        A, B = _bits(A), _bits(B)
+    return A, B
+
+
+def _run_mm(x, A, B, sched=None):
+    import torch
+    a, b = to_dev(A), to_dev(B)
+    c = torch.full((A.shape[0], B.shape[1]), float("nan"), dtype=torch.float32, device="cuda")
+    x.matmul(a, b, out=c, sched=sched)
+    return to_host(c)
+
+
+# ------------------------------------------------------------ full configs
+
+
+@pytest.mark.parametrize("ci", [0, 1, 2, 3])
+def test_matmul_config_parity(x, ci):
+    import torch
+    cfg = xi.CONFIGS[ci]
+    say("matmul config", ci, cfg["name"])
+    A, B = xi.matmul_inputs(cfg)
+    a, b = to_dev(A), to_dev(B)
+    c = x.matmul(a, b)
+    if cfg["check"] == "full":
+        ref = oracle.matmul(A, B)
+        got = to_host(c)
+    else:
+        i, j = xi.sample_indices_matmul(xi.seed(ci, 3), cfg["M"], cfg["N"], cfg["check"])
+        ref = oracle.matmul_sampled(A, B, i, j)
+        got = to_host(c[torch.from_numpy(i).cuda(), torch.from_numpy(j).cuda()])
+    err = assert_parity(got, ref, cfg["dtype"], cfg["name"])
+    say("  rel_fro = %.3e" % err)
+
+
+def test_conv_config_parity(x):
+    import torch
+    cfg = xi.CONFIGS[4]
+    say("conv config", cfg["name"])
+    X, W = xi.conv_inputs(cfg)
+    y = x.conv2d_nchw(to_dev(X), to_dev(W), stride=cfg["stride"], pad=cfg["pad"])
+    F = xi.sample_indices_flat(xi.seed(4, 3), y.numel(), cfg["check"])
+    ref = oracle.conv2d_sampled(X, W, F, stride=cfg["stride"], pad=cfg["pad"])
+    got = to_host(y.reshape(-1)[torch.from_numpy(F).cuda()])
+    err = assert_parity(got, ref, "f32", cfg["name"])
+    say("  rel_fro = %.3e" % err)
+
+
+# ------------------------------------------------- exact, every instance
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("M,N,K", [(300, 200, 150), (128, 256, 64), (65, 33, 1000)])
+def test_small_int_exact_every_instance(x, dtype, M, N, K):
+    A, B = _prep(xi.small_int_f32(7, (M, K)), xi.small_int_f32(8, (K, N)), dtype)
+    ref = oracle.matmul(A, B)
+    code = x.XTC_F32 if dtype == "f32" else x.XTC_BF16
+    for s in x.xtc_sched_list(x.XTC_OP_MATMUL, code):
+        for raster, xcd in ((0, 1), (8, 1), (1, 0)):
+            s.raster, s.xcd_remap = raster, xcd
+            say(dtype, (M, N, K), s)
+            got = _run_mm(x, A, B, sched=s)
+            assert np.array_equal(got, ref), "%s %s: not bit-exact" % (dtype, s)
+
+
+def test_conv_small_int_exact_every_instance(x):
+    X = xi.small_int_f32(9, (3, 5, 13, 11))
+    W = xi.small_int_f32(10, (7, 5, 3, 3))
+    ref = oracle.conv2d(X, W, stride=1, pad=1)
+    for s in x.xtc_sched_list(x.XTC_OP_CONV2D, x.XTC_F32):
+        for raster in (0, 1, 8):
+            s.raster = raster
+            say("conv exact", s)
+            got = to_host(x.conv2d_nchw(to_dev(X), to_dev(W), stride=1, pad=1, sched=s))
+            assert np.array_equal(got, ref), "conv %s: not bit-exact" % s
+
+
+# ---------------------------------------------------------- closed forms
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_identity(x, dtype):
+    M, K, N = 200, 200, 333
+    B = xi.uniform_f32(11, (K, N))
+    I = np.eye(K, dtype=np.float32)
+    Ih, Bh = _prep(I, B, dtype)
+    say("identity", dtype)
+    got = _run_mm(x, Ih, Bh)
+    Bval = xi.bf16_bits_to_f32(Bh) if dtype == "bf16" else B
+    assert np.array_equal(got, Bval)
+    A = xi.uniform_f32(12, (M, K))
+    Ah, Ih2 = _prep(A, I, dtype)
+    got = _run_mm(x, Ah, Ih2)
+    Aval = xi.bf16_bits_to_f32(Ah) if dtype == "bf16" else A
+    assert np.array_equal(got, Aval)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("K", [1, 7, 1000, 4097])
+def test_all_ones_gives_K(x, dtype, K):
+    A, B = _prep(np.ones((130, K), np.float32), np.ones((K, 70), np.float32), dtype)
+    say("ones", dtype, K)
+    assert np.all(_run_mm(x, A, B) == float(K))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rank_one(x, dtype):
+    rng = np.random.default_rng(3)
+    K = 333
+    u = rng.integers(-3, 4, size=150).astype(np.float32)
+    w = rng.integers(-3, 4, size=170).astype(np.float32)
+    A, B = _prep(np.repeat(u[:, None], K, 1), np.repeat(w[None, :], K, 0), dtype)
+    say("rank-1", dtype)
+    assert np.array_equal(_run_mm(x, A, B), K * np.outer(u, w).astype(np.float64))
+
+
+@pytest.mark.parametrize("name", ["matmul_2x2.json", "matmul_3x3.json"])
+def test_hand_worked(x, name):
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", name)))
+    A = np.array(g["A"], np.float32)
+    B = np.array(g["B"], np.float32)
+    for dtype in ("f32", "bf16"):
+        Ah, Bh = _prep(A, B, dtype)
+        assert np.array_equal(_run_mm(x, Ah, Bh), np.array(g["C"], np.float64))
+
+
+# -------------------------------------------------------------- edges
+
+
+def _ragged_cases():
+    sizes = [1, 2, 15, 16, 17, 31, 33, 63, 65, 127, 129, 255, 257, 258, 1000]
+    rng = np.random.default_rng(2024)
+    cases = [(s, s, s) for s in sizes]
+    cases += [tuple(int(v) for v in rng.choice(sizes, 3)) for _ in range(30)]
+    return cases
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_ragged_sweep_exact(x, dtype):
+    for (M, N, K) in _ragged_cases():
+        A, B = _prep(xi.small_int_f32(M * 7 + K, (M, K)), xi.small_int_f32(N * 5 + K, (K, N)), dtype)
+        say("ragged", dtype, (M, N, K))
+        got = _run_mm(x, A, B)
+        assert np.array_equal(got, oracle.matmul(A, B)), (dtype, M, N, K)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_paper_running_example_shape(x, dtype):
+    # The paper's running example (Fig. 2): I=256, J=258, K=512, row-major;
+    # J = 258 leaves a 2-column remainder and makes ldb unaligned to 16 bytes.
+    A, B = _prep(xi.uniform_f32(13, (256, 512)), xi.uniform_f32(14, (512, 258)), dtype)
+    say("paper shape 256x258x512", dtype)
+    got = _run_mm(x, A, B)
+    assert_parity(got, oracle.matmul(A, B), dtype, "256x258x512")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("pad", [(5, 3, 7), (8, 8, 8)])
+def test_leading_dims_with_guard_bands(x, dtype, pad):
+    import torch
+    M, N, K = 190, 140, 77
+    pa, pb, pc = pad
+    A, B = _prep(xi.small_int_f32(15, (M, K)), xi.small_int_f32(16, (K, N)), dtype)
+    ref = oracle.matmul(A, B)
+    nan_bits = np.uint16(0x7FC0)
+    fill = nan_bits if dtype == "bf16" else np.float32(np.nan)
+    Ap = np.full((M, K + pa), fill, dtype=A.dtype); Ap[:, :K] = A
+    Bp = np.full((K, N + pb), fill, dtype=B.dtype); Bp[:, :N] = B
+    ad, bd = to_dev(Ap), to_dev(Bp)
+    c = torch.full((M, N + pc), -123.0, dtype=torch.float32, device="cuda")
+    say("leading dims", dtype, pad)
+    code = x.XTC_F32 if dtype == "f32" else x.XTC_BF16
+    st = x.xtc_matmul(M, N, K, ad.data_ptr(), K + pa, bd.data_ptr(), N + pb, c.data_ptr(), N + pc,
+                      code, None, torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    got = to_host(c)
+    assert np.array_equal(got[:, :N], ref), "logical C wrong or NaN leaked from the guard bands"
+    assert np.all(got[:, N:] == -123.0), "columns N..ldc of C were written"
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_K_zero_writes_zeros_and_empty_is_noop(x, dtype):
+    import torch
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    a = torch.empty((50, 0), dtype=tdt, device="cuda")
+    b = torch.empty((0, 70), dtype=tdt, device="cuda")
+    c = torch.full((50, 70), 5.0, device="cuda")
+    x.matmul(a, b, out=c)
+    assert np.all(to_host(c) == 0.0)
+    e = torch.full((0, 70), 5.0, device="cuda")
+    x.matmul(torch.empty((0, 3), dtype=tdt, device="cuda"), torch.ones((3, 70), dtype=tdt, device="cuda"), out=e)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_deterministic_and_raster_independent(x, dtype):
+    import torch
+    A, B = _prep(xi.uniform_f32(17, (1000, 1000)), xi.uniform_f32(18, (1000, 1000)), dtype)
+    a, b = to_dev(A), to_dev(B)
+    code = x.XTC_F32 if dtype == "f32" else x.XTC_BF16
+    s = x.xtc_default_schedule(x.XTC_OP_MATMUL, code, 1000, 1000, 1000)
+    say("determinism", dtype, s)
+    first = to_host(x.matmul(a, b, sched=s))
+    for rep in range(20):
+        assert np.array_equal(to_host(x.matmul(a, b, sched=s)), first), "run %d differs" % rep
+    for raster, xcd in ((0, 0), (1, 1), (3, 1), (16, 0)):
+        s.raster, s.xcd_remap = raster, xcd
+        assert np.array_equal(to_host(x.matmul(a, b, sched=s)), first), (raster, xcd)
+    assert_parity(first, oracle.matmul(A, B), dtype, "1000^3")
+
+
+# --------------------------------------------------------------- conv
+
+
+def _conv(x, X, W, stride, pad, sched=None):
+    return to_host(x.conv2d_nchw(to_dev(X), to_dev(W), stride=stride, pad=pad, sched=sched))
+
+
+def test_conv_delta_is_identity(x):
+    C = 6
+    X = xi.uniform_f32(19, (2, C, 17, 19))
+    W = np.zeros((C, C, 3, 3), np.float32)
+    for c in range(C):
+        W[c, c, 1, 1] = 1.0
+    say("conv delta")
+    assert np.array_equal(_conv(x, X, W, 1, 1), X.astype(np.float64))
+
+
+def test_conv_all_ones_borders(x):
+    C = 64
+    say("conv ones")
+    Y = _conv(x, np.ones((2, C, 9, 10), np.float32), np.ones((3, C, 3, 3), np.float32), 1, 1)
+    assert np.all(Y[:, :, 0, 0] == 4 * C) and np.all(Y[:, :, -1, -1] == 4 * C)
+    assert np.all(Y[:, :, 0, 1:-1] == 6 * C) and np.all(Y[:, :, 1:-1, 0] == 6 * C)
+    assert np.all(Y[:, :, 1:-1, 1:-1] == 9 * C)
+
+
+@pytest.mark.parametrize("name", ["conv_3x3_ones.json", "conv_orientation.json", "conv_stride2.json"])
+def test_conv_hand_worked(x, name):
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", name)))
+    Y = _conv(x, np.array(g["X"], np.float32), np.array(g["W"], np.float32), g["stride"], g["pad"])
+    assert np.array_equal(Y, np.array(g["Y"], np.float64))
+
+
+@pytest.mark.parametrize("N,C,H,W,OC,R,S,stride,pad", [
+    (2, 3, 64, 64, 16, 7, 7, 2, 3),      # the paper's 7x7 stride-2 conv, reduced spatially
+    (3, 4, 10, 9, 5, 1, 1, 1, 0),        # 1x1
+    (2, 8, 15, 13, 70, 3, 3, 2, 1),      # OC > 64: two tile rows, ragged
+    (1, 16, 30, 30, 32, 5, 5, 1, 2),
+    (4, 64, 14, 14, 64, 3, 3, 1, 1),
+])
+def test_conv_shapes_vs_oracle(x, N, C, H, W, OC, R, S, stride, pad):
+    X = xi.uniform_f32(20, (N, C, H, W))
+    Wt = xi.uniform_f32(21, (OC, C, R, S))
+    say("conv", (N, C, H, W, OC, R, S, stride, pad))
+    got = _conv(x, X, Wt, stride, pad)
+    assert_parity(got, oracle.conv2d(X, Wt, stride=stride, pad=pad), "f32", "conv")
