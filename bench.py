@@ -210,6 +210,9 @@ def main():
     ap.add_argument("--only", default="fp32,bf16,conv")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 256 MiB device-to-device copy (the reference kernel "
+                         "for scaling the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -222,6 +225,16 @@ def main():
         print("bench.py needs a GPU (torch.cuda.is_available() is False)", file=sys.stderr)
         sys.exit(1)
     import paper_2512_16512_amd  # noqa: F401  (fails loudly if libxtc.so is missing)
+
+    if args.calibrate_copy:
+        n = 64 << 20  # fp32 elements: 256 MiB read + 256 MiB written per copy
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        ms = time_launches(lambda: dst.copy_(src), args.steps, args.warmup)
+        print(json.dumps({"calibration": "copy", "bytes_read": 4 * n, "bytes_written": 4 * n,
+                          "ms_per_copy": round(ms, 4),
+                          "GBps": round(8 * n / (ms * 1e-3) / 1e9, 1)}), flush=True)
+        return
 
     kinds = [k.strip() for k in args.only.split(",") if k.strip()]
     results, summaries = {}, {}

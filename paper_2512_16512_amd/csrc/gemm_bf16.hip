@@ -243,6 +243,331 @@ gemm_bf16_kernel(GemmArgs p) {
         }
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS variant.  Global tiles are copied straight into LDS with
+// buffer_load_dwordx4 ... lds (16 bytes per lane, no register staging), into
+// a ring of STAGES LDS buffers, so STAGES-1 K-steps are in flight while the
+// matrix cores work on the oldest one.  One such instruction writes 1 KiB of
+// LDS contiguously (lane i at byte 16*i of the block), so the layout is
+// chosen on the global side: each 16-byte chunk of a tile row is placed at
+// slot = chunk ^ swizzle(row) of its LDS row, which keeps the fragment reads
+// free of bank conflicts with unpadded rows.  Out-of-range chunks (rows >= M
+// or >= K, columns >= N or k >= K) are fetched through a buffer offset past
+// the end of the buffer, which the hardware returns as zero: this variant
+// needs K and N to be multiples of 8 and 16-byte aligned rows, and otherwise
+// the register-staged kernel above runs.
+
+// A rows hold CA = BK/8 chunks of 16 bytes; chunk c of row m sits at slot
+// c ^ swz_a(m).  Two ways of reading an A fragment (16 bytes per lane) are
+// compiled (AMODE):
+//  0: one ds_read_b128.  On gfx950 a wave-wide ds_read_b128 keeps the LDS
+//     busy for 16 cycles even when it is contiguous; the swizzle keeps it at
+//     that floor (unswizzled 64-byte rows cost 3.5 times more).
+//  1: two ds_read_b64, each conflict-free (2 LDS cycles): rows sharing a
+//     256-byte window are spread over the CA slots, and the first read of
+//     lanes whose row has bit 4 set takes the high half of the chunk, so the
+//     32 lanes served together hit 32 distinct 8-byte bank pairs.  A per-lane
+//     select restores k order.
+template <int CA, int AMODE>
+__device__ __forceinline__ int swz_a(int row) {
+    if constexpr (AMODE == 1) return CA == 4 ? (row >> 2) & 3 : (row >> 1) & 7;
+    return CA == 4 ? ((row >> 1) ^ (row >> 3)) & 3 : (row ^ (row >> 3)) & 7;
+}
+
+// B rows (one k each) are read four consecutive rows at a time by the
+// transpose reads; XOR values {0, 6, 10, 12} on k % 4 spread those rows over
+// distinct bank groups.
+__device__ __forceinline__ int swz_b(int k) { return ((k & 1) * 6) ^ ((k & 2) * 5); }
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// Buffer resource of a raw (unstructured) buffer: base address, no stride,
+// `bytes` records; word 3 holds the gfx9 default data format.  Reads at an
+// offset with offset + size > bytes return zero.
+__device__ __forceinline__ i32x4 make_rsrc(const void *base, int bytes) {
+    const unsigned long long a = reinterpret_cast<unsigned long long>(base);
+    i32x4 r;
+    r[0] = (int)(unsigned)(a & 0xffffffffull);
+    r[1] = (int)(unsigned)((a >> 32) & 0xffffull);
+    r[2] = bytes;
+    r[3] = 0x00020000;
+    return r;
+}
+
+// One 16-byte-per-lane copy global -> LDS: lane i's 16 bytes at buffer offset
+// `voffset` land at LDS byte `lds_addr + 16*i`.  Written as inline assembly
+// so that the compiler does not treat every later LDS read as dependent on
+// every copy in flight (the completion of these copies is tracked with
+// explicit vmcnt waits instead).  M0 carries the LDS base; one wait state
+// separates its write from the copy.
+__device__ __forceinline__ void dma16(const i32x4 &rsrc, unsigned lds_addr, int voffset) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds"
+        :
+        : "s"(lds_addr), "v"(voffset), "s"(rsrc)
+        : "memory", "m0");
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ unsigned lds_address(const void *p) {
+    return (unsigned)reinterpret_cast<unsigned long long>(
+        (const __attribute__((address_space(3))) unsigned char *)(p));
+}
+
+// s_waitcnt on the vector-memory counter only (gfx9 encoding: vmcnt in bits
+// 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+constexpr int kOOB = 0x7FFFFFF0;  // buffer offset beyond any operand (spans are < 2^31 - 1)
+
+template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES>
+struct Bf16DmaCfg {
+    static constexpr int NWM = BM / WM, NWN = BN / WN;
+    static constexpr int NWAVES = NWM * NWN;
+    static constexpr int NT = NWAVES * 64;
+    static constexpr int TM = WM / MI, TN = WN / MI;
+    typedef Bf16Mfma<MI> MF;
+    static constexpr int KG = MF::KG;
+    static constexpr int KCH = 8 * KG;                  // k per MFMA
+    static constexpr int NS = BK / KCH;                 // MFMA k-steps per LDS stage
+    static constexpr int RA = BK * 2, CA = BK / 8;      // A row bytes / chunks
+    static constexpr int RB = BN * 2, CB = BN / 8;      // B row bytes / chunks
+    static constexpr int A_BYTES = BM * RA, B_BYTES = BK * RB;
+    static constexpr int A_BLOCKS = A_BYTES / 1024, B_BLOCKS = B_BYTES / 1024;
+    static constexpr int A_PER_WAVE = A_BLOCKS / NWAVES, B_PER_WAVE = B_BLOCKS / NWAVES;
+    static constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;   // copies per wave per stage
+    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+    static_assert(A_PER_WAVE * NWAVES == A_BLOCKS && B_PER_WAVE * NWAVES == B_BLOCKS,
+                  "tiles must split into whole 1 KiB blocks per wave");
+    static_assert(CA == 4 || CA == 8, "block_k must be 32 or 64");
+    static_assert(CB >= 16 && RB <= 1024, "block_n must be 128..512");
+    static_assert(BK % KCH == 0 && NS % 2 == 0, "an even number of MFMA k-steps per stage");
+    static_assert(STAGES >= 2 && STAGES * STAGE_BYTES <= 160 * 1024, "LDS budget");
+    static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
+};
+
+// Main loop (per workgroup):
+//   prologue: copy stages 0 .. STAGES-1 into the ring; wait for stage 0;
+//             read the fragments of its first k-step.
+//   stage kt: for each k-step s, read the fragments of step s+1 (two
+//             register sets alternate) while the MFMAs of step s run.  The
+//             fragments of the last step are read before the barrier that
+//             publishes stage kt+1, so that barrier also frees slot kt
+//             (no wave reads it any more); the copy of stage kt+STAGES into
+//             that slot and the first fragment reads of stage kt+1 are
+//             issued before the last step's MFMAs.
+// SCHED = 1 adds scheduling-group barriers that interleave one or two LDS
+// reads with each MFMA.
+template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES, int AMODE, int SCHED>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+gemm_bf16_dma_kernel(GemmArgs p) {
+    typedef Bf16DmaCfg<BM, BN, BK, WM, WN, MI, STAGES> G;
+    typedef typename G::MF MF;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * G::STAGE_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / G::NWN, wn = wave % G::NWN;
+    const int lrow = lane % MI, lgrp = lane / MI;
+
+    const int M = p.M, N = p.N, K = p.K;
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const i32x4 ra = make_rsrc(p.A, ((M - 1) * p.lda + K) * 2);
+    const i32x4 rb = make_rsrc(p.B, ((K - 1) * p.ldb + N) * 2);
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const unsigned smem_base = lds_address(smem);
+
+    // Per-lane source coordinates of this wave's copy blocks (fixed over K).
+    int a_row[G::A_PER_WAVE], a_col[G::A_PER_WAVE];
+#pragma unroll
+    for (int q = 0; q < G::A_PER_WAVE; ++q) {
+        const int blk = wave * G::A_PER_WAVE + q;
+        const int row = blk * (1024 / G::RA) + lane / G::CA;
+        a_row[q] = row;
+        a_col[q] = 8 * ((lane % G::CA) ^ swz_a<G::CA, AMODE>(row));
+    }
+    int b_row[G::B_PER_WAVE], b_col[G::B_PER_WAVE];
+#pragma unroll
+    for (int q = 0; q < G::B_PER_WAVE; ++q) {
+        const int blk = wave * G::B_PER_WAVE + q;
+        const int row = blk * (1024 / G::RB) + lane / G::CB;
+        b_row[q] = row;
+        b_col[q] = 8 * ((lane % G::CB) ^ swz_b(row));
+    }
+
+    auto issue = [&](int kt, int st) {
+        const int k0 = kt * BK;
+        const unsigned base = smem_base + st * G::STAGE_BYTES;
+#pragma unroll
+        for (int q = 0; q < G::A_PER_WAVE; ++q) {
+            const int gm = m0 + a_row[q], gk = k0 + a_col[q];
+            const int off = (gm < M && gk < K) ? (gm * p.lda + gk) * 2 : kOOB;
+            dma16(ra, base + (wave_u * G::A_PER_WAVE + q) * 1024, off);
+        }
+#pragma unroll
+        for (int q = 0; q < G::B_PER_WAVE; ++q) {
+            const int gk = k0 + b_row[q], gn = n0 + b_col[q];
+            const int off = (gk < K && gn < N) ? (gk * p.ldb + gn) * 2 : kOOB;
+            dma16(rb, base + G::A_BYTES + (wave_u * G::B_PER_WAVE + q) * 1024, off);
+        }
+    };
+
+    // Fragment addressing inside one stage (byte offsets).
+    int a_off[G::TM], a_swz[G::TM], a_first[G::TM];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i) {
+        const int row = wm * WM + i * MI + lrow;
+        a_off[i] = row * G::RA;
+        a_swz[i] = swz_a<G::CA, AMODE>(row);
+        // AMODE 1: 8-byte half read first (row bit 4 for 32-row instruction
+        // tiles; for 16-row tiles the k-groups sharing a cycle differ in lgrp)
+        a_first[i] = MI == 32 ? (row >> 4) & 1 : (lgrp & 1);
+    }
+    const int rsub = (lane & 15) >> 2;  // transpose-read row inside the group of four
+    const int bsw = swz_b(rsub);        // the rows this lane reads are all == rsub (mod 4)
+    int b_chunk[G::TN];
+#pragma unroll
+    for (int j = 0; j < G::TN; ++j)
+        b_chunk[j] = (((wn * WN + j * MI + (lrow & ~15) + 4 * (lane & 3)) >> 3) ^ bsw) * 16 +
+                     8 * (lane & 1);
+
+    typename MF::acc_t acc[G::TM][G::TN];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[i][j][r] = 0.f;
+
+    u16x8 af[2][G::TM], bfr[2][G::TN];
+
+    auto load_frags = [&](int st, int step, int buf) {
+        const unsigned char *As = smem + st * G::STAGE_BYTES;
+        const unsigned char *Bs = As + G::A_BYTES;
+        const int kk = step * G::KCH;
+#pragma unroll
+        for (int i = 0; i < G::TM; ++i) {
+            const int slot = ((kk >> 3) + lgrp) ^ a_swz[i];
+            if constexpr (AMODE == 1) {
+                // The offsets go through an empty asm so that the compiler
+                // cannot see that reads of neighbouring fragments are a
+                // constant distance apart: it would fuse them into
+                // ds_read2st64_b64, which costs as much LDS time as b128.
+                int o1 = a_off[i] + slot * 16 + 8 * a_first[i];
+                int o2 = a_off[i] + slot * 16 + 8 - 8 * a_first[i];
+                asm volatile("" : "+v"(o1), "+v"(o2));
+                const u16x4 first = *reinterpret_cast<const u16x4 *>(As + o1);
+                const u16x4 second = *reinterpret_cast<const u16x4 *>(As + o2);
+                const u16x4 lo = a_first[i] ? second : first;
+                const u16x4 hi = a_first[i] ? first : second;
+                af[buf][i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+            } else {
+                af[buf][i] = *reinterpret_cast<const u16x8 *>(As + a_off[i] + slot * 16);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j) {
+            const unsigned char *q0 = Bs + (kk + 8 * lgrp + rsub) * G::RB + b_chunk[j];
+            const u16x4 lo = ds_read_tr16(reinterpret_cast<const unsigned short *>(q0));
+            const u16x4 hi = ds_read_tr16(reinterpret_cast<const unsigned short *>(q0 + 4 * G::RB));
+            bfr[buf][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+    };
+
+    auto mfmas = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+            for (int j = 0; j < G::TN; ++j) acc[i][j] = MF::mma(af[buf][i], bfr[buf][j], acc[i][j]);
+    };
+
+    // One MFMA followed by its share of the next step's LDS reads.
+    auto interleave = [&]() {
+        if constexpr (SCHED == 1) {
+            constexpr int NM = G::TM * G::TN;
+            constexpr int ND = (AMODE == 1 ? 2 : 1) * G::TM + 2 * G::TN;
+            constexpr int PER = (ND + NM - 1) / NM;
+#pragma unroll
+            for (int m = 0; m < NM; ++m) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+                if (m * PER < ND) __builtin_amdgcn_sched_group_barrier(0x100, PER, 0);  // DS read
+            }
+        }
+    };
+
+    const int KT = (K + BK - 1) / BK;
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s)
+        if (s < KT) issue(s, s);
+    if (KT > 0) {
+        if (STAGES - 1 < KT)
+            wait_vmcnt<(STAGES - 1) * G::LOADS>();
+        else
+            wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        load_frags(0, 0, 0);
+    }
+    for (int kt = 0; kt < KT; ++kt) {
+        const int st = kt % STAGES;
+#pragma unroll
+        for (int s = 0; s + 1 < G::NS; ++s) {
+            load_frags(st, s + 1, (s + 1) & 1);
+            mfmas(s & 1);
+            interleave();
+        }
+        if (kt + 1 < KT) {
+            // this wave's copies of stage kt+1 have landed, then everyone's
+            if (kt + STAGES - 1 < KT)
+                wait_vmcnt<(STAGES - 2) * G::LOADS>();
+            else
+                wait_vmcnt<0>();
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            if (kt + STAGES < KT) issue(kt + STAGES, st);
+            load_frags((kt + 1) % STAGES, 0, 0);
+        }
+        mfmas((G::NS - 1) & 1);
+        interleave();
+    }
+
+    float *__restrict__ C = p.C;
+    const int ldc = p.ldc;
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j) {
+            const int col = n0 + wn * WN + j * MI + lrow;
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
+                if (row < M && col < N) C[row * ldc + col] = acc[i][j][r];
+            }
+        }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES, int AMODE, int SCHED>
+hipError_t launch_bf16_dma(const GemmArgs &a, hipStream_t s) {
+    typedef Bf16DmaCfg<BM, BN, BK, WM, WN, MI, STAGES> G;
+    const unsigned tiles = (unsigned)(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
+    GemmArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(
+        reinterpret_cast<const void *>(
+            &gemm_bf16_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES, AMODE, SCHED>),
+        dim3(tiles), dim3(G::NT), kargs, 0, s);
+}
+
 template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD, bool VEC>
 hipError_t launch_bf16(const GemmArgs &a, hipStream_t s) {
     typedef GemmBf16Cfg<BM, BN, BK, WM, WN, MI, PAD, VEC> G;
@@ -258,14 +583,31 @@ hipError_t launch_bf16(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), 2, PAD, 0),               \
             &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, true>,                                  \
-            &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, false>                                  \
+            &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, false>, false                           \
+    }
+
+// Direct-to-LDS ring (lds_pad = -1: swizzled, unpadded LDS rows), b128 A
+// reads, MFMA / LDS-read interleaving.  The fallback for unaligned or
+// non-16-byte-granular operands is the register-staged kernel with the same
+// tiles.
+#define XTC_BF16_DMA_INSTANCE(BM, BN, BK, WM, WN, MI, STAGES)                                 \
+    GemmInstance {                                                                            \
+        make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), STAGES, -1, 0),           \
+            &launch_bf16_dma<BM, BN, BK, WM, WN, MI, STAGES, 0, 1>,                           \
+            &launch_bf16<BM, BN, BK, WM, WN, MI, 8, false>, true                              \
     }
 
 const GemmInstance kBf16Instances[] = {
-    XTC_BF16_INSTANCE(256, 256, 64, 128, 64, 32, 8),  // default for large problems
+    XTC_BF16_DMA_INSTANCE(256, 256, 64, 128, 64, 32, 2),  // default for large problems
+    XTC_BF16_DMA_INSTANCE(256, 256, 64, 128, 128, 32, 2), // 4 waves of 128x128
+    XTC_BF16_DMA_INSTANCE(256, 256, 32, 128, 64, 32, 4),
+    XTC_BF16_DMA_INSTANCE(256, 128, 32, 128, 64, 32, 3),
+    XTC_BF16_DMA_INSTANCE(128, 128, 32, 64, 64, 32, 4),   // medium problems
+    XTC_BF16_DMA_INSTANCE(128, 128, 64, 64, 64, 16, 2),
+    XTC_BF16_INSTANCE(256, 256, 64, 128, 64, 32, 8),
     XTC_BF16_INSTANCE(128, 128, 64, 64, 64, 32, 8),
-    XTC_BF16_INSTANCE(64, 64, 64, 32, 32, 32, 8),     // small problems
-    XTC_BF16_INSTANCE(128, 128, 64, 64, 64, 16, 8),   // 16x16x32 instruction tile
+    XTC_BF16_INSTANCE(64, 64, 64, 32, 32, 32, 8),         // small problems
+    XTC_BF16_INSTANCE(128, 128, 64, 64, 64, 16, 8),       // 16x16x32 instruction tile
 };
 
 }  // namespace

@@ -192,7 +192,7 @@ hipError_t launch_f32(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 2 : 4), 2, PAD, 0),                 \
             &launch_f32<BM, BN, BK, WM, WN, MI, PAD, true>,                                   \
-            &launch_f32<BM, BN, BK, WM, WN, MI, PAD, false>                                   \
+            &launch_f32<BM, BN, BK, WM, WN, MI, PAD, false>, false                            \
     }
 
 const GemmInstance kF32Instances[] = {

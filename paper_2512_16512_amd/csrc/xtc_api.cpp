@@ -132,19 +132,22 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     }
     if (dt == XTC_F32) {
         // Large tiles once they still give at least one tile per CU.
-        if (tiles(128, 128) >= cus)
+        if (tiles(256, 128) >= 2 * cus)
+            *out = make_sched(256, 128, 16, 128, 64, 32, 32, 2, 2, 4, 0);
+        else if (tiles(128, 128) >= cus)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, 4, 0);
         else
             *out = make_sched(64, 64, 32, 32, 32, 32, 32, 2, 2, 4, 0);
     } else {
         if (tiles(256, 256) >= cus)
-            *out = make_sched(256, 256, 64, 128, 64, 32, 32, 16, 2, 8, 0);
+            *out = make_sched(256, 256, 64, 128, 64, 32, 32, 16, 2, -1, 0);
         else if (tiles(128, 128) >= cus)
-            *out = make_sched(128, 128, 64, 64, 64, 32, 32, 16, 2, 8, 0);
+            *out = make_sched(128, 128, 32, 64, 64, 32, 32, 16, 4, -1, 0);
         else
             *out = make_sched(64, 64, 64, 32, 32, 32, 32, 16, 2, 8, 0);
     }
-    out->raster = tiles(out->block_m, out->block_n) >= 64 ? 8 : 0;
+    const int64_t t = tiles(out->block_m, out->block_n);
+    out->raster = dt == XTC_BF16 && t >= 4 * cus ? 16 : (t >= 64 ? 8 : 0);
     return XTC_OK;
 }
 
@@ -204,8 +207,9 @@ xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     a.M = (int)M; a.N = (int)N; a.K = (int)K;
     a.A = A; a.lda = (int)lda; a.B = B; a.ldb = (int)ldb; a.C = C; a.ldc = (int)ldc;
     a.raster = s.raster; a.xcd_remap = s.xcd_remap;
-    const bool vec = K == 0 || (aligned16(A) && aligned16(B) && (lda * elt) % 16 == 0 &&
-                                (ldb * elt) % 16 == 0);
+    bool vec = K == 0 || (aligned16(A) && aligned16(B) && (lda * elt) % 16 == 0 &&
+                          (ldb * elt) % 16 == 0);
+    if (inst->vec_whole_chunks && ((K * elt) % 16 != 0 || (N * elt) % 16 != 0)) vec = false;
     const GemmLaunch fn = vec ? inst->vec_launch : inst->any_launch;
     return hip_status(fn(a, static_cast<hipStream_t>(stream)));
 }

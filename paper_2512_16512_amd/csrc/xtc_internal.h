@@ -40,12 +40,14 @@ using GemmLaunch = hipError_t (*)(const GemmArgs &, hipStream_t);
 using ConvLaunch = hipError_t (*)(const ConvArgs &, hipStream_t);
 
 // One compiled kernel instance.  `vec_launch` requires 16-byte aligned
-// operand rows (base pointers and leading dimensions); `any_launch` has no
-// alignment requirement.
+// operand rows (base pointers and leading dimensions) and, when
+// `vec_whole_chunks` is set, also K and N to be multiples of 16 bytes of
+// elements; `any_launch` has no such requirement.
 struct GemmInstance {
     xtc_sched sched;
     GemmLaunch vec_launch;
     GemmLaunch any_launch;
+    bool vec_whole_chunks;
 };
 
 struct ConvInstance {

@@ -83,7 +83,7 @@ def test_conv_config_parity(x):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("M,N,K", [(300, 200, 150), (128, 256, 64), (65, 33, 1000)])
+@pytest.mark.parametrize("M,N,K", [(300, 200, 150), (128, 256, 64), (65, 33, 1000), (300, 264, 200), (520, 136, 1032)])
 def test_small_int_exact_every_instance(x, dtype, M, N, K):
     A, B = _prep(xi.small_int_f32(7, (M, K)), xi.small_int_f32(8, (K, N)), dtype)
     ref = oracle.matmul(A, B)
