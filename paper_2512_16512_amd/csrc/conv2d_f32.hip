@@ -16,6 +16,7 @@
 // mapping k to (ic*H*W + kh*W + kw, kh, kw), so the gather needs no integer
 // division in the main loop: an element (k, q) is X[base(q) + off(k)] when
 // 0 <= ih0(q) + kh < H and 0 <= iw0(q) + kw < W, else zero.
+#include "lds_dma.h"
 #include "mfma_f32.h"
 #include "tile_map.h"
 #include "xtc_internal.h"
@@ -195,6 +196,288 @@ conv2d_f32_kernel(ConvArgs p) {
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD>
+hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Direct-to-LDS variant.  Both operands reach LDS through buffer loads with
+// the `lds` modifier, into a ring of STAGES buffers:
+//  - weights (the GEMM A operand, row-major [OC][C*R*S]): 16-byte copies of
+//    128-byte tile rows, chunk c of row m stored at slot c ^ ((m ^ m>>3) & 7);
+//  - the im2col gather (the B operand): one 4-byte copy per lane per k row,
+//    64 consecutive output pixels per instruction.  Each lane's buffer
+//    offset is base(pixel) + off(k) from the k-offset table, or an offset
+//    past the end of X when the tap falls in the zero padding (or the pixel
+//    or k is past the end), which the hardware returns as zero: the padding
+//    predicate costs no branch and no register staging.  Inside each group
+//    of 64 columns, rows whose (k >> 2) is odd store column c at c ^ 32, so
+//    the two halves of a wave (k rows 4 apart in the MFMA operand layout)
+//    read different bank halves.
+// The main loop is the same ping-pong as the bf16 direct-to-LDS GEMM: the
+// fragments of k-step s+1 are read while the MFMAs of step s run, and the
+// barrier that publishes stage kt+1 is taken inside the last step of stage
+// kt.  Needs C*R*S to be a multiple of 4 and a 16-byte aligned weight
+// pointer (else the register-staged kernel above runs).
+template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+struct ConvDmaCfg {
+    static constexpr int MI = 32;
+    static constexpr int NWM = BM / WM, NWN = BN / WN;
+    static constexpr int NWAVES = NWM * NWN;
+    static constexpr int NT = NWAVES * 64;
+    static constexpr int TM = WM / MI, TN = WN / MI;
+    typedef F32Mfma<MI> MF;
+    static constexpr int KCH = 4 * MF::KG;          // k per fragment set (8)
+    static constexpr int NS = BK / KCH;             // fragment sets per stage
+    static constexpr int RA = BK * 4, CA = BK / 4;  // weight tile row bytes / chunks
+    static constexpr int A_BYTES = BM * RA;
+    static constexpr int A_BLOCKS = A_BYTES / 1024;
+    static constexpr int A_PER_WAVE = A_BLOCKS / NWAVES;
+    static constexpr int NCG = BN / 64;             // 64-column groups of the B tile
+    static constexpr int B_BYTES = BK * BN * 4;
+    static constexpr int B_INSTR = BK * NCG;
+    static constexpr int B_PER_WAVE = B_INSTR / NWAVES;
+    static constexpr int ROWS_PER_WAVE = BK / NWAVES;
+    static constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;
+    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+    static_assert(CA == 8, "block_k must be 32 (128-byte weight rows)");
+    static_assert(A_PER_WAVE * NWAVES == A_BLOCKS && A_PER_WAVE >= 1, "weight tile split");
+    static_assert(B_PER_WAVE * NWAVES == B_INSTR, "gather split");
+    static_assert(ROWS_PER_WAVE % 8 == 0, "each wave gathers whole groups of 8 k rows");
+    static_assert(NS % 2 == 0, "an even number of fragment sets per stage");
+    static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
+};
+
+template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+conv2d_f32_dma_kernel(ConvArgs p) {
+    typedef ConvDmaCfg<BM, BN, BK, WM, WN, STAGES> G;
+    typedef typename G::MF MF;
+    constexpr int MI = G::MI;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * G::STAGE_BYTES];
+    extern __shared__ int2 ktab[];  // [K]: {ic*H*W + kh*W + kw, kh | kw << 16}
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / G::NWN, wn = wave % G::NWN;
+    const int lrow = lane % MI, lgrp = lane / MI;
+
+    const int C = p.C, H = p.H, Wd = p.W, R = p.R, S = p.S;
+    const int OC = p.OC, OW = p.OW, OHW = p.OH * p.OW;
+    const int M = OC, N = p.Nb * OHW, K = C * R * S;
+    const int HW = H * Wd;
+
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const int RS = R * S;
+    for (int k = tid; k < K; k += G::NT) {
+        const int ic = k / RS, rem = k - ic * RS;
+        const int kh = rem / S, kw = rem - kh * S;
+        ktab[k] = make_int2(ic * HW + kh * Wd + kw, kh | (kw << 16));
+    }
+
+    const i32x4 rw = make_rsrc(p.Wt, OC * K * 4);
+    const i32x4 rx = make_rsrc(p.X, p.Nb * C * HW * 4);
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const unsigned smem_base = lds_address(smem);
+
+    // Weight copies: this wave's blocks of 8 rows x 8 chunks.
+    int a_row[G::A_PER_WAVE], a_col[G::A_PER_WAVE];
+#pragma unroll
+    for (int q = 0; q < G::A_PER_WAVE; ++q) {
+        const int row = (wave * G::A_PER_WAVE + q) * 8 + lane / 8;
+        a_row[q] = row;
+        a_col[q] = 4 * ((lane & 7) ^ ((row ^ (row >> 3)) & 7));
+    }
+
+    // Gather: this wave owns k rows [wave*ROWS_PER_WAVE, ...) of every
+    // stage, all NCG column groups.  Its lane covers pixel column
+    // cg*64 + (lane ^ 32x) with x = (k row >> 2) & 1.
+    int g_xb[G::NCG][2], g_ih[G::NCG][2], g_iw[G::NCG][2];
+#pragma unroll
+    for (int cg = 0; cg < G::NCG; ++cg)
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            const int q = n0 + cg * 64 + (lane ^ (32 * x));
+            if (q < N) {
+                const int img = q / OHW, pix = q - img * OHW;
+                const int oh = pix / OW, ow = pix - oh * OW;
+                g_ih[cg][x] = oh * p.sh - p.ph;
+                g_iw[cg][x] = ow * p.sw - p.pw;
+                g_xb[cg][x] = img * C * HW + g_ih[cg][x] * Wd + g_iw[cg][x];
+            } else {
+                g_ih[cg][x] = -(1 << 28);  // fails the row-range test: reads zero
+                g_iw[cg][x] = 0;
+                g_xb[cg][x] = 0;
+            }
+        }
+
+    __syncthreads();  // k-offset table ready
+
+    // Copies of one stage are split in two halves: prepare() computes every
+    // buffer offset (k-offset table reads and predicates, no LDS writes), so
+    // it can run early, overlapped with the MFMAs of the current stage;
+    // fire() issues the copies once the target slot is free.
+    int offA[G::A_PER_WAVE], offB[G::ROWS_PER_WAVE][G::NCG];
+    auto prepare = [&](int kt) {
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int q = 0; q < G::A_PER_WAVE; ++q) {
+            const int gm = m0 + a_row[q], gk = k0 + a_col[q];
+            offA[q] = (gm < M && gk < K) ? (gm * K + gk) * 4 : kOOB;
+        }
+        int2 t[G::ROWS_PER_WAVE];
+#pragma unroll
+        for (int r = 0; r < G::ROWS_PER_WAVE; ++r) {
+            const int k = k0 + wave_u * G::ROWS_PER_WAVE + r;
+            t[r] = ktab[k < K ? k : K - 1];
+        }
+#pragma unroll
+        for (int r = 0; r < G::ROWS_PER_WAVE; ++r) {
+            const int k = k0 + wave_u * G::ROWS_PER_WAVE + r;
+            const int kh = t[r].y & 0xffff, kw = t[r].y >> 16;
+            const int x = (r >> 2) & 1;  // == (k row >> 2) & 1 since ROWS_PER_WAVE % 8 == 0
+#pragma unroll
+            for (int cg = 0; cg < G::NCG; ++cg) {
+                const int ih = g_ih[cg][x] + kh, iw = g_iw[cg][x] + kw;
+                const bool ok = k < K && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)Wd;
+                offB[r][cg] = ok ? (g_xb[cg][x] + t[r].x) * 4 : kOOB;
+            }
+        }
+    };
+    auto fire = [&](int st) {
+        const unsigned base = smem_base + st * G::STAGE_BYTES;
+#pragma unroll
+        for (int q = 0; q < G::A_PER_WAVE; ++q)
+            dma16(rw, base + (wave_u * G::A_PER_WAVE + q) * 1024, offA[q]);
+#pragma unroll
+        for (int r = 0; r < G::ROWS_PER_WAVE; ++r)
+#pragma unroll
+            for (int cg = 0; cg < G::NCG; ++cg)
+                dma4(rx, base + G::A_BYTES + ((wave_u * G::ROWS_PER_WAVE + r) * BN + cg * 64) * 4,
+                     offB[r][cg]);
+    };
+
+    // Fragment addressing (byte offsets inside a stage).
+    int a_off[G::TM], a_swz[G::TM];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i) {
+        const int row = wm * WM + i * MI + lrow;
+        a_off[i] = row * G::RA;
+        a_swz[i] = (row ^ (row >> 3)) & 7;
+    }
+    // B: row kk + 4*lgrp + s has (row >> 2) & 1 == lgrp & 1 for kk % 8 == 0.
+    int b_off[G::TN];
+#pragma unroll
+    for (int j = 0; j < G::TN; ++j)
+        b_off[j] = (4 * lgrp * BN + ((wn * WN + j * MI + lrow) ^ (32 * (lgrp & 1)))) * 4;
+
+    typename MF::acc_t acc[G::TM][G::TN];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[i][j][r] = 0.f;
+
+    f32x4 af[2][G::TM];
+    float bfr[2][G::TN][4];
+
+    auto load_frags = [&](int st, int step, int buf) {
+        const unsigned char *As = smem + st * G::STAGE_BYTES;
+        const unsigned char *Bs = As + G::A_BYTES;
+        const int kk = step * G::KCH;
+#pragma unroll
+        for (int i = 0; i < G::TM; ++i) {
+            const int slot = ((kk >> 2) + lgrp) ^ a_swz[i];
+            af[buf][i] = *reinterpret_cast<const f32x4 *>(As + a_off[i] + slot * 16);
+        }
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+                bfr[buf][j][s] = *reinterpret_cast<const float *>(Bs + (kk + s) * BN * 4 + b_off[j]);
+    };
+
+    auto mfmas = [&](int buf) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < G::TN; ++j)
+                    acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
+    };
+
+    const int KT = (K + BK - 1) / BK;
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s)
+        if (s < KT) {
+            prepare(s);
+            fire(s);
+        }
+    if (STAGES - 1 < KT)
+        wait_vmcnt<(STAGES - 1) * G::LOADS>();
+    else
+        wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    load_frags(0, 0, 0);
+    for (int kt = 0; kt < KT; ++kt) {
+        const int st = kt % STAGES;
+        const bool refill = kt + STAGES < KT;
+        if (refill) prepare(kt + STAGES);
+#pragma unroll
+        for (int s = 0; s + 1 < G::NS; ++s) {
+            load_frags(st, s + 1, (s + 1) & 1);
+            mfmas(s & 1);
+        }
+        if (kt + 1 < KT) {
+            if (kt + STAGES - 1 < KT)
+                wait_vmcnt<(STAGES - 2) * G::LOADS>();
+            else
+                wait_vmcnt<0>();
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            if (refill) fire(st);
+            load_frags((kt + 1) % STAGES, 0, 0);
+        }
+        mfmas((G::NS - 1) & 1);
+    }
+
+    float *__restrict__ Y = p.Y;
+#pragma unroll
+    for (int j = 0; j < G::TN; ++j) {
+        const int col = n0 + wn * WN + j * MI + lrow;
+        if (col >= N) continue;
+        const int img = col / OHW, pix = col - img * OHW;
+        float *ybase = Y + img * OC * OHW + pix;
+#pragma unroll
+        for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int oc = m0 + wm * WM + i * MI + MF::row(lane, r);
+                if (oc < M) ybase[oc * OHW] = acc[i][j][r];
+            }
+    }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+hipError_t launch_conv_f32_dma(const ConvArgs &a, hipStream_t s) {
+    typedef ConvDmaCfg<BM, BN, BK, WM, WN, STAGES> G;
+    const int M = a.OC, N = a.Nb * a.OH * a.OW, K = a.C * a.R * a.S;
+    const unsigned tiles = (unsigned)(((M + BM - 1) / BM) * ((N + BN - 1) / BN));
+    const size_t dyn = (size_t)K * sizeof(int2);
+    if (K % 4 != 0 || (reinterpret_cast<uintptr_t>(a.Wt) & 15) != 0)
+        return launch_conv_f32<BM, BN, BK, WM, WN, 32, 4>(a, s);  // register-staged fallback
+    ConvArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_dma_kernel<BM, BN, BK, WM, WN, STAGES>),
+                           dim3(tiles), dim3(G::NT), kargs, dyn, s);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD>
 hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
     const int M = a.OC, N = a.Nb * a.OH * a.OW, K = a.C * a.R * a.S;
     const unsigned tiles = (unsigned)(((M + BM - 1) / BM) * ((N + BN - 1) / BN));
@@ -213,8 +496,17 @@ hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
             &launch_conv_f32<BM, BN, BK, WM, WN, MI, PAD>                                     \
     }
 
+#define XTC_CONV_DMA_INSTANCE(BM, BN, BK, WM, WN, STAGES)                                     \
+    ConvInstance {                                                                            \
+        make_sched(BM, BN, BK, WM, WN, 32, 32, 2, STAGES, -1, 0),                             \
+            &launch_conv_f32_dma<BM, BN, BK, WM, WN, STAGES>                                  \
+    }
+
 const ConvInstance kConvInstances[] = {
-    XTC_CONV_INSTANCE(64, 128, 32, 32, 64, 32, 4),   // default: OC = 64 in one tile row
+    XTC_CONV_DMA_INSTANCE(64, 128, 32, 32, 64, 3),   // default: OC = 64 in one tile row
+    XTC_CONV_DMA_INSTANCE(64, 64, 32, 32, 32, 4),
+    XTC_CONV_DMA_INSTANCE(128, 128, 32, 64, 64, 3),
+    XTC_CONV_INSTANCE(64, 128, 32, 32, 64, 32, 4),
     XTC_CONV_INSTANCE(64, 64, 32, 32, 32, 32, 4),
     XTC_CONV_INSTANCE(128, 128, 32, 64, 64, 32, 4),
     XTC_CONV_INSTANCE(64, 128, 32, 32, 64, 16, 4),

@@ -125,8 +125,8 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     if (op == XTC_OP_CONV2D) {
         if (dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
-        *out = make_sched(64, 128, 32, 32, 64, 32, 32, 2, 2, 4, 0);
-        if (M > 64) *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, 4, 0);
+        *out = make_sched(64, 128, 32, 32, 64, 32, 32, 2, 3, -1, 0);
+        if (M > 64) *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 3, -1, 0);
         out->raster = 0;
         return XTC_OK;
     }

@@ -96,16 +96,24 @@ def test_small_int_exact_every_instance(x, dtype, M, N, K):
             assert np.array_equal(got, ref), "%s %s: not bit-exact" % (dtype, s)
 
 
-def test_conv_small_int_exact_every_instance(x):
-    X = xi.small_int_f32(9, (3, 5, 13, 11))
-    W = xi.small_int_f32(10, (7, 5, 3, 3))
-    ref = oracle.conv2d(X, W, stride=1, pad=1)
+@pytest.mark.parametrize("shape", [
+    (3, 5, 13, 11, 7, 3, 3, 1, 1),      # C*R*S = 45: not a multiple of 4 (register-staged path)
+    (2, 8, 17, 19, 70, 3, 3, 1, 1),     # C*R*S = 72, OC = 70: ragged weight rows, pixel tail
+    (3, 16, 9, 14, 64, 3, 3, 2, 1),     # stride 2
+    (1, 4, 20, 20, 33, 5, 5, 1, 2),     # 5x5, pad 2, C*R*S = 100
+    (2, 12, 11, 7, 16, 1, 1, 1, 0),     # 1x1
+])
+def test_conv_small_int_exact_every_instance(x, shape):
+    N, C, H, W_, OC, R, S, stride, pad = shape
+    X = xi.small_int_f32(9, (N, C, H, W_))
+    W = xi.small_int_f32(10, (OC, C, R, S))
+    ref = oracle.conv2d(X, W, stride=stride, pad=pad)
     for s in x.xtc_sched_list(x.XTC_OP_CONV2D, x.XTC_F32):
         for raster in (0, 1, 8):
             s.raster = raster
-            say("conv exact", s)
-            got = to_host(x.conv2d_nchw(to_dev(X), to_dev(W), stride=1, pad=1, sched=s))
-            assert np.array_equal(got, ref), "conv %s: not bit-exact" % s
+            say("conv exact", shape, s)
+            got = to_host(x.conv2d_nchw(to_dev(X), to_dev(W), stride=stride, pad=pad, sched=s))
+            assert np.array_equal(got, ref), "conv %s %s: not bit-exact" % (shape, s)
 
 
 # ---------------------------------------------------------- closed forms
