@@ -97,8 +97,19 @@ def run_matmul(cfg, steps, warmup):
     a, b = to_dev(A), to_dev(B)
     c = torch.empty((cfg["M"], cfg["N"]), dtype=torch.float32, device="cuda")
     code = xtc.XTC_F32 if cfg["dtype"] == "f32" else xtc.XTC_BF16
-    sched = xtc.xtc_default_schedule(xtc.XTC_OP_MATMUL, code, cfg["M"], cfg["N"], cfg["K"])
-    ms = time_launches(lambda: xtc.matmul(a, b, out=c, sched=sched), steps, warmup)
+    M, N, K = cfg["M"], cfg["N"], cfg["K"]
+    sched = xtc.xtc_default_schedule(xtc.XTC_OP_MATMUL, code, M, N, K)
+    # the C ABI called with pre-marshalled arguments, so that host-side
+    # launch cost stays well below the kernel time
+    args = (M, N, K, a.data_ptr(), K, b.data_ptr(), N, c.data_ptr(), N, code, sched,
+            torch.cuda.current_stream().cuda_stream)
+
+    def launch():
+        st = xtc.xtc_matmul(*args)
+        if st != xtc.XTC_OK:
+            raise xtc.XtcError(st, "xtc_matmul")
+
+    ms = time_launches(launch, steps, warmup)
     flops = 2.0 * cfg["M"] * cfg["N"] * cfg["K"]
     elt = 4 if cfg["dtype"] == "f32" else 2
     alg_bytes = elt * (cfg["M"] * cfg["K"] + cfg["K"] * cfg["N"]) + 4 * cfg["M"] * cfg["N"]
@@ -118,8 +129,17 @@ def run_conv(cfg, steps, warmup):
     y = torch.empty((cfg["N"], cfg["OC"], OH, OW), dtype=torch.float32, device="cuda")
     Mg, Ng, Kg = cfg["OC"], cfg["N"] * OH * OW, cfg["C"] * cfg["R"] * cfg["S"]
     sched = xtc.xtc_default_schedule(xtc.XTC_OP_CONV2D, xtc.XTC_F32, Mg, Ng, Kg)
-    ms = time_launches(lambda: xtc.conv2d_nchw(xd, wd, cfg["stride"], cfg["pad"], out=y, sched=sched),
-                       steps, warmup)
+    st_, pd = cfg["stride"], cfg["pad"]
+    args = (cfg["N"], cfg["C"], cfg["H"], cfg["W"], cfg["OC"], cfg["R"], cfg["S"], st_, st_, pd, pd,
+            xd.data_ptr(), wd.data_ptr(), y.data_ptr(), xtc.XTC_F32, sched,
+            torch.cuda.current_stream().cuda_stream)
+
+    def launch():
+        st = xtc.xtc_conv2d_nchw(*args)
+        if st != xtc.XTC_OK:
+            raise xtc.XtcError(st, "xtc_conv2d_nchw")
+
+    ms = time_launches(launch, steps, warmup)
     F = xi.sample_indices_flat(xi.seed(cfg["index"], 3), y.numel(), cfg["check"])
     sampled = y.reshape(-1)[torch.from_numpy(F).cuda()].cpu().numpy()
     alg_bytes = 4 * (X.size + W.size + y.numel())

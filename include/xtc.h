@@ -81,9 +81,15 @@ typedef enum {
  *  xcd_remap     1: renumber workgroups so that each of the 8 XCDs (which
  *                receive workgroups round-robin and each own an L2) works on
  *                one contiguous band of the tile order; 0: hardware order.
+ *  k_order       conv2d only (0 for matmul): order of the reduction over
+ *                (ic, kh, kw).  0: channel-major, k = (ic*R + kh)*S + kw (the
+ *                OIHW weight layout); 1: tap-major, k = (kh*S + kw)*C + ic
+ *                (needs C % 32 == 0, else the channel-major kernel with the
+ *                same tiles runs).  Results differ only by rounding order.
  *
- * block_*, wave_*, mfma_*, lds_stages, lds_pad and unroll_k select a compiled
- * kernel instance; raster and xcd_remap are run-time choices valid for all.
+ * block_*, wave_*, mfma_*, lds_stages, lds_pad, unroll_k and k_order select a
+ * compiled kernel instance; raster and xcd_remap are run-time choices valid
+ * for all.
  */
 typedef struct {
     int32_t size;
@@ -95,6 +101,7 @@ typedef struct {
     int32_t unroll_k;
     int32_t raster;
     int32_t xcd_remap;
+    int32_t k_order;
 } xtc_sched;
 
 /*
@@ -134,7 +141,7 @@ xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K,
  * input positions outside [0,H) x [0,W) contributing zero, with
  *   OH = (H + 2*pad_h - R)/stride_h + 1,  OW = (W + 2*pad_w - S)/stride_w + 1.
  * Computed as an implicit GEMM (no im2col buffer): M = OC, N = N*OH*OW,
- * K = C*R*S with k = (ic*R + kh)*S + kw.
+ * K = C*R*S, reduced in the order the schedule's k_order selects.
  *
  *  X    device, NCHW contiguous fp32.      Wt  device, OIHW contiguous fp32.
  *  Y    device, N x OC x OH x OW contiguous fp32 (overwritten).

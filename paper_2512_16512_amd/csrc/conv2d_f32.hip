@@ -477,6 +477,273 @@ hipError_t launch_conv_f32_dma(const ConvArgs &a, hipStream_t s) {
                            dim3(tiles), dim3(G::NT), kargs, dyn, s);
 }
 
+// ---------------------------------------------------------------------------
+// Tap-major direct-to-LDS variant (channel counts that are a multiple of 32).
+// The reduction runs over k = (kh*S + kw)*C + ic instead of (ic*R + kh)*S +
+// kw: the sum is the same up to rounding order.  One LDS stage then holds 32
+// consecutive input channels of a single tap (kh, kw), so
+//  - the padding predicate and the pixel part of the input offset are the
+//    same for every channel of the stage: each lane computes them once per
+//    stage, and the channel goes into the copy's scalar offset (soffset), so
+//    a gather copy needs no vector arithmetic at all;
+//  - the weights of the stage, W[oc][ic0 .. ic0+31][kh][kw], are a strided
+//    gather too: each lane owns one (oc, channel) slot of the weight tile for
+//    the whole K loop (a fixed vector offset) and the stage moves the scalar
+//    offset to (ic0*R*S + tap).
+// LDS layouts and fragment reads are those of the variant above (128-byte
+// weight rows with 16-byte chunks swizzled by (m ^ m>>3) & 7; 64-column
+// pixel groups with columns XOR 32 on rows whose (k >> 2) is odd).
+template <int BM, int BN, int WM, int WN, int STAGES>
+struct ConvTapCfg {
+    static constexpr int BK = 32, MI = 32;
+    static constexpr int NWM = BM / WM, NWN = BN / WN;
+    static constexpr int NWAVES = NWM * NWN;
+    static constexpr int NT = NWAVES * 64;
+    static constexpr int TM = WM / MI, TN = WN / MI;
+    typedef F32Mfma<MI> MF;
+    static constexpr int KCH = 4 * MF::KG;
+    static constexpr int NS = BK / KCH;
+    static constexpr int RA = BK * 4;                // weight tile row bytes
+    static constexpr int A_BYTES = BM * RA;
+    static constexpr int A_INSTR = BM * BK / 64;     // dword copies (two weight rows each)
+    static constexpr int A_PER_WAVE = A_INSTR / NWAVES;
+    static constexpr int NCG = BN / 64;
+    static constexpr int B_BYTES = BK * BN * 4;
+    static constexpr int ROWS_PER_WAVE = BK / NWAVES;
+    static constexpr int B_PER_WAVE = ROWS_PER_WAVE * NCG;
+    static constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;
+    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+    static_assert(A_PER_WAVE * NWAVES == A_INSTR && A_PER_WAVE >= 1, "weight tile split");
+    static_assert(ROWS_PER_WAVE * NWAVES == BK && ROWS_PER_WAVE >= 1, "gather split");
+    static_assert(NS % 2 == 0, "an even number of fragment sets per stage");
+    static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
+    static_assert(STAGES * STAGE_BYTES <= 160 * 1024, "LDS budget");
+};
+
+template <int BM, int BN, int WM, int WN, int STAGES>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+conv2d_f32_tap_kernel(ConvArgs p) {
+    typedef ConvTapCfg<BM, BN, WM, WN, STAGES> G;
+    typedef typename G::MF MF;
+    constexpr int MI = G::MI, BK = G::BK;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * G::STAGE_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / G::NWN, wn = wave % G::NWN;
+    const int lrow = lane % MI, lgrp = lane / MI;
+
+    const int C = p.C, H = p.H, Wd = p.W, R = p.R, S = p.S;
+    const int OC = p.OC, OW = p.OW, OHW = p.OH * p.OW;
+    const int M = OC, N = p.Nb * OHW;
+    const int HW = H * Wd, RS = R * S;
+    const int CB = C / BK;                 // channel chunks per tap
+    const int KT = RS * CB;                // LDS stages
+
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const i32x4 rw = make_rsrc(p.Wt, OC * C * RS * 4);
+    const i32x4 rx = make_rsrc(p.X, p.Nb * C * HW * 4);
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const unsigned smem_base = lds_address(smem);
+
+    // Weight copies: copy q of this wave fills tile rows 2*(wave*A_PER_WAVE+q)
+    // and +1; lane i lands at row position i % 32, i.e. chunk slot (i%32)/4
+    // holding channel chunk slot ^ swizzle(row).
+    int voffA[G::A_PER_WAVE];
+#pragma unroll
+    for (int q = 0; q < G::A_PER_WAVE; ++q) {
+        const int row = 2 * (wave * G::A_PER_WAVE + q) + lane / 32;
+        const int pos = lane % 32;
+        const int kl = 4 * ((pos >> 2) ^ ((row ^ (row >> 3)) & 7)) + (pos & 3);
+        const int oc = m0 + row;
+        voffA[q] = oc < M ? (oc * C * RS + kl * RS) * 4 : kOOB;
+    }
+
+    // Gather columns (as in the variant above).
+    int g_xb[G::NCG][2], g_ih[G::NCG][2], g_iw[G::NCG][2];
+#pragma unroll
+    for (int cg = 0; cg < G::NCG; ++cg)
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            const int q = n0 + cg * 64 + (lane ^ (32 * x));
+            if (q < N) {
+                const int img = q / OHW, pix = q - img * OHW;
+                const int oh = pix / OW, ow = pix - oh * OW;
+                g_ih[cg][x] = oh * p.sh - p.ph;
+                g_iw[cg][x] = ow * p.sw - p.pw;
+                g_xb[cg][x] = img * C * HW + g_ih[cg][x] * Wd + g_iw[cg][x];
+            } else {
+                g_ih[cg][x] = -(1 << 28);  // fails the row-range test: reads zero
+                g_iw[cg][x] = 0;
+                g_xb[cg][x] = 0;
+            }
+        }
+
+    // Stage walk: (tap, channel chunk) of the next stage to prepare.  prepare()
+    // is called once per stage, in stage order.
+    int nx_c0 = 0, nx_kh = 0, nx_kw = 0;
+    int voffB[G::NCG][2];
+    int so_a = 0, so_b = 0;
+    auto prepare = [&]() {
+        const int kh = nx_kh, kw = nx_kw, c0 = nx_c0;
+#pragma unroll
+        for (int cg = 0; cg < G::NCG; ++cg)
+#pragma unroll
+            for (int x = 0; x < 2; ++x) {
+                const int ih = g_ih[cg][x] + kh, iw = g_iw[cg][x] + kw;
+                const bool ok = (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)Wd;
+                voffB[cg][x] = ok ? (g_xb[cg][x] + kh * Wd + kw) * 4 : kOOB;
+            }
+        so_a = (c0 * RS + kh * S + kw) * 4;
+        so_b = (c0 + wave_u * G::ROWS_PER_WAVE) * HW * 4;
+        // advance to the next stage: channels, then kw, then kh
+        nx_c0 = c0 + BK;
+        if (nx_c0 == C) {
+            nx_c0 = 0;
+            nx_kw = kw + 1;
+            if (nx_kw == S) {
+                nx_kw = 0;
+                nx_kh = kh + 1;
+            }
+        }
+    };
+    auto fire = [&](int st) {
+        const unsigned base = smem_base + st * G::STAGE_BYTES;
+#pragma unroll
+        for (int q = 0; q < G::A_PER_WAVE; ++q)
+            dma4_so(rw, base + (wave_u * G::A_PER_WAVE + q) * 256, voffA[q], so_a);
+#pragma unroll
+        for (int r = 0; r < G::ROWS_PER_WAVE; ++r) {
+            // column swizzle of this k row (a constant when each wave owns a
+            // multiple of 8 rows, else a wave-uniform select)
+            const int x = ((wave_u * G::ROWS_PER_WAVE + r) >> 2) & 1;
+#pragma unroll
+            for (int cg = 0; cg < G::NCG; ++cg)
+                dma4_so(rx, base + G::A_BYTES + ((wave_u * G::ROWS_PER_WAVE + r) * BN + cg * 64) * 4,
+                        x ? voffB[cg][1] : voffB[cg][0], so_b + r * HW * 4);
+        }
+    };
+
+    int a_off[G::TM], a_swz[G::TM];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i) {
+        const int row = wm * WM + i * MI + lrow;
+        a_off[i] = row * G::RA;
+        a_swz[i] = (row ^ (row >> 3)) & 7;
+    }
+    int b_off[G::TN];
+#pragma unroll
+    for (int j = 0; j < G::TN; ++j)
+        b_off[j] = (4 * lgrp * BN + ((wn * WN + j * MI + lrow) ^ (32 * (lgrp & 1)))) * 4;
+
+    typename MF::acc_t acc[G::TM][G::TN];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[i][j][r] = 0.f;
+
+    f32x4 af[2][G::TM];
+    float bfr[2][G::TN][4];
+
+    auto load_frags = [&](int st, int step, int buf) {
+        const unsigned char *As = smem + st * G::STAGE_BYTES;
+        const unsigned char *Bs = As + G::A_BYTES;
+        const int kk = step * G::KCH;
+#pragma unroll
+        for (int i = 0; i < G::TM; ++i) {
+            const int slot = ((kk >> 2) + lgrp) ^ a_swz[i];
+            af[buf][i] = *reinterpret_cast<const f32x4 *>(As + a_off[i] + slot * 16);
+        }
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+                bfr[buf][j][s] = *reinterpret_cast<const float *>(Bs + (kk + s) * BN * 4 + b_off[j]);
+    };
+
+    auto mfmas = [&](int buf) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < G::TN; ++j)
+                    acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
+    };
+
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s)
+        if (s < KT) {
+            prepare();
+            fire(s);
+        }
+    if (STAGES - 1 < KT)
+        wait_vmcnt<(STAGES - 1) * G::LOADS>();
+    else
+        wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    load_frags(0, 0, 0);
+    for (int kt = 0; kt < KT; ++kt) {
+        const int st = kt % STAGES;
+        const bool refill = kt + STAGES < KT;
+        if (refill) prepare();
+#pragma unroll
+        for (int s = 0; s + 1 < G::NS; ++s) {
+            load_frags(st, s + 1, (s + 1) & 1);
+            mfmas(s & 1);
+        }
+        if (kt + 1 < KT) {
+            if (kt + STAGES - 1 < KT)
+                wait_vmcnt<(STAGES - 2) * G::LOADS>();
+            else
+                wait_vmcnt<0>();
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            if (refill) fire(st);
+            load_frags((kt + 1) % STAGES, 0, 0);
+        }
+        mfmas((G::NS - 1) & 1);
+    }
+
+    float *__restrict__ Y = p.Y;
+#pragma unroll
+    for (int j = 0; j < G::TN; ++j) {
+        const int col = n0 + wn * WN + j * MI + lrow;
+        if (col >= N) continue;
+        const int img = col / OHW, pix = col - img * OHW;
+        float *ybase = Y + img * OC * OHW + pix;
+#pragma unroll
+        for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int oc = m0 + wm * WM + i * MI + MF::row(lane, r);
+                if (oc < M) ybase[oc * OHW] = acc[i][j][r];
+            }
+    }
+}
+
+// Tap-major kernel when the channel count is a multiple of 32, else the
+// k-table kernel with the same tiles (which itself falls back to the
+// register-staged one when C*R*S is not a multiple of 4).
+template <int BM, int BN, int WM, int WN, int STAGES, int FALLBACK_STAGES>
+hipError_t launch_conv_f32_tap(const ConvArgs &a, hipStream_t s) {
+    typedef ConvTapCfg<BM, BN, WM, WN, STAGES> G;
+    if (a.C % G::BK != 0) return launch_conv_f32_dma<BM, BN, 32, WM, WN, FALLBACK_STAGES>(a, s);
+    const int M = a.OC, N = a.Nb * a.OH * a.OW;
+    const unsigned tiles = (unsigned)(((M + BM - 1) / BM) * ((N + BN - 1) / BN));
+    ConvArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_tap_kernel<BM, BN, WM, WN, STAGES>),
+                           dim3(tiles), dim3(G::NT), kargs, 0, s);
+}
+
 template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD>
 hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
     const int M = a.OC, N = a.Nb * a.OH * a.OW, K = a.C * a.R * a.S;
@@ -502,9 +769,20 @@ hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
             &launch_conv_f32_dma<BM, BN, BK, WM, WN, STAGES>                                  \
     }
 
+// Tap-major direct-to-LDS instances (k_order = 1).
+#define XTC_CONV_TAP_INSTANCE(BM, BN, WM, WN, STAGES, FB)                                     \
+    ConvInstance {                                                                            \
+        make_sched(BM, BN, 32, WM, WN, 32, 32, 2, STAGES, -1, 0, 1),                          \
+            &launch_conv_f32_tap<BM, BN, WM, WN, STAGES, FB>                                  \
+    }
+
 const ConvInstance kConvInstances[] = {
-    XTC_CONV_DMA_INSTANCE(64, 128, 32, 32, 64, 3),   // default: OC = 64 in one tile row
-    XTC_CONV_DMA_INSTANCE(64, 64, 32, 32, 32, 4),
+    XTC_CONV_TAP_INSTANCE(64, 256, 64, 64, 2, 2),    // default for OC <= 64
+    XTC_CONV_TAP_INSTANCE(64, 128, 32, 64, 2, 3),
+    XTC_CONV_TAP_INSTANCE(64, 64, 32, 32, 2, 4),
+    XTC_CONV_TAP_INSTANCE(128, 128, 64, 64, 2, 3),   // default for OC > 64
+    XTC_CONV_DMA_INSTANCE(64, 128, 32, 32, 64, 3),
+    XTC_CONV_DMA_INSTANCE(64, 64, 32, 32, 32, 3),
     XTC_CONV_DMA_INSTANCE(128, 128, 32, 64, 64, 3),
     XTC_CONV_INSTANCE(64, 128, 32, 32, 64, 32, 4),
     XTC_CONV_INSTANCE(64, 64, 32, 32, 32, 32, 4),

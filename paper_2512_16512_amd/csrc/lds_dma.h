@@ -68,4 +68,18 @@ __device__ __forceinline__ void dma4(const i32x4 &rsrc, unsigned lds_addr, int v
         : "memory", "m0");
 }
 
+// dma4 with a wave-uniform byte offset `soffset` added to every lane's
+// address.  A lane whose `voffset` is past the end of the buffer still reads
+// zero (the sum stays below 2^32 for soffset < 2^31 - 16).
+__device__ __forceinline__ void dma4_so(const i32x4 &rsrc, unsigned lds_addr, int voffset,
+                                        int soffset) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dword %1, %2, %3 offen lds"
+        :
+        : "s"(lds_addr), "v"(voffset), "s"(rsrc), "s"(soffset)
+        : "memory", "m0");
+}
+
 }  // namespace xtc

@@ -25,7 +25,7 @@ bool same_instance(const xtc_sched &a, const xtc_sched &b) {
     return a.block_m == b.block_m && a.block_n == b.block_n && a.block_k == b.block_k &&
            a.wave_m == b.wave_m && a.wave_n == b.wave_n && a.mfma_m == b.mfma_m &&
            a.mfma_n == b.mfma_n && a.mfma_k == b.mfma_k && a.lds_stages == b.lds_stages &&
-           a.lds_pad == b.lds_pad && (a.unroll_k == b.unroll_k || a.unroll_k == 0 || b.unroll_k == 0);
+           a.lds_pad == b.lds_pad && a.unroll_k == b.unroll_k && a.k_order == b.k_order;
 }
 
 bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -56,6 +56,8 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     if (s.lds_pad < -1 || s.lds_pad > 64) return XTC_ERR_BAD_SCHEDULE;
     if (s.unroll_k < 0) return XTC_ERR_BAD_SCHEDULE;
     if (s.raster < 0 || s.xcd_remap < 0 || s.xcd_remap > 1) return XTC_ERR_BAD_SCHEDULE;
+    if (s.k_order < 0 || s.k_order > 1 || (op == XTC_OP_MATMUL && s.k_order != 0))
+        return XTC_ERR_BAD_SCHEDULE;
     // LDS budget of the staged tiles
     const int elt = dt == XTC_F32 ? 4 : 2;
     const int pad = s.lds_pad > 0 ? s.lds_pad : 0;
@@ -125,8 +127,10 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     if (op == XTC_OP_CONV2D) {
         if (dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
-        *out = make_sched(64, 128, 32, 32, 64, 32, 32, 2, 3, -1, 0);
-        if (M > 64) *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 3, -1, 0);
+        // 64x256 tiles of 4 waves (64x64 each) with a two-stage ring: two
+        // workgroups per CU, so up to 512 tiles run in a single wave.
+        *out = make_sched(64, 256, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
+        if (M > 64) *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
         out->raster = 0;
         return XTC_OK;
     }
@@ -147,7 +151,7 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
             *out = make_sched(64, 64, 64, 32, 32, 32, 32, 16, 2, 8, 0);
     }
     const int64_t t = tiles(out->block_m, out->block_n);
-    out->raster = dt == XTC_BF16 && t >= 4 * cus ? 16 : (t >= 64 ? 8 : 0);
+    out->raster = t >= 64 ? 8 : 0;
     return XTC_OK;
 }
 

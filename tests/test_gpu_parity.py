@@ -102,6 +102,9 @@ def test_small_int_exact_every_instance(x, dtype, M, N, K):
     (3, 16, 9, 14, 64, 3, 3, 2, 1),     # stride 2
     (1, 4, 20, 20, 33, 5, 5, 1, 2),     # 5x5, pad 2, C*R*S = 100
     (2, 12, 11, 7, 16, 1, 1, 1, 0),     # 1x1
+    (2, 64, 9, 10, 40, 3, 3, 1, 1),     # C % 32 == 0: tap-major kernel, OC < 64
+    (1, 32, 12, 12, 64, 3, 3, 2, 1),    # tap-major, stride 2
+    (2, 96, 7, 7, 70, 1, 1, 1, 0),      # tap-major 1x1, three channel chunks, OC > 64
 ])
 def test_conv_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape
