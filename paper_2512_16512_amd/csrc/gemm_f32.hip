@@ -22,6 +22,7 @@
 // fetches the A values of four consecutive instructions from a k-contiguous
 // LDS row, and B (n-contiguous in LDS) is read with conflict-free
 // ds_read_b32 (lanes of one group read consecutive columns).
+#include "lds_dma.h"
 #include "mfma_f32.h"
 #include "tile_map.h"
 #include "xtc_internal.h"
@@ -188,6 +189,227 @@ hipError_t launch_f32(const GemmArgs &a, hipStream_t s) {
                            dim3(tiles), dim3(G::NT), kargs, 0, s);
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS variant: A and B tiles reach a ring of STAGES LDS buffers
+// through 16-byte buffer loads with the `lds` modifier (no register
+// staging); out-of-range chunks read as zero through the buffer range check
+// (needs K and N multiples of 4 and 16-byte aligned rows, else the
+// register-staged kernel above runs).
+//  - A rows (BK floats, 16-byte chunks) store chunk c of row m at slot
+//    c ^ swizzle(m), which keeps the wave-wide ds_read_b128 of a fragment at
+//    its 16-cycle floor;
+//  - B rows (n-contiguous) store chunk c of row k at c ^ 8*((k >> 2) & 1):
+//    a ds_read_b32 of the B operand reads rows k and k+4 with the two halves
+//    of the wave, which then land 128 bytes apart (different bank halves).
+// Main loop: the ping-pong of the bf16 direct-to-LDS kernel.
+template <int CA>
+__device__ __forceinline__ int swz_a_f32(int row) {
+    return CA == 4 ? ((row >> 1) ^ (row >> 3)) & 3 : (row ^ (row >> 3)) & 7;
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+struct F32DmaCfg {
+    static constexpr int MI = 32;
+    static constexpr int NWM = BM / WM, NWN = BN / WN;
+    static constexpr int NWAVES = NWM * NWN;
+    static constexpr int NT = NWAVES * 64;
+    static constexpr int TM = WM / MI, TN = WN / MI;
+    typedef F32Mfma<MI> MF;
+    static constexpr int KCH = 4 * MF::KG;          // k per fragment set (8)
+    static constexpr int NS = BK / KCH;
+    static constexpr int RA = BK * 4, CA = BK / 4;  // A row bytes / chunks
+    static constexpr int RB = BN * 4, CB = BN / 4;  // B row bytes / chunks
+    static constexpr int A_BYTES = BM * RA, B_BYTES = BK * RB;
+    static constexpr int A_BLOCKS = A_BYTES / 1024, B_BLOCKS = B_BYTES / 1024;
+    static constexpr int A_PER_WAVE = A_BLOCKS / NWAVES, B_PER_WAVE = B_BLOCKS / NWAVES;
+    static constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;
+    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+    static_assert(A_PER_WAVE * NWAVES == A_BLOCKS && B_PER_WAVE * NWAVES == B_BLOCKS,
+                  "tiles must split into whole 1 KiB blocks per wave");
+    static_assert(CA == 4 || CA == 8, "block_k must be 16 or 32");
+    static_assert(CB >= 16 && RB <= 1024, "block_n must be 64..256");
+    static_assert(NS % 2 == 0, "an even number of fragment sets per stage");
+    static_assert(STAGES >= 2 && STAGES * STAGE_BYTES <= 160 * 1024, "LDS budget");
+    static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
+};
+
+template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+gemm_f32_dma_kernel(GemmArgs p) {
+    typedef F32DmaCfg<BM, BN, BK, WM, WN, STAGES> G;
+    typedef typename G::MF MF;
+    constexpr int MI = G::MI;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * G::STAGE_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / G::NWN, wn = wave % G::NWN;
+    const int lrow = lane % MI, lgrp = lane / MI;
+
+    const int M = p.M, N = p.N, K = p.K;
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const i32x4 ra = make_rsrc(p.A, ((M - 1) * p.lda + K) * 4);
+    const i32x4 rb = make_rsrc(p.B, ((K - 1) * p.ldb + N) * 4);
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const unsigned smem_base = lds_address(smem);
+
+    int a_row[G::A_PER_WAVE], a_col[G::A_PER_WAVE];
+#pragma unroll
+    for (int q = 0; q < G::A_PER_WAVE; ++q) {
+        const int row = (wave * G::A_PER_WAVE + q) * (1024 / G::RA) + lane / G::CA;
+        a_row[q] = row;
+        a_col[q] = 4 * ((lane % G::CA) ^ swz_a_f32<G::CA>(row));
+    }
+    int b_row[G::B_PER_WAVE], b_col[G::B_PER_WAVE];
+#pragma unroll
+    for (int q = 0; q < G::B_PER_WAVE; ++q) {
+        const int row = (wave * G::B_PER_WAVE + q) * (1024 / G::RB) + lane / G::CB;
+        b_row[q] = row;
+        b_col[q] = 4 * ((lane % G::CB) ^ (8 * ((row >> 2) & 1)));
+    }
+
+    int offA[G::A_PER_WAVE], offB[G::B_PER_WAVE];
+    auto prepare = [&](int kt) {
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int q = 0; q < G::A_PER_WAVE; ++q) {
+            const int gm = m0 + a_row[q], gk = k0 + a_col[q];
+            offA[q] = (gm < M && gk < K) ? (gm * p.lda + gk) * 4 : kOOB;
+        }
+#pragma unroll
+        for (int q = 0; q < G::B_PER_WAVE; ++q) {
+            const int gk = k0 + b_row[q], gn = n0 + b_col[q];
+            offB[q] = (gk < K && gn < N) ? (gk * p.ldb + gn) * 4 : kOOB;
+        }
+    };
+    auto fire = [&](int st) {
+        const unsigned base = smem_base + st * G::STAGE_BYTES;
+#pragma unroll
+        for (int q = 0; q < G::A_PER_WAVE; ++q)
+            dma16(ra, base + (wave_u * G::A_PER_WAVE + q) * 1024, offA[q]);
+#pragma unroll
+        for (int q = 0; q < G::B_PER_WAVE; ++q)
+            dma16(rb, base + G::A_BYTES + (wave_u * G::B_PER_WAVE + q) * 1024, offB[q]);
+    };
+
+    int a_off[G::TM], a_swz[G::TM];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i) {
+        const int row = wm * WM + i * MI + lrow;
+        a_off[i] = row * G::RA;
+        a_swz[i] = swz_a_f32<G::CA>(row);
+    }
+    // B row kk + 4*lgrp + s has (row >> 2) & 1 == lgrp & 1 (kk % 8 == 0).
+    int b_off[G::TN];
+#pragma unroll
+    for (int j = 0; j < G::TN; ++j)
+        b_off[j] = (4 * lgrp * BN + ((wn * WN + j * MI + lrow) ^ (32 * (lgrp & 1)))) * 4;
+
+    typename MF::acc_t acc[G::TM][G::TN];
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[i][j][r] = 0.f;
+
+    f32x4 af[2][G::TM];
+    float bfr[2][G::TN][4];
+
+    auto load_frags = [&](int st, int step, int buf) {
+        const unsigned char *As = smem + st * G::STAGE_BYTES;
+        const unsigned char *Bs = As + G::A_BYTES;
+        const int kk = step * G::KCH;
+#pragma unroll
+        for (int i = 0; i < G::TM; ++i) {
+            const int slot = ((kk >> 2) + lgrp) ^ a_swz[i];
+            af[buf][i] = *reinterpret_cast<const f32x4 *>(As + a_off[i] + slot * 16);
+        }
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+                bfr[buf][j][s] = *reinterpret_cast<const float *>(Bs + (kk + s) * G::RB + b_off[j]);
+    };
+
+    auto mfmas = [&](int buf) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < G::TN; ++j)
+                    acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
+    };
+
+    const int KT = (K + BK - 1) / BK;
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s)
+        if (s < KT) {
+            prepare(s);
+            fire(s);
+        }
+    if (KT > 0) {
+        if (STAGES - 1 < KT)
+            wait_vmcnt<(STAGES - 1) * G::LOADS>();
+        else
+            wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        load_frags(0, 0, 0);
+    }
+    for (int kt = 0; kt < KT; ++kt) {
+        const int st = kt % STAGES;
+        const bool refill = kt + STAGES < KT;
+        if (refill) prepare(kt + STAGES);
+#pragma unroll
+        for (int s = 0; s + 1 < G::NS; ++s) {
+            load_frags(st, s + 1, (s + 1) & 1);
+            mfmas(s & 1);
+        }
+        if (kt + 1 < KT) {
+            if (kt + STAGES - 1 < KT)
+                wait_vmcnt<(STAGES - 2) * G::LOADS>();
+            else
+                wait_vmcnt<0>();
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            if (refill) fire(st);
+            load_frags((kt + 1) % STAGES, 0, 0);
+        }
+        mfmas((G::NS - 1) & 1);
+    }
+
+    float *__restrict__ C = p.C;
+    const int ldc = p.ldc;
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j) {
+            const int col = n0 + wn * WN + j * MI + lrow;
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
+                if (row < M && col < N) C[row * ldc + col] = acc[i][j][r];
+            }
+        }
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+hipError_t launch_f32_dma(const GemmArgs &a, hipStream_t s) {
+    typedef F32DmaCfg<BM, BN, BK, WM, WN, STAGES> G;
+    const unsigned tiles = (unsigned)(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
+    GemmArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(
+        reinterpret_cast<const void *>(&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, STAGES>),
+        dim3(tiles), dim3(G::NT), kargs, 0, s);
+}
+
 #define XTC_F32_INSTANCE(BM, BN, BK, WM, WN, MI, PAD)                                         \
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 2 : 4), 2, PAD, 0),                 \
@@ -195,7 +417,19 @@ hipError_t launch_f32(const GemmArgs &a, hipStream_t s) {
             &launch_f32<BM, BN, BK, WM, WN, MI, PAD, false>, false                            \
     }
 
+// Direct-to-LDS ring (lds_pad = -1); register-staged fallback, same tiles.
+#define XTC_F32_DMA_INSTANCE(BM, BN, BK, WM, WN, STAGES)                                      \
+    GemmInstance {                                                                            \
+        make_sched(BM, BN, BK, WM, WN, 32, 32, 2, STAGES, -1, 0),                             \
+            &launch_f32_dma<BM, BN, BK, WM, WN, STAGES>,                                      \
+            &launch_f32<BM, BN, BK, WM, WN, 32, 4, false>, true                               \
+    }
+
 const GemmInstance kF32Instances[] = {
+    XTC_F32_DMA_INSTANCE(256, 128, 16, 128, 64, 3),
+    XTC_F32_DMA_INSTANCE(256, 128, 32, 128, 64, 2),
+    XTC_F32_DMA_INSTANCE(128, 128, 32, 64, 64, 2),
+    XTC_F32_DMA_INSTANCE(128, 128, 16, 64, 64, 4),
     XTC_F32_INSTANCE(128, 128, 32, 64, 64, 32, 4),   // default for large problems
     XTC_F32_INSTANCE(128, 128, 16, 64, 64, 32, 4),
     XTC_F32_INSTANCE(64, 64, 32, 32, 32, 32, 4),     // small problems: more tiles

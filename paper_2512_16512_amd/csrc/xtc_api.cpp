@@ -136,10 +136,8 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     }
     if (dt == XTC_F32) {
         // Large tiles once they still give at least one tile per CU.
-        if (tiles(256, 128) >= 2 * cus)
-            *out = make_sched(256, 128, 16, 128, 64, 32, 32, 2, 2, 4, 0);
-        else if (tiles(128, 128) >= cus)
-            *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, 4, 0);
+        if (tiles(128, 128) >= cus)
+            *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0);
         else
             *out = make_sched(64, 64, 32, 32, 32, 32, 32, 2, 2, 4, 0);
     } else {

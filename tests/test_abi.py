@@ -119,7 +119,7 @@ def _base(x, dt=0):
 
 
 @pytest.mark.parametrize("field,value", [
-    ("block_m", 96), ("block_n", 0), ("wave_m", 256), ("mfma_m", 8), ("mfma_k", 16),
+    ("block_m", 96), ("block_n", 0), ("wave_m", 512), ("mfma_m", 8), ("mfma_k", 16),
     ("lds_stages", 0), ("lds_pad", -2), ("raster", -1), ("xcd_remap", 2), ("block_k", 4),
     ("size", 12), ("k_order", 1), ("k_order", -1),
 ])
