@@ -410,41 +410,34 @@ conv2d_f32_dma_kernel(ConvArgs p) {
                     acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
     };
 
+    // Branch-free main loop (zero-fill copies past the end of K keep the
+    // number of copies in flight constant; see the GEMM kernels).
     const int KT = (K + BK - 1) / BK;
 #pragma unroll
-    for (int s = 0; s < STAGES; ++s)
-        if (s < KT) {
-            prepare(s);
-            fire(s);
-        }
-    if (STAGES - 1 < KT)
-        wait_vmcnt<(STAGES - 1) * G::LOADS>();
-    else
-        wait_vmcnt<0>();
+    for (int s = 0; s < STAGES; ++s) {
+        prepare(s);
+        fire(s);
+    }
+    wait_vmcnt<(STAGES - 1) * G::LOADS>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     load_frags(0, 0, 0);
     for (int kt = 0; kt < KT; ++kt) {
         const int st = kt % STAGES;
-        const bool refill = kt + STAGES < KT;
-        if (refill) prepare(kt + STAGES);
+        prepare(kt + STAGES);
 #pragma unroll
         for (int s = 0; s + 1 < G::NS; ++s) {
             load_frags(st, s + 1, (s + 1) & 1);
             mfmas(s & 1);
         }
-        if (kt + 1 < KT) {
-            if (kt + STAGES - 1 < KT)
-                wait_vmcnt<(STAGES - 2) * G::LOADS>();
-            else
-                wait_vmcnt<0>();
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            if (refill) fire(st);
-            load_frags((kt + 1) % STAGES, 0, 0);
-        }
+        wait_vmcnt<(STAGES - 2) * G::LOADS>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        fire(st);
+        load_frags((kt + 1) % STAGES, 0, 0);
         mfmas((G::NS - 1) & 1);
     }
+    wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
 
     float *__restrict__ Y = p.Y;
 #pragma unroll
@@ -585,21 +578,29 @@ conv2d_f32_tap_kernel(ConvArgs p) {
 
     // Stage walk: (tap, channel chunk) of the next stage to prepare.  prepare()
     // is called once per stage, in stage order.
+    // prepare(live): a stage past the end of K (live == false) copies only
+    // zeros: every vector offset out of range and the scalar offsets 0, so
+    // no address of it depends on the (then meaningless) walk state.
     int nx_c0 = 0, nx_kh = 0, nx_kw = 0;
+    int voffA_st[G::A_PER_WAVE];
     int voffB[G::NCG][2];
     int so_a = 0, so_b = 0;
-    auto prepare = [&]() {
+    bool st_live = true;
+    auto prepare = [&](bool live) {
         const int kh = nx_kh, kw = nx_kw, c0 = nx_c0;
+        st_live = live;
 #pragma unroll
         for (int cg = 0; cg < G::NCG; ++cg)
 #pragma unroll
             for (int x = 0; x < 2; ++x) {
                 const int ih = g_ih[cg][x] + kh, iw = g_iw[cg][x] + kw;
-                const bool ok = (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)Wd;
+                const bool ok = live && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)Wd;
                 voffB[cg][x] = ok ? (g_xb[cg][x] + kh * Wd + kw) * 4 : kOOB;
             }
-        so_a = (c0 * RS + kh * S + kw) * 4;
-        so_b = (c0 + wave_u * G::ROWS_PER_WAVE) * HW * 4;
+#pragma unroll
+        for (int q = 0; q < G::A_PER_WAVE; ++q) voffA_st[q] = live ? voffA[q] : kOOB;
+        so_a = live ? (c0 * RS + kh * S + kw) * 4 : 0;
+        so_b = live ? (c0 + wave_u * G::ROWS_PER_WAVE) * HW * 4 : 0;
         // advance to the next stage: channels, then kw, then kh
         nx_c0 = c0 + BK;
         if (nx_c0 == C) {
@@ -615,7 +616,7 @@ conv2d_f32_tap_kernel(ConvArgs p) {
         const unsigned base = smem_base + st * G::STAGE_BYTES;
 #pragma unroll
         for (int q = 0; q < G::A_PER_WAVE; ++q)
-            dma4_so(rw, base + (wave_u * G::A_PER_WAVE + q) * 256, voffA[q], so_a);
+            dma4_so(rw, base + (wave_u * G::A_PER_WAVE + q) * 256, voffA_st[q], so_a);
 #pragma unroll
         for (int r = 0; r < G::ROWS_PER_WAVE; ++r) {
             // column swizzle of this k row (a constant when each wave owns a
@@ -624,7 +625,7 @@ conv2d_f32_tap_kernel(ConvArgs p) {
 #pragma unroll
             for (int cg = 0; cg < G::NCG; ++cg)
                 dma4_so(rx, base + G::A_BYTES + ((wave_u * G::ROWS_PER_WAVE + r) * BN + cg * 64) * 4,
-                        x ? voffB[cg][1] : voffB[cg][0], so_b + r * HW * 4);
+                        x ? voffB[cg][1] : voffB[cg][0], st_live ? so_b + r * HW * 4 : 0);
         }
     };
 
@@ -677,40 +678,33 @@ conv2d_f32_tap_kernel(ConvArgs p) {
                     acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
     };
 
+    // Branch-free main loop (see the GEMM kernels); stages past the end are
+    // zero-fill copies.
 #pragma unroll
-    for (int s = 0; s < STAGES; ++s)
-        if (s < KT) {
-            prepare();
-            fire(s);
-        }
-    if (STAGES - 1 < KT)
-        wait_vmcnt<(STAGES - 1) * G::LOADS>();
-    else
-        wait_vmcnt<0>();
+    for (int s = 0; s < STAGES; ++s) {
+        prepare(s < KT);
+        fire(s);
+    }
+    wait_vmcnt<(STAGES - 1) * G::LOADS>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     load_frags(0, 0, 0);
     for (int kt = 0; kt < KT; ++kt) {
         const int st = kt % STAGES;
-        const bool refill = kt + STAGES < KT;
-        if (refill) prepare();
+        prepare(kt + STAGES < KT);
 #pragma unroll
         for (int s = 0; s + 1 < G::NS; ++s) {
             load_frags(st, s + 1, (s + 1) & 1);
             mfmas(s & 1);
         }
-        if (kt + 1 < KT) {
-            if (kt + STAGES - 1 < KT)
-                wait_vmcnt<(STAGES - 2) * G::LOADS>();
-            else
-                wait_vmcnt<0>();
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            if (refill) fire(st);
-            load_frags((kt + 1) % STAGES, 0, 0);
-        }
+        wait_vmcnt<(STAGES - 2) * G::LOADS>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        fire(st);
+        load_frags((kt + 1) % STAGES, 0, 0);
         mfmas((G::NS - 1) & 1);
     }
+    wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
 
     float *__restrict__ Y = p.Y;
 #pragma unroll

@@ -360,21 +360,33 @@ gemm_bf16_dma_kernel(GemmArgs p) {
         b_col[q] = 8 * ((lane % G::CB) ^ swz_b(row));
     }
 
-    auto issue = [&](int kt, int st) {
+    // Copies of one stage: prepare() computes the buffer offsets (out of
+    // range, i.e. zero fill, for a stage past the end of K), fire() issues
+    // them once the target slot is free.  Every stage index issues exactly
+    // LOADS copies per wave, so the number of copies in flight is the same in
+    // every iteration and one vmcnt value is exact throughout.
+    int offA[G::A_PER_WAVE], offB[G::B_PER_WAVE];
+    auto prepare = [&](int kt) {
         const int k0 = kt * BK;
-        const unsigned base = smem_base + st * G::STAGE_BYTES;
 #pragma unroll
         for (int q = 0; q < G::A_PER_WAVE; ++q) {
             const int gm = m0 + a_row[q], gk = k0 + a_col[q];
-            const int off = (gm < M && gk < K) ? (gm * p.lda + gk) * 2 : kOOB;
-            dma16(ra, base + (wave_u * G::A_PER_WAVE + q) * 1024, off);
+            offA[q] = (gm < M && gk < K) ? (gm * p.lda + gk) * 2 : kOOB;
         }
 #pragma unroll
         for (int q = 0; q < G::B_PER_WAVE; ++q) {
             const int gk = k0 + b_row[q], gn = n0 + b_col[q];
-            const int off = (gk < K && gn < N) ? (gk * p.ldb + gn) * 2 : kOOB;
-            dma16(rb, base + G::A_BYTES + (wave_u * G::B_PER_WAVE + q) * 1024, off);
+            offB[q] = (gk < K && gn < N) ? (gk * p.ldb + gn) * 2 : kOOB;
         }
+    };
+    auto fire = [&](int st) {
+        const unsigned base = smem_base + st * G::STAGE_BYTES;
+#pragma unroll
+        for (int q = 0; q < G::A_PER_WAVE; ++q)
+            dma16(ra, base + (wave_u * G::A_PER_WAVE + q) * 1024, offA[q]);
+#pragma unroll
+        for (int q = 0; q < G::B_PER_WAVE; ++q)
+            dma16(rb, base + G::A_BYTES + (wave_u * G::B_PER_WAVE + q) * 1024, offB[q]);
     };
 
     // Fragment addressing inside one stage (byte offsets).
@@ -460,41 +472,40 @@ gemm_bf16_dma_kernel(GemmArgs p) {
         }
     };
 
+    // The loop body is branch-free: the tail iterations copy zeros into
+    // slots nobody reads any more and read fragments they do not use, which
+    // keeps the compiler's LDS-wait analysis exact (no conservative waits at
+    // control-flow merges in front of the last k-step's MFMAs).
     const int KT = (K + BK - 1) / BK;
 #pragma unroll
-    for (int s = 0; s < STAGES; ++s)
-        if (s < KT) issue(s, s);
-    if (KT > 0) {
-        if (STAGES - 1 < KT)
-            wait_vmcnt<(STAGES - 1) * G::LOADS>();
-        else
-            wait_vmcnt<0>();
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        load_frags(0, 0, 0);
+    for (int s = 0; s < STAGES; ++s) {
+        prepare(s);
+        fire(s);
     }
+    wait_vmcnt<(STAGES - 1) * G::LOADS>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    load_frags(0, 0, 0);
     for (int kt = 0; kt < KT; ++kt) {
         const int st = kt % STAGES;
+        prepare(kt + STAGES);
 #pragma unroll
         for (int s = 0; s + 1 < G::NS; ++s) {
             load_frags(st, s + 1, (s + 1) & 1);
             mfmas(s & 1);
             interleave();
         }
-        if (kt + 1 < KT) {
-            // this wave's copies of stage kt+1 have landed, then everyone's
-            if (kt + STAGES - 1 < KT)
-                wait_vmcnt<(STAGES - 2) * G::LOADS>();
-            else
-                wait_vmcnt<0>();
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            if (kt + STAGES < KT) issue(kt + STAGES, st);
-            load_frags((kt + 1) % STAGES, 0, 0);
-        }
+        // stage kt+1 has landed (this wave's copies, then everyone's); the
+        // barrier also frees slot st, whose fragments are all in registers
+        wait_vmcnt<(STAGES - 2) * G::LOADS>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        fire(st);
+        load_frags((kt + 1) % STAGES, 0, 0);
         mfmas((G::NS - 1) & 1);
         interleave();
     }
+    wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
 
     float *__restrict__ C = p.C;
     const int ldc = p.ldc;
@@ -553,9 +564,9 @@ hipError_t launch_bf16(const GemmArgs &a, hipStream_t s) {
     }
 
 const GemmInstance kBf16Instances[] = {
-    XTC_BF16_DMA_INSTANCE(256, 256, 64, 128, 64, 32, 2),  // default for large problems
+    XTC_BF16_DMA_INSTANCE(256, 256, 32, 128, 64, 32, 4),  // default for large problems
+    XTC_BF16_DMA_INSTANCE(256, 256, 64, 128, 64, 32, 2),
     XTC_BF16_DMA_INSTANCE(256, 256, 64, 128, 128, 32, 2), // 4 waves of 128x128
-    XTC_BF16_DMA_INSTANCE(256, 256, 32, 128, 64, 32, 4),
     XTC_BF16_DMA_INSTANCE(256, 128, 32, 128, 64, 32, 3),
     XTC_BF16_DMA_INSTANCE(128, 128, 32, 64, 64, 32, 4),   // medium problems
     XTC_BF16_DMA_INSTANCE(128, 128, 64, 64, 64, 16, 2),

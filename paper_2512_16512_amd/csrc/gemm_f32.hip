@@ -346,43 +346,35 @@ gemm_f32_dma_kernel(GemmArgs p) {
                     acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
     };
 
+    // Branch-free main loop: every stage index issues LOADS copies per wave
+    // (zero-fill copies past the end of K), so one vmcnt value is exact in
+    // every iteration and the compiler's LDS waits stay tight.
     const int KT = (K + BK - 1) / BK;
 #pragma unroll
-    for (int s = 0; s < STAGES; ++s)
-        if (s < KT) {
-            prepare(s);
-            fire(s);
-        }
-    if (KT > 0) {
-        if (STAGES - 1 < KT)
-            wait_vmcnt<(STAGES - 1) * G::LOADS>();
-        else
-            wait_vmcnt<0>();
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        load_frags(0, 0, 0);
+    for (int s = 0; s < STAGES; ++s) {
+        prepare(s);
+        fire(s);
     }
+    wait_vmcnt<(STAGES - 1) * G::LOADS>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    load_frags(0, 0, 0);
     for (int kt = 0; kt < KT; ++kt) {
         const int st = kt % STAGES;
-        const bool refill = kt + STAGES < KT;
-        if (refill) prepare(kt + STAGES);
+        prepare(kt + STAGES);
 #pragma unroll
         for (int s = 0; s + 1 < G::NS; ++s) {
             load_frags(st, s + 1, (s + 1) & 1);
             mfmas(s & 1);
         }
-        if (kt + 1 < KT) {
-            if (kt + STAGES - 1 < KT)
-                wait_vmcnt<(STAGES - 2) * G::LOADS>();
-            else
-                wait_vmcnt<0>();
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            if (refill) fire(st);
-            load_frags((kt + 1) % STAGES, 0, 0);
-        }
+        wait_vmcnt<(STAGES - 2) * G::LOADS>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        fire(st);
+        load_frags((kt + 1) % STAGES, 0, 0);
         mfmas((G::NS - 1) & 1);
     }
+    wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
 
     float *__restrict__ C = p.C;
     const int ldc = p.ldc;

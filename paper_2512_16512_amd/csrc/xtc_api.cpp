@@ -142,7 +142,7 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
             *out = make_sched(64, 64, 32, 32, 32, 32, 32, 2, 2, 4, 0);
     } else {
         if (tiles(256, 256) >= cus)
-            *out = make_sched(256, 256, 64, 128, 64, 32, 32, 16, 2, -1, 0);
+            *out = make_sched(256, 256, 32, 128, 64, 32, 32, 16, 4, -1, 0);
         else if (tiles(128, 128) >= cus)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 16, 4, -1, 0);
         else
