@@ -7,12 +7,16 @@ the HIP-event time of exactly ``--steps`` launches, after ``--warmup``
 untimed ones).  The same line also reports, timed the same way, the bf16
 matmul 8192^3 (fp32 accumulate and output) and the fp32 conv2d 32x64x56x56
 -> 64, 3x3, stride 1, pad 1 as an implicit GEMM, each with its fraction of
-the MI355X matrix-core peak, and the fp64 CPU oracle timed on the host cores
-on a bounded sample of the headline workload (``cpu_baseline``), which also
-checks sampled outputs of every timed launch against the oracle.
+the MI355X matrix-core peak; the paper's other, smaller workloads (matmuls
+1024^3, [512,128]x[128,1024], matmul+relu [256,128]x[128,1024], 256x258x512,
+and the 7x7 stride-2 conv2d 3 -> 16 channels at 224x224), timed as replays of
+a HIP graph of launches; and the fp64 CPU oracle timed on the host cores on a
+bounded sample of the headline workload (``cpu_baseline``), which also checks
+sampled outputs of every timed launch (every output of the small workloads)
+against the oracle.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--only fp32,bf16,conv]
-                       [--no-cpu-baseline]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+                       [--only fp32,bf16,conv,paper] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -147,6 +151,86 @@ def run_conv(cfg, steps, warmup):
                 F=F, sampled=sampled, gemm=(Mg, Ng, Kg))
 
 
+def _paper_launcher(xtc, cfg):
+    """(launch(stream), output tensor, gemm extents, schedule) for one of the
+    paper's other workloads, the C ABI called with pre-marshalled arguments."""
+    import torch
+    if cfg["op"] == "conv2d":
+        X, W = xi.conv_inputs(cfg)
+        xd, wd = to_dev(X), to_dev(W)
+        OH, OW = xi.conv_out_hw(cfg["H"], cfg["W"], cfg["R"], cfg["S"], cfg["stride"],
+                                cfg["stride"], cfg["pad"], cfg["pad"])
+        y = torch.empty((cfg["N"], cfg["OC"], OH, OW), dtype=torch.float32, device="cuda")
+        Mg, Ng, Kg = cfg["OC"], cfg["N"] * OH * OW, cfg["C"] * cfg["R"] * cfg["S"]
+        sched = xtc.xtc_default_schedule(xtc.XTC_OP_CONV2D, xtc.XTC_F32, Mg, Ng, Kg)
+        st_, pd = cfg["stride"], cfg["pad"]
+        pre = (cfg["N"], cfg["C"], cfg["H"], cfg["W"], cfg["OC"], cfg["R"], cfg["S"], st_, st_, pd,
+               pd, xd.data_ptr(), wd.data_ptr(), y.data_ptr(), xtc.XTC_F32, sched)
+
+        def launch(stream):
+            st = xtc.xtc_conv2d_nchw(*pre, stream)
+            if st != xtc.XTC_OK:
+                raise xtc.XtcError(st, "xtc_conv2d_nchw")
+        keep = (xd, wd)
+        alg = 4 * (X.size + W.size + y.numel())
+        return launch, y, (Mg, Ng, Kg), sched, alg, keep
+    A, B = xi.matmul_inputs(cfg)
+    a, b = to_dev(A), to_dev(B)
+    M, N, K = cfg["M"], cfg["N"], cfg["K"]
+    c = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    code = xtc.XTC_F32 if cfg["dtype"] == "f32" else xtc.XTC_BF16
+    sched = xtc.xtc_default_schedule(xtc.XTC_OP_MATMUL, code, M, N, K)
+    fn = xtc.xtc_matmul_relu if cfg["op"] == "matmul_relu" else xtc.xtc_matmul
+    pre = (M, N, K, a.data_ptr(), K, b.data_ptr(), N, c.data_ptr(), N, code, sched)
+
+    def launch(stream):
+        st = fn(*pre, stream)
+        if st != xtc.XTC_OK:
+            raise xtc.XtcError(st, fn.__name__)
+    elt = 4 if cfg["dtype"] == "f32" else 2
+    alg = elt * (M * K + K * N) + 4 * M * N
+    return launch, c, (M, N, K), sched, alg, (a, b)
+
+
+def run_paper(cfg, steps, warmup, per_graph=50):
+    """One of the paper's small workloads.  A launch lasts a few microseconds,
+    less than a host-side launch through ctypes, so ``per_graph`` launches are
+    captured in one HIP graph and the graph is replayed: ``steps`` timed
+    replays after ``warmup`` untimed ones, between HIP events on the replay
+    stream.  The graph's output is checked bit for bit against an eager launch
+    (the kernels are deterministic) after two replays separated by eager
+    refills of the output."""
+    import torch
+    import paper_2512_16512_amd as xtc
+    launch, out, (Mg, Ng, Kg), sched, alg, keep = _paper_launcher(xtc, cfg)
+    cur = torch.cuda.current_stream()
+    launch(cur.cuda_stream)
+    torch.cuda.synchronize()
+    eager = out.clone()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(cur)
+    with torch.cuda.stream(side):
+        launch(side.cuda_stream)
+    cur.wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        cs = torch.cuda.current_stream().cuda_stream
+        for _ in range(per_graph):
+            launch(cs)
+    replay_ok = True
+    for _ in range(2):
+        out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        replay_ok = replay_ok and bool(torch.equal(out, eager))
+    ms = time_launches(g.replay, steps, warmup) / per_graph
+    flops = 2.0 * Mg * Ng * Kg
+    return dict(ms=ms, flops=flops, alg_bytes=alg, sched=repr(sched), out=out.cpu().numpy(),
+                replay_ok=replay_ok, keep=keep)
+
+
 def summary(kind, cfg, r, workload):
     tflops = r["flops"] / (r["ms"] * 1e-3) / 1e12
     traffic = measured_traffic(kind, workload)
@@ -212,6 +296,26 @@ def cpu_baseline_leg(results, budget_s: float):
     return out
 
 
+def paper_parity(paper):
+    """Every output of each of the paper's workloads against the oracle."""
+    import oracle
+    out = {}
+    for key, v in paper.items():
+        cfg, r = v["cfg"], v["r"]
+        if cfg["op"] == "conv2d":
+            X, W = xi.conv_inputs(cfg)
+            ref = oracle.conv2d(X, W, stride=cfg["stride"], pad=cfg["pad"])
+        else:
+            A, B = xi.matmul_inputs(cfg)
+            ref = oracle.matmul(A, B)
+            if cfg["op"] == "matmul_relu":
+                ref = oracle.relu(ref)
+        err = oracle.rel_fro(r["out"], ref)
+        out[key] = {"rel_fro": float("%.3e" % err), "tol": 1e-5, "samples": int(ref.size),
+                    "ok": bool(err <= 1e-5 and r["replay_ok"])}
+    return out
+
+
 def _cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -227,7 +331,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--only", default="fp32,bf16,conv")
+    ap.add_argument("--only", default="fp32,bf16,conv,paper")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -274,6 +378,22 @@ def main():
         summaries["conv"] = summary("conv", cfg, results["conv"], "conv2d_f32_n32c64h56w56_oc64_r3s3")
         print("# conv: %.4f ms/launch" % results["conv"]["ms"], file=sys.stderr, flush=True)
 
+    paper = {}
+    if "paper" in kinds:
+        for cfg in xi.PAPER_WORKLOADS:
+            r = run_paper(cfg, args.steps, args.warmup)
+            tf = r["flops"] / (r["ms"] * 1e-3) / 1e12
+            paper["w%d" % cfg["index"]] = dict(
+                cfg=cfg, r=r, line={
+                    "workload": cfg["name"], "value": round(tf, 2), "unit": "TFLOP/s",
+                    "us_per_launch": round(r["ms"] * 1e3, 2),
+                    "frac_of_peak": round(tf / PEAK["f32"], 4), "schedule": r["sched"],
+                    "timing": "HIP graph of 50 launches, replayed", "graph_replay_exact":
+                        r["replay_ok"]})
+            print("# %s: %.2f us/launch" % (cfg["name"], r["ms"] * 1e3), file=sys.stderr,
+                  flush=True)
+        summaries["paper"] = {k: v["line"] for k, v in paper.items()}
+
     head_kind = "fp32" if "fp32" in summaries else kinds[0]
     head = summaries[head_kind]
     line = {
@@ -304,6 +424,7 @@ def main():
         if "cpu_baseline" in extra:
             line["cpu_baseline"] = extra["cpu_baseline"]
         line["parity"] = extra["parity"]
+        line["parity"].update(paper_parity(paper))
     print(json.dumps(line), flush=True)
 
 

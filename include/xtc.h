@@ -160,6 +160,29 @@ xtc_status xtc_conv2d_nchw(int64_t N, int64_t C, int64_t H, int64_t W,
                            xtc_dtype dtype, const xtc_sched *sched, void *stream);
 
 /*
+ * xtc_matmul_relu, xtc_conv2d_nchw_relu -- the contraction followed by its
+ * consumer relu, fused into the epilogue (the paper's matmul+relu graph,
+ * Sec. 5.2, Fig. 9, and its "fusion of consumer", Sec. 3.2): every output
+ * element is written once, as relu(v) = (v < 0 ? 0 : v) of the value v that
+ * xtc_matmul / xtc_conv2d_nchw would write (a NaN stays NaN, -0.0 stays
+ * -0.0).  Arguments, layouts, ownership, schedules and errors are exactly
+ * those of xtc_matmul / xtc_conv2d_nchw; the same kernel instances run, so
+ * no extra pass over the output and no extra memory traffic is added.
+ */
+xtc_status xtc_matmul_relu(int64_t M, int64_t N, int64_t K,
+                           const void *A, int64_t lda,
+                           const void *B, int64_t ldb,
+                           float *C, int64_t ldc,
+                           xtc_dtype dtype, const xtc_sched *sched, void *stream);
+
+xtc_status xtc_conv2d_nchw_relu(int64_t N, int64_t C, int64_t H, int64_t W,
+                                int64_t OC, int64_t R, int64_t S,
+                                int64_t stride_h, int64_t stride_w,
+                                int64_t pad_h, int64_t pad_w,
+                                const void *X, const void *Wt, float *Y,
+                                xtc_dtype dtype, const xtc_sched *sched, void *stream);
+
+/*
  * xtc_default_schedule -- the schedule used when sched == NULL, chosen from
  * the problem shape (the paper's default_schedule of an exploration
  * strategy, Sec. 5.2).  For op == XTC_OP_CONV2D pass the implicit-GEMM

@@ -12,6 +12,10 @@ cross-correlation, NCHW / OIHW):
 * ``conv2d``: ``Y[n,oc,oh,ow] = sum_{ic,kh,kw} X[n,ic,oh*s-p+kh,ow*s-p+kw] *
   W[oc,ic,kh,kw]`` with out-of-range input terms zero, fp64, ascending
   (ic, kh, kw).
+* ``relu``: elementwise ``v < 0 ? 0 : v`` (one of the paper's operators,
+  Sec. 3.1; the consumer of the matmul in its matmul+relu graph, Fig. 9).  A
+  NaN stays NaN.  The fused forms are ``relu(matmul(A, B))`` and
+  ``relu(conv2d(X, W))``: the consumer applied to the finished fp64 result.
 
 Operands are fp32 arrays, or uint16 arrays holding bf16 bit patterns (widened
 exactly).  Both operands of one call must be of the same kind.
@@ -156,6 +160,12 @@ def conv2d_sampled(X, W, F, stride=1, pad=0, nthreads: int = 0, lib=None) -> np.
     lib.xo_conv2d_sampled(N, C, H, Wd, OC, R, S, sh, sw, ph, pw, _ptr(X), _ptr(W),
                           _kind(X, W), _ptr(F), F.shape[0], _ptr(out), nthreads)
     return out
+
+
+def relu(v) -> np.ndarray:
+    """Elementwise ``v < 0 ? 0 : v`` in fp64 (NaN propagates)."""
+    v = np.asarray(v, dtype=np.float64)
+    return np.where(v < 0.0, 0.0, v)
 
 
 def rel_fro(got, ref) -> float:

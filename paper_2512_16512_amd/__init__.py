@@ -2,7 +2,7 @@
 
 Argument marshalling only: every step of the computation runs in the HIP
 kernels of ``libxtc.so``.  The functions ``xtc_matmul``, ``xtc_conv2d_nchw``,
-``xtc_default_schedule``, ``xtc_sched_check``, ``xtc_sched_list``,
+``xtc_matmul_relu``, ``xtc_conv2d_nchw_relu``, ``xtc_default_schedule``, ``xtc_sched_check``, ``xtc_sched_list``,
 ``xtc_status_str`` mirror the C ABI of ``include/xtc.h`` one to one (pointers
 are Python ints holding device addresses; the stream is a ``hipStream_t`` as
 an int, 0 for the null stream).  ``matmul`` and ``conv2d_nchw`` are
@@ -74,7 +74,7 @@ class XtcError(RuntimeError):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            "libxtc.so is not built (expected at %s); run `python -m paper_2512_16512_amd.build`"
+            "libxtc.so is not built (expected at %s); run `python paper_2512_16512_amd/build.py`"
             % LIB_PATH)
     lib = ctypes.CDLL(LIB_PATH)
     i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32
@@ -83,6 +83,10 @@ def _load():
     lib.xtc_matmul.restype = i32
     lib.xtc_conv2d_nchw.argtypes = [i64] * 11 + [vp, vp, vp, i32, sp, vp]
     lib.xtc_conv2d_nchw.restype = i32
+    lib.xtc_matmul_relu.argtypes = lib.xtc_matmul.argtypes
+    lib.xtc_matmul_relu.restype = i32
+    lib.xtc_conv2d_nchw_relu.argtypes = lib.xtc_conv2d_nchw.argtypes
+    lib.xtc_conv2d_nchw_relu.restype = i32
     lib.xtc_default_schedule.argtypes = [i32, i32, i64, i64, i64, sp]
     lib.xtc_default_schedule.restype = i32
     lib.xtc_sched_check.argtypes = [i32, i32, sp]
@@ -103,7 +107,8 @@ def _load():
 _lib = _load()
 
 # Every symbol include/xtc.h declares.
-EXPORTS = ("xtc_matmul", "xtc_conv2d_nchw", "xtc_default_schedule", "xtc_sched_check",
+EXPORTS = ("xtc_matmul", "xtc_conv2d_nchw", "xtc_matmul_relu", "xtc_conv2d_nchw_relu",
+           "xtc_default_schedule", "xtc_sched_check",
            "xtc_sched_list", "xtc_status_str", "xtc_last_hip_error", "xtc_conv_max_k",
            "xtc_version")
 
@@ -123,6 +128,16 @@ def xtc_conv2d_nchw(N, C, H, W, OC, R, S, stride_h, stride_w, pad_h, pad_w, X, W
                     sched=None, stream=0) -> int:
     return _lib.xtc_conv2d_nchw(N, C, H, W, OC, R, S, stride_h, stride_w, pad_h, pad_w, X, Wt, Y,
                                 dtype, _sp(sched), stream)
+
+
+def xtc_matmul_relu(M, N, K, A, lda, B, ldb, C, ldc, dtype, sched=None, stream=0) -> int:
+    return _lib.xtc_matmul_relu(M, N, K, A, lda, B, ldb, C, ldc, dtype, _sp(sched), stream)
+
+
+def xtc_conv2d_nchw_relu(N, C, H, W, OC, R, S, stride_h, stride_w, pad_h, pad_w, X, Wt, Y, dtype,
+                         sched=None, stream=0) -> int:
+    return _lib.xtc_conv2d_nchw_relu(N, C, H, W, OC, R, S, stride_h, stride_w, pad_h, pad_w, X,
+                                     Wt, Y, dtype, _sp(sched), stream)
 
 
 def xtc_default_schedule(op, dtype, M, N, K) -> Sched:
@@ -182,10 +197,11 @@ def _check_rowmajor(t, name):
         raise ValueError("%s must be a 2-D row-major tensor (unit column stride)" % name)
 
 
-def matmul(a, b, out=None, sched=None):
-    """``out = a @ b`` on the GPU.  ``a`` [M,K] and ``b`` [K,N] are both
-    float32 or both bfloat16 CUDA tensors with unit column stride; ``out`` is
-    float32 [M,N] (allocated when None).  Enqueued on torch's current stream."""
+def matmul(a, b, out=None, sched=None, relu=False):
+    """``out = a @ b`` on the GPU (``relu(a @ b)`` fused when ``relu``).
+    ``a`` [M,K] and ``b`` [K,N] are both float32 or both bfloat16 CUDA tensors
+    with unit column stride; ``out`` is float32 [M,N] (allocated when None).
+    Enqueued on torch's current stream."""
     import torch
     _check_rowmajor(a, "a")
     _check_rowmajor(b, "b")
@@ -205,16 +221,18 @@ def matmul(a, b, out=None, sched=None):
     lda = a.stride(0) if M > 1 else max(K, 1)
     ldb = b.stride(0) if K > 1 else max(N, 1)
     ldc = out.stride(0) if M > 1 else max(N, 1)
-    st = xtc_matmul(M, N, K, a.data_ptr(), lda, b.data_ptr(), ldb, out.data_ptr(), ldc,
-                    _dtype_code(torch, a), sched, _stream(torch, a.device))
+    fn = xtc_matmul_relu if relu else xtc_matmul
+    st = fn(M, N, K, a.data_ptr(), lda, b.data_ptr(), ldb, out.data_ptr(), ldc,
+            _dtype_code(torch, a), sched, _stream(torch, a.device))
     if st != XTC_OK:
-        raise XtcError(st, "xtc_matmul")
+        raise XtcError(st, fn.__name__)
     return out
 
 
-def conv2d_nchw(x, w, stride=1, pad=0, out=None, sched=None):
+def conv2d_nchw(x, w, stride=1, pad=0, out=None, sched=None, relu=False):
     """Zero-padded cross-correlation of NCHW ``x`` with OIHW ``w`` (float32,
-    contiguous CUDA tensors) into a float32 NCHW ``out``."""
+    contiguous CUDA tensors) into a float32 NCHW ``out`` (relu fused into the
+    epilogue when ``relu``)."""
     import torch
     if x.dim() != 4 or w.dim() != 4 or not x.is_contiguous() or not w.is_contiguous():
         raise ValueError("x and w must be contiguous 4-D tensors")
@@ -230,8 +248,9 @@ def conv2d_nchw(x, w, stride=1, pad=0, out=None, sched=None):
         out = torch.empty((N, OC, max(OH, 0), max(OW, 0)), dtype=torch.float32, device=x.device)
     if not out.is_contiguous() or tuple(out.shape) != (N, OC, OH, OW):
         raise ValueError("out must be a contiguous [N, OC, OH, OW] tensor")
-    st = xtc_conv2d_nchw(N, C, H, W, OC, R, S, sh, sw, ph, pw, x.data_ptr(), w.data_ptr(),
-                         out.data_ptr(), _dtype_code(torch, x), sched, _stream(torch, x.device))
+    fn = xtc_conv2d_nchw_relu if relu else xtc_conv2d_nchw
+    st = fn(N, C, H, W, OC, R, S, sh, sw, ph, pw, x.data_ptr(), w.data_ptr(), out.data_ptr(),
+            _dtype_code(torch, x), sched, _stream(torch, x.device))
     if st != XTC_OK:
-        raise XtcError(st, "xtc_conv2d_nchw")
+        raise XtcError(st, fn.__name__)
     return out

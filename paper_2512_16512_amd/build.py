@@ -2,7 +2,8 @@
 
 Every translation unit is compiled for gfx950 only, with packed-fp32
 instruction selection disabled, then linked into one shared library next to
-this file.  Run ``python -m paper_2512_16512_amd.build`` or call ``build()``.
+this file.  Run ``python paper_2512_16512_amd/build.py`` (a plain script: importing the
+package needs the built library) or call ``build()``.
 """
 from __future__ import annotations
 

@@ -190,7 +190,7 @@ conv2d_f32_kernel(ConvArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int oc = m0 + wm * WM + i * MI + MF::row(lane, r);
-                if (oc < M) ybase[oc * OHW] = acc[i][j][r];
+                if (oc < M) ybase[oc * OHW] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
             }
     }
 }
@@ -451,7 +451,7 @@ conv2d_f32_dma_kernel(ConvArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int oc = m0 + wm * WM + i * MI + MF::row(lane, r);
-                if (oc < M) ybase[oc * OHW] = acc[i][j][r];
+                if (oc < M) ybase[oc * OHW] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
             }
     }
 }
@@ -718,7 +718,7 @@ conv2d_f32_tap_kernel(ConvArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int oc = m0 + wm * WM + i * MI + MF::row(lane, r);
-                if (oc < M) ybase[oc * OHW] = acc[i][j][r];
+                if (oc < M) ybase[oc * OHW] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
             }
     }
 }

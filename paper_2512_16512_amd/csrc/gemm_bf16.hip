@@ -239,7 +239,7 @@ gemm_bf16_kernel(GemmArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
-                if (row < M && col < N) C[row * ldc + col] = acc[i][j][r];
+                if (row < M && col < N) C[row * ldc + col] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
             }
         }
 }
@@ -517,7 +517,7 @@ gemm_bf16_dma_kernel(GemmArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
-                if (row < M && col < N) C[row * ldc + col] = acc[i][j][r];
+                if (row < M && col < N) C[row * ldc + col] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
             }
         }
 }

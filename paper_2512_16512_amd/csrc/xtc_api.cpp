@@ -180,9 +180,13 @@ int32_t xtc_sched_list(xtc_op op, xtc_dtype dt, xtc_sched *out, int32_t cap) {
     return n;
 }
 
-xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
-                      int64_t ldb, float *C, int64_t ldc, xtc_dtype dtype, const xtc_sched *sched,
-                      void *stream) {
+}  // extern "C"
+
+namespace {
+
+xtc_status matmul_impl(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
+                       int64_t ldb, float *C, int64_t ldc, xtc_dtype dtype, const xtc_sched *sched,
+                       void *stream, int relu) {
     if (dtype != XTC_F32 && dtype != XTC_BF16) return XTC_ERR_BAD_DTYPE;
     if (M < 0 || N < 0 || K < 0) return XTC_ERR_BAD_SHAPE;
     if (lda < (K > 1 ? K : 1) || ldb < (N > 1 ? N : 1) || ldc < (N > 1 ? N : 1))
@@ -209,6 +213,7 @@ xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     a.M = (int)M; a.N = (int)N; a.K = (int)K;
     a.A = A; a.lda = (int)lda; a.B = B; a.ldb = (int)ldb; a.C = C; a.ldc = (int)ldc;
     a.raster = s.raster; a.xcd_remap = s.xcd_remap;
+    a.relu = relu;
     bool vec = K == 0 || (aligned16(A) && aligned16(B) && (lda * elt) % 16 == 0 &&
                           (ldb * elt) % 16 == 0);
     if (inst->vec_whole_chunks && ((K * elt) % 16 != 0 || (N * elt) % 16 != 0)) vec = false;
@@ -216,10 +221,10 @@ xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     return hip_status(fn(a, static_cast<hipStream_t>(stream)));
 }
 
-xtc_status xtc_conv2d_nchw(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int64_t R,
-                           int64_t S, int64_t stride_h, int64_t stride_w, int64_t pad_h,
-                           int64_t pad_w, const void *X, const void *Wt, float *Y, xtc_dtype dtype,
-                           const xtc_sched *sched, void *stream) {
+xtc_status conv_impl(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int64_t R,
+                     int64_t S, int64_t stride_h, int64_t stride_w, int64_t pad_h, int64_t pad_w,
+                     const void *X, const void *Wt, float *Y, xtc_dtype dtype,
+                     const xtc_sched *sched, void *stream, int relu) {
     if (dtype != XTC_F32 && dtype != XTC_BF16) return XTC_ERR_BAD_DTYPE;
     if (dtype != XTC_F32) return XTC_ERR_BAD_DTYPE;
     if (N < 0 || OC < 0 || C < 1 || H < 1 || W < 1 || R < 1 || S < 1 || stride_h < 1 ||
@@ -254,7 +259,40 @@ xtc_status xtc_conv2d_nchw(int64_t N, int64_t C, int64_t H, int64_t W, int64_t O
     a.Wt = static_cast<const float *>(Wt);
     a.Y = Y;
     a.raster = s.raster; a.xcd_remap = s.xcd_remap;
+    a.relu = relu;
     return hip_status(inst->launch(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
+                      int64_t ldb, float *C, int64_t ldc, xtc_dtype dtype, const xtc_sched *sched,
+                      void *stream) {
+    return matmul_impl(M, N, K, A, lda, B, ldb, C, ldc, dtype, sched, stream, 0);
+}
+
+xtc_status xtc_matmul_relu(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                           const void *B, int64_t ldb, float *C, int64_t ldc, xtc_dtype dtype,
+                           const xtc_sched *sched, void *stream) {
+    return matmul_impl(M, N, K, A, lda, B, ldb, C, ldc, dtype, sched, stream, 1);
+}
+
+xtc_status xtc_conv2d_nchw(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int64_t R,
+                           int64_t S, int64_t stride_h, int64_t stride_w, int64_t pad_h,
+                           int64_t pad_w, const void *X, const void *Wt, float *Y, xtc_dtype dtype,
+                           const xtc_sched *sched, void *stream) {
+    return conv_impl(N, C, H, W, OC, R, S, stride_h, stride_w, pad_h, pad_w, X, Wt, Y, dtype, sched,
+                     stream, 0);
+}
+
+xtc_status xtc_conv2d_nchw_relu(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int64_t R,
+                                int64_t S, int64_t stride_h, int64_t stride_w, int64_t pad_h,
+                                int64_t pad_w, const void *X, const void *Wt, float *Y,
+                                xtc_dtype dtype, const xtc_sched *sched, void *stream) {
+    return conv_impl(N, C, H, W, OC, R, S, stride_h, stride_w, pad_h, pad_w, X, Wt, Y, dtype, sched,
+                     stream, 1);
 }
 
 }  // extern "C"

@@ -21,6 +21,7 @@ struct GemmArgs {
     int ldc;
     int raster;     // 0 row-major, 1 column-major, g >= 2 grouped by g tile-rows
     int xcd_remap;  // 1: give each XCD a contiguous band of the tile order
+    int relu;       // 1: the epilogue writes relu(acc) = (acc < 0 ? 0 : acc) (fused consumer)
 };
 
 // Arguments of one conv2d launch (implicit GEMM: M = OC, N = Nb*OH*OW,
@@ -34,6 +35,7 @@ struct ConvArgs {
     float *Y;
     int raster;
     int xcd_remap;
+    int relu;       // 1: the epilogue writes relu(acc) = (acc < 0 ? 0 : acc) (fused consumer)
 };
 
 using GemmLaunch = hipError_t (*)(const GemmArgs &, hipStream_t);

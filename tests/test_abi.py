@@ -71,12 +71,14 @@ BAD = 0x10  # a dummy non-NULL pointer: dereferencing it would fault
 ])
 def test_matmul_validation(x, args, expected):
     assert x.xtc_matmul(*args) == expected
+    assert x.xtc_matmul_relu(*args) == expected
 
 
 def test_matmul_empty_is_noop(x):
     # M == 0 or N == 0 returns OK without any device work (NULL pointers allowed)
     assert x.xtc_matmul(0, 5, 5, 0, 5, 0, 5, 0, 5, 0) == 0
     assert x.xtc_matmul(5, 0, 5, 0, 5, 0, 1, 0, 1, 1) == 0
+    assert x.xtc_matmul_relu(0, 5, 5, 0, 5, 0, 5, 0, 5, 0) == 0
 
 
 @pytest.mark.parametrize("args,expected", [
@@ -93,6 +95,7 @@ def test_matmul_empty_is_noop(x):
 ])
 def test_conv_validation(x, args, expected):
     assert x.xtc_conv2d_nchw(*args) == expected
+    assert x.xtc_conv2d_nchw_relu(*args) == expected
 
 
 def test_conv_empty_is_noop(x):
@@ -129,6 +132,7 @@ def test_sched_illegal_fields(x, field, value):
     assert x.xtc_sched_check(0, 0, s) == 5
     # and the same schedule is refused by the entry point before any device work
     assert x.xtc_matmul(4, 4, 4, BAD, 4, BAD, 4, BAD, 4, 0, s) == 5
+    assert x.xtc_matmul_relu(4, 4, 4, BAD, 4, BAD, 4, BAD, 4, 0, s) == 5
 
 
 def test_sched_legal_but_not_compiled(x):

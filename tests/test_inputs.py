@@ -86,3 +86,16 @@ def test_config_shapes():
     assert (c[3]["M"], c[3]["dtype"]) == (8192, "bf16")
     oh, ow = xi.conv_out_hw(56, 56, 3, 3, 1, 1, 1, 1)
     assert (oh, ow) == (56, 56)
+
+
+def test_paper_workload_shapes():
+    w = {c["index"]: c for c in xi.PAPER_WORKLOADS}
+    assert sorted(w) == [5, 6, 7, 8, 9]
+    assert (w[6]["M"], w[6]["K"], w[6]["N"]) == (512, 128, 1024)
+    assert (w[7]["M"], w[7]["K"], w[7]["N"], w[7]["op"]) == (256, 128, 1024, "matmul_relu")
+    assert (w[8]["M"], w[8]["N"], w[8]["K"]) == (256, 258, 512)
+    c = w[9]
+    oh, ow = xi.conv_out_hw(c["H"], c["W"], c["R"], c["S"], c["stride"], c["stride"], c["pad"],
+                            c["pad"])
+    assert (oh, ow, c["OC"], c["C"]) == (112, 112, 16, 3)     # [112,112,16] x [7,7,3]
+    assert not set(w) & {x["index"] for x in xi.CONFIGS}        # distinct seeds

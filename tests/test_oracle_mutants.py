@@ -116,3 +116,19 @@ def test_mutant_is_caught(name):
         lib = oracle._load(lib_path)
         failed = _battery(lib)
     assert failed, "planted mistake %r was not caught by any pin" % name
+
+
+RELU_MUTANTS = {
+    "relu_abs": np.abs,
+    "relu_min": lambda v: np.minimum(np.asarray(v, np.float64), 0.0),
+    "relu_identity": lambda v: np.asarray(v, np.float64),
+    "relu_nan_to_zero": lambda v: np.where(np.asarray(v, np.float64) > 0.0, v, 0.0),
+    "relu_shifted": lambda v: np.where(np.asarray(v, np.float64) < 1e-7, 0.0, v),
+}
+
+
+@pytest.mark.parametrize("name", sorted(RELU_MUTANTS))
+def test_relu_mutant_is_caught(name):
+    from tests.test_oracle_pins import relu_battery
+    with pytest.raises(AssertionError):
+        relu_battery(RELU_MUTANTS[name])

@@ -238,3 +238,44 @@ def test_rel_fro():
     assert oracle.rel_fro([0.0, 0.0], [0.0, 0.0]) == 0.0
     assert oracle.rel_fro([1.0], [0.0]) == float("inf")
     assert abs(oracle.rel_fro([3.0, 4.0 + 1e-3], [3.0, 4.0]) - 1e-3 / 5.0) < 1e-15
+
+
+# -------------------------------------------------------------------- relu
+# The consumer of the paper's matmul+relu graph (Sec. 5.2, Fig. 9), fused into
+# the contraction's epilogue on the GPU; the oracle applies it to the finished
+# fp64 result.
+
+
+def relu_battery(relu_fn):
+    """Pins of relu(v) = (v < 0 ? 0 : v); raises AssertionError on a mismatch.
+    Shared with the planted-mistake test, which must see it fail."""
+    g = _golden("matmul_relu_2x3.json")
+    A = np.array(g["A"], np.float32)
+    B = np.array(g["B"], np.float32)
+    C = oracle.matmul(A, B)
+    assert np.array_equal(C, np.array(g["C"], np.float64))
+    assert np.array_equal(relu_fn(C), np.array(g["relu_C"], np.float64))
+    # against the library routine in float64, specials included
+    v = np.concatenate([xi.uniform_f32(141, (1000,)).astype(np.float64) * 1e3,
+                        [0.0, -0.0, np.inf, -np.inf, np.nan, 1e-300, -1e-300]])
+    ref = torch.nn.functional.relu(torch.from_numpy(v)).numpy()
+    assert np.array_equal(relu_fn(v), ref, equal_nan=True)
+    # closed forms: relu(v) - relu(-v) == v and relu(v) + relu(-v) == |v|
+    w = xi.uniform_f32(142, (777,)).astype(np.float64)
+    assert np.array_equal(relu_fn(w) - relu_fn(-w), w)
+    assert np.array_equal(relu_fn(w) + relu_fn(-w), np.abs(w))
+
+
+def test_relu_pins():
+    relu_battery(oracle.relu)
+
+
+def test_conv_relu_vs_torch_float64():
+    X = xi.uniform_f32(143, (2, 3, 9, 9))
+    Wt = xi.uniform_f32(144, (4, 3, 3, 3))
+    ref = torch.relu(torch.nn.functional.conv2d(torch.from_numpy(X).double(),
+                                                torch.from_numpy(Wt).double(), stride=2,
+                                                padding=1)).numpy()
+    got = oracle.relu(oracle.conv2d(X, Wt, stride=2, pad=1))
+    assert np.max(np.abs(got - ref)) < 1e-12
+    assert (got == 0).mean() > 0.2      # the case really exercises the negative branch

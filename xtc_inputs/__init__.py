@@ -166,6 +166,24 @@ CONFIGS = [
 ]
 
 
+# The other workloads the paper runs, as extra parity and measurement cases.
+# Same generators; seeds follow the index.  "matmul_relu" is the matmul with
+# its consumer relu fused (the graph of the paper's strategy example).
+PAPER_WORKLOADS = [
+    dict(index=5, op="matmul", dtype="f32", M=1024, N=1024, K=1024, check="full",
+         name="matmul fp32 1024x1024x1024 (Sec. 6.1)"),
+    dict(index=6, op="matmul", dtype="f32", M=512, N=1024, K=128, check="full",
+         name="matmul fp32 [512,128]x[128,1024] (Sec. 6.2)"),
+    dict(index=7, op="matmul_relu", dtype="f32", M=256, N=1024, K=128, check="full",
+         name="matmul+relu fp32 [256,128]x[128,1024] (Sec. 5.2)"),
+    dict(index=8, op="matmul", dtype="f32", M=256, N=258, K=512, check="full",
+         name="matmul fp32 256x258x512 (Sec. 3.1 running example)"),
+    dict(index=9, op="conv2d", dtype="f32", N=1, C=3, H=224, W=224, OC=16, R=7, S=7,
+         stride=2, pad=3, check="full",
+         name="conv2d NCHW fp32 1x3x224x224 -> 16, 7x7, stride 2, pad 3 (Sec. 6.2)"),
+]
+
+
 def matmul_inputs(cfg: dict):
     """A[M,K], B[K,N] for a matmul config: fp32 arrays, or bf16 bit arrays
     (uint16) when ``cfg['dtype'] == 'bf16'``."""
