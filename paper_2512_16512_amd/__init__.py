@@ -72,6 +72,14 @@ class XtcError(RuntimeError):
 
 
 def _load():
+    # torch ships its own HIP runtime (same soname as ROCm's).  Loading torch
+    # first makes libxtc.so bind to that one runtime; loaded the other way
+    # round, the process would map two runtimes, and torch's device memory
+    # and streams would be invalid handles for the library's launches.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             "libxtc.so is not built (expected at %s); run `python paper_2512_16512_amd/build.py`"

@@ -128,9 +128,14 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     if (op == XTC_OP_CONV2D) {
         if (dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
         // 64x256 tiles of 4 waves (64x64 each) with a two-stage ring: two
-        // workgroups per CU, so up to 512 tiles run in a single wave.
+        // workgroups per CU, so up to 512 tiles run in a single wave.  When
+        // that leaves CUs idle (a small image batch), 64x64 tiles of four
+        // 32x32 waves give four times as many workgroups.
         *out = make_sched(64, 256, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
-        if (M > 64) *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
+        if (M > 64)
+            *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
+        else if (tiles(64, 256) < cus)
+            *out = make_sched(64, 64, 32, 32, 32, 32, 32, 2, 2, -1, 0, 1);
         out->raster = 0;
         return XTC_OK;
     }

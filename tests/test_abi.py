@@ -157,7 +157,8 @@ def test_bf16_schedule_rejected_for_f32(x):
 def test_default_schedules_are_compiled(x):
     for (op, dt, M, N, K) in [(0, 0, 4096, 4096, 4096), (0, 0, 256, 256, 256), (0, 0, 1, 1, 1),
                               (0, 1, 8192, 8192, 8192), (0, 1, 100, 100, 100), (0, 1, 2048, 2048, 64),
-                              (1, 0, 64, 100352, 576), (1, 0, 256, 1000, 2304)]:
+                              (1, 0, 64, 100352, 576), (1, 0, 256, 1000, 2304),
+                              (1, 0, 16, 12544, 147)]:
         s = x.xtc_default_schedule(op, dt, M, N, K)
         assert x.xtc_sched_check(op, dt, s) == 0, (op, dt, M, N, K, s)
     with pytest.raises(x.XtcError):
@@ -167,3 +168,16 @@ def test_default_schedules_are_compiled(x):
 def test_no_hip_error_recorded_by_validation(x):
     assert x.xtc_last_hip_error() == 0
     assert x.xtc_conv_max_k() >= 576
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    # The binding loads torch before libxtc.so, so the process maps a single
+    # HIP runtime (two would make torch's device pointers invalid handles for
+    # the library's launches).
+    import subprocess
+    import sys
+    code = ("import paper_2512_16512_amd\nimport torch\n"
+            "print(len({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}))")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip().splitlines()[-1] == "1"
