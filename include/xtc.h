@@ -71,7 +71,8 @@ typedef enum {
  *                (block_m/wave_m)*(block_n/wave_n) waves.
  *  mfma_m/n/k    matrix-core instruction tile (the vectorize primitive):
  *                fp32: 32x32x2 or 16x16x4; bf16: 32x32x16 or 16x16x32.
- *  lds_stages    LDS buffers per operand (pack + software pipelining): 2.
+ *  lds_stages    LDS buffers per operand (pack + software pipelining), 1-4;
+ *                0 = no LDS staging (the k_split kernels).
  *  lds_pad       LDS row padding in elements (pack with padding against bank
  *                conflicts); -1 selects an XOR-swizzled layout instead.
  *  unroll_k      MFMA k-steps unrolled per LDS stage (0 = the whole stage).
@@ -86,9 +87,18 @@ typedef enum {
  *                OIHW weight layout); 1: tap-major, k = (kh*S + kw)*C + ic
  *                (needs C % 32 == 0, else the channel-major kernel with the
  *                same tiles runs).  Results differ only by rounding order.
+ *  k_split       waves that share one workgroup tile, each reducing every
+ *                k_split-th group of block_k reduction steps (a parallel
+ *                split of the reduction for problems with too few tiles to
+ *                fill the chip); their partial sums are added in a fixed
+ *                order through LDS, so results stay deterministic.  1 = no
+ *                split.  With k_split > 1 each wave covers the whole
+ *                workgroup tile (wave_m = block_m, wave_n = block_n) and
+ *                lds_stages = 0: operands go from memory straight to the
+ *                matrix-core registers, double-buffered in registers.
  *
- * block_*, wave_*, mfma_*, lds_stages, lds_pad, unroll_k and k_order select a
- * compiled kernel instance; raster and xcd_remap are run-time choices valid
+ * block_*, wave_*, mfma_*, lds_stages, lds_pad, unroll_k, k_order and k_split
+ * select a compiled kernel instance; raster and xcd_remap are run-time choices valid
  * for all.
  */
 typedef struct {
@@ -102,6 +112,7 @@ typedef struct {
     int32_t raster;
     int32_t xcd_remap;
     int32_t k_order;
+    int32_t k_split;
 } xtc_sched;
 
 /*

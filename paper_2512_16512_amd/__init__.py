@@ -41,11 +41,12 @@ class Sched(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "size", "block_m", "block_n", "block_k", "wave_m", "wave_n",
         "mfma_m", "mfma_n", "mfma_k", "lds_stages", "lds_pad", "unroll_k",
-        "raster", "xcd_remap", "k_order")]
+        "raster", "xcd_remap", "k_order", "k_split")]
 
     def __init__(self, **kw):
         super().__init__()
         self.size = ctypes.sizeof(Sched)
+        self.k_split = 1
         for k, v in kw.items():
             setattr(self, k, v)
 
@@ -55,11 +56,10 @@ class Sched(ctypes.Structure):
     def __repr__(self):
         d = self.as_dict()
         return ("Sched(block=%dx%dx%d wave=%dx%d mfma=%dx%dx%d stages=%d pad=%d unroll=%d "
-                "raster=%d xcd=%d k_order=%d)" % (d["block_m"], d["block_n"], d["block_k"],
-                                                  d["wave_m"], d["wave_n"], d["mfma_m"], d["mfma_n"],
-                                                  d["mfma_k"], d["lds_stages"], d["lds_pad"],
-                                                  d["unroll_k"], d["raster"], d["xcd_remap"],
-                                                  d["k_order"]))
+                "raster=%d xcd=%d k_order=%d k_split=%d)" % (
+                    d["block_m"], d["block_n"], d["block_k"], d["wave_m"], d["wave_n"],
+                    d["mfma_m"], d["mfma_n"], d["mfma_k"], d["lds_stages"], d["lds_pad"],
+                    d["unroll_k"], d["raster"], d["xcd_remap"], d["k_order"], d["k_split"]))
 
 
 class XtcError(RuntimeError):

@@ -402,6 +402,172 @@ hipError_t launch_f32_dma(const GemmArgs &a, hipStream_t s) {
         dim3(tiles), dim3(G::NT), kargs, 0, s);
 }
 
+// ---------------------------------------------------------------------------
+// Reduction-split kernel (k_split = KS > 1) for problems with too few output
+// tiles to fill the chip.  KS waves share one BM x BN tile (BM = MI*TM,
+// BN = MI*TN); wave g reduces the K-steps g, g + KS, g + 2KS, ... of
+// BK = U*KCH k values each.  Operands go from memory straight to the MFMA
+// operand registers (a small problem is L2-resident, and no LDS round trip
+// sits on the latency path) through a ring of D register buffers: the loads
+// of the wave's K-step t + D - 1 are issued before the MFMAs of step t, so
+// that D - 1 steps of loads are in flight behind the matrix-core work.  At the
+// end every wave writes its partial accumulators to LDS and the KS partials
+// are added in the fixed order g = 0, 1, ..., KS-1 (deterministic results),
+// each wave finishing an interleaved share of the tile's registers, with the
+// epilogue applied to the sum.
+template <int MI, int TM, int TN, int KS, int U, int D, bool VEC>
+__global__ void __launch_bounds__(KS * 64)
+gemm_f32_ksplit_kernel(GemmArgs p) {
+    typedef F32Mfma<MI> MF;
+    constexpr int KCH = 4 * MF::KG;  // k values of one fragment set (4 instructions)
+    constexpr int BK = U * KCH;      // k values of one K-step
+    constexpr int BM = MI * TM, BN = MI * TN;
+    constexpr int NREG = TM * TN * MF::NACC;
+    __shared__ float red[KS][NREG][64];
+
+    const int lane = threadIdx.x & 63, g = threadIdx.x >> 6;
+    const int lrow = lane % MI, lgrp = lane / MI;
+    const int M = p.M, N = p.N, K = p.K;
+    const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+
+    const float *__restrict__ A = static_cast<const float *>(p.A);
+    const float *__restrict__ B = static_cast<const float *>(p.B);
+    const int lda = p.lda, ldb = p.ldb;
+
+    // Branch-free loads: buffer loads whose offset is moved past the end of
+    // the operand (kOOB) when the element lies outside the matrix read zero.
+    // VEC (K a multiple of 4, 16-byte aligned rows): one 16-byte load per A
+    // row segment; otherwise one 4-byte load per element.
+    const __amdgpu_buffer_rsrc_t ra =
+        __builtin_amdgcn_make_buffer_rsrc((void *)A, (short)0, ((M - 1) * lda + K) * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rb =
+        __builtin_amdgcn_make_buffer_rsrc((void *)B, (short)0, K > 0 ? ((K - 1) * ldb + N) * 4 : 0,
+                                          0x00020000);
+    // Per-lane byte offsets of this lane's A rows and B columns, moved out of
+    // range when the row or column lies outside the matrix.  B rows at or
+    // past K are out of range by themselves (K*ldb + n >= (K-1)*ldb + N), so
+    // the k index of B is only clamped to K (which also keeps the unsigned
+    // offset from wrapping); A, whose next row follows row i directly, tests
+    // k < K.
+    unsigned aoff[TM], boff[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+        const int r = m0 + i * MI + lrow;
+        aoff[i] = r < M ? (unsigned)(r * lda) * 4u : (unsigned)kOOB;
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int c = n0 + j * MI + lrow;
+        boff[j] = c < N ? (unsigned)c * 4u : (unsigned)kOOB;
+    }
+
+    // Lane group lgrp of instruction s takes k = kb + s with kb = k0 + 4*lgrp
+    // (as in the LDS-staged kernels): one 16-byte row segment of A and four
+    // column values of B per fragment set.
+    f32x4 fa[D][U][TM];
+    float fb[D][U][TN][4];
+    auto load = [&](const int buf, const int kt) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int kb = kt * BK + u * KCH + 4 * lgrp;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                if (VEC) {
+                    const unsigned off = kb < K ? aoff[i] + (unsigned)kb * 4u : (unsigned)kOOB;
+                    fa[buf][u][i] = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)off, 0, 0));
+                } else {
+#pragma unroll
+                    for (int s = 0; s < 4; ++s) {
+                        const unsigned off =
+                            kb + s < K ? aoff[i] + (unsigned)(kb + s) * 4u : (unsigned)kOOB;
+                        fa[buf][u][i][s] = __builtin_bit_cast(
+                            float, __builtin_amdgcn_raw_buffer_load_b32(ra, (int)off, 0, 0));
+                    }
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const unsigned roff = (unsigned)(min(kb + s, K) * ldb) * 4u;
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    fb[buf][u][j][s] = __builtin_bit_cast(
+                        float, __builtin_amdgcn_raw_buffer_load_b32(rb, (int)(roff + boff[j]), 0, 0));
+            }
+        }
+    };
+
+    typename MF::acc_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[i][j][r] = 0.f;
+
+    auto compute = [&](const int buf) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = MF::mma(fa[buf][u][i][s], fb[buf][u][j][s], acc[i][j]);
+    };
+
+    // D K-steps per iteration (unrolled) so that every register buffer is
+    // named by a constant.  This wave's steps are g, g + KS, ...  The loop
+    // is branch-free: steps past the end are loaded (as zeros, every offset
+    // being out of range) and multiplied like the others, so every step
+    // issues the same loads and the compiler's wait counts stay exact.
+    const int KT = (K + BK - 1) / BK;
+#pragma unroll
+    for (int d = 0; d + 1 < D; ++d) load(d, g + d * KS);
+    for (int base = g; base < KT; base += D * KS) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            load((d + D - 1) % D, base + (d + D - 1) * KS);
+            compute(d);
+        }
+    }
+
+    // Fixed-order reduction of the KS partial tiles through LDS.
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) red[g][(i * TN + j) * MF::NACC + r][lane] = acc[i][j][r];
+    __syncthreads();
+    float *__restrict__ C = p.C;
+    const int ldc = p.ldc;
+    for (int q = g; q < NREG; q += KS) {
+        float v = red[0][q][lane];
+#pragma unroll
+        for (int h = 1; h < KS; ++h) v += red[h][q][lane];
+        const int i = q / (TN * MF::NACC), j = (q / MF::NACC) % TN, r = q % MF::NACC;
+        const int row = m0 + i * MI + MF::row(lane, r);
+        const int col = n0 + j * MI + lrow;
+        if (row < M && col < N) C[row * ldc + col] = (p.relu && v < 0.f) ? 0.f : v;
+    }
+}
+
+template <int MI, int TM, int TN, int KS, int U, int D, bool VEC>
+hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
+    constexpr int BM = MI * TM, BN = MI * TN;
+    const unsigned tiles = (unsigned)(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
+    GemmArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(
+        reinterpret_cast<const void *>(&gemm_f32_ksplit_kernel<MI, TM, TN, KS, U, D, VEC>),
+        dim3(tiles), dim3(KS * 64), kargs, 0, s);
+}
+
 #define XTC_F32_INSTANCE(BM, BN, BK, WM, WN, MI, PAD)                                         \
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 2 : 4), 2, PAD, 0),                 \
@@ -417,16 +583,32 @@ hipError_t launch_f32_dma(const GemmArgs &a, hipStream_t s) {
             &launch_f32<BM, BN, BK, WM, WN, 32, 4, false>, true                               \
     }
 
+// Reduction-split instances: KS waves per MI*TM x MI*TN tile, U fragment
+// sets per K-step, D K-steps in flight per wave, no LDS staging.
+#define XTC_F32_KSPLIT_INSTANCE(MI, TM, TN, KS, U, D)                                         \
+    GemmInstance {                                                                            \
+        make_sched(MI * TM, MI * TN, U * 4 * (64 / MI), MI * TM, MI * TN, MI, MI,             \
+                   (MI == 32 ? 2 : 4), 0, 0, 0, 0, KS),                                       \
+            &launch_f32_ksplit<MI, TM, TN, KS, U, D, true>,                                   \
+            &launch_f32_ksplit<MI, TM, TN, KS, U, D, false>, true                             \
+    }
+
 const GemmInstance kF32Instances[] = {
     XTC_F32_DMA_INSTANCE(256, 128, 16, 128, 64, 3),
     XTC_F32_DMA_INSTANCE(256, 128, 32, 128, 64, 2),
     XTC_F32_DMA_INSTANCE(128, 128, 32, 64, 64, 2),
     XTC_F32_DMA_INSTANCE(128, 128, 16, 64, 64, 4),
-    XTC_F32_INSTANCE(128, 128, 32, 64, 64, 32, 4),   // default for large problems
+    XTC_F32_INSTANCE(128, 128, 32, 64, 64, 32, 4),
     XTC_F32_INSTANCE(128, 128, 16, 64, 64, 32, 4),
     XTC_F32_INSTANCE(64, 64, 32, 32, 32, 32, 4),     // small problems: more tiles
     XTC_F32_INSTANCE(128, 128, 32, 64, 64, 16, 4),   // 16x16x4 instruction tile
     XTC_F32_INSTANCE(256, 128, 16, 128, 64, 32, 4),
+    XTC_F32_KSPLIT_INSTANCE(32, 1, 1, 4, 4, 4),      // 32x32 tiles, 4 waves
+    XTC_F32_KSPLIT_INSTANCE(32, 1, 1, 8, 4, 4),      // 32x32 tiles, 8 waves
+    XTC_F32_KSPLIT_INSTANCE(32, 2, 1, 4, 2, 4),      // 64x32 tiles
+    XTC_F32_KSPLIT_INSTANCE(32, 2, 2, 4, 2, 3),      // 64x64 tiles
+    XTC_F32_KSPLIT_INSTANCE(16, 1, 1, 4, 2, 4),      // 16x16 tiles, 16x16x4 instruction
+    XTC_F32_KSPLIT_INSTANCE(16, 1, 1, 8, 2, 4),      // 16x16 tiles, 8 waves
 };
 
 }  // namespace

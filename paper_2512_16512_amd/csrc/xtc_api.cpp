@@ -25,7 +25,8 @@ bool same_instance(const xtc_sched &a, const xtc_sched &b) {
     return a.block_m == b.block_m && a.block_n == b.block_n && a.block_k == b.block_k &&
            a.wave_m == b.wave_m && a.wave_n == b.wave_n && a.mfma_m == b.mfma_m &&
            a.mfma_n == b.mfma_n && a.mfma_k == b.mfma_k && a.lds_stages == b.lds_stages &&
-           a.lds_pad == b.lds_pad && a.unroll_k == b.unroll_k && a.k_order == b.k_order;
+           a.lds_pad == b.lds_pad && a.unroll_k == b.unroll_k && a.k_order == b.k_order &&
+           a.k_split == b.k_split;
 }
 
 bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -38,8 +39,13 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
         !pow2(s.wave_n))
         return XTC_ERR_BAD_SCHEDULE;
     if (s.block_m % s.wave_m || s.block_n % s.wave_n) return XTC_ERR_BAD_SCHEDULE;
-    const int waves = (s.block_m / s.wave_m) * (s.block_n / s.wave_n);
+    if (s.k_split != 1 && s.k_split != 2 && s.k_split != 4 && s.k_split != 8)
+        return XTC_ERR_BAD_SCHEDULE;
+    const int waves = (s.block_m / s.wave_m) * (s.block_n / s.wave_n) * s.k_split;
     if (waves < 1 || waves > 16) return XTC_ERR_BAD_SCHEDULE;  // <= 1024 threads
+    if (s.k_split > 1 && (s.wave_m != s.block_m || s.wave_n != s.block_n || s.lds_stages != 0 ||
+                          op != XTC_OP_MATMUL))
+        return XTC_ERR_BAD_SCHEDULE;
     // instruction tiles the matrix cores offer for this dtype
     if (s.mfma_m != s.mfma_n) return XTC_ERR_BAD_SCHEDULE;
     if (dt == XTC_F32) {
@@ -52,7 +58,7 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     if (s.wave_m % s.mfma_m || s.wave_n % s.mfma_n) return XTC_ERR_BAD_SCHEDULE;
     const int kchunk = dt == XTC_F32 ? 4 * (64 / s.mfma_m) : s.mfma_k;
     if (s.block_k % kchunk) return XTC_ERR_BAD_SCHEDULE;
-    if (s.lds_stages < 1 || s.lds_stages > 4) return XTC_ERR_BAD_SCHEDULE;
+    if (s.lds_stages < (s.k_split > 1 ? 0 : 1) || s.lds_stages > 4) return XTC_ERR_BAD_SCHEDULE;
     if (s.lds_pad < -1 || s.lds_pad > 64) return XTC_ERR_BAD_SCHEDULE;
     if (s.unroll_k < 0) return XTC_ERR_BAD_SCHEDULE;
     if (s.raster < 0 || s.xcd_remap < 0 || s.xcd_remap > 1) return XTC_ERR_BAD_SCHEDULE;
@@ -61,8 +67,9 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     // LDS budget of the staged tiles
     const int elt = dt == XTC_F32 ? 4 : 2;
     const int pad = s.lds_pad > 0 ? s.lds_pad : 0;
-    const int64_t lds = (int64_t)s.lds_stages * elt *
-                        ((int64_t)s.block_m * (s.block_k + pad) + (int64_t)s.block_n * (s.block_k + 8));
+    int64_t lds = (int64_t)s.lds_stages * elt *
+                  ((int64_t)s.block_m * (s.block_k + pad) + (int64_t)s.block_n * (s.block_k + 8));
+    if (s.k_split > 1) lds += (int64_t)s.k_split * s.block_m * s.block_n * 4;  // partial sums
     if (lds > kLdsBytes) return XTC_ERR_BAD_SCHEDULE;
     if (op == XTC_OP_CONV2D && dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
     return XTC_OK;
@@ -140,11 +147,20 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
         return XTC_OK;
     }
     if (dt == XTC_F32) {
-        // Large tiles once they still give at least one tile per CU.
+        // Large tiles once they still give at least one tile per CU; below
+        // that, the largest reduction-split tile that does (measured over
+        // 16x16 .. 128x128 tiles on shapes from 256^3 to 2048^3 and skinny
+        // ones such as 128x128x4096 and 64x4096x1024).
         if (tiles(128, 128) >= cus)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0);
+        else if (tiles(64, 64) >= cus)
+            *out = make_sched(64, 64, 16, 64, 64, 32, 32, 2, 0, 0, 0, 0, 4);
+        else if (tiles(64, 32) >= cus)
+            *out = make_sched(64, 32, 16, 64, 32, 32, 32, 2, 0, 0, 0, 0, 4);
+        else if (tiles(32, 32) >= cus)
+            *out = make_sched(32, 32, 32, 32, 32, 32, 32, 2, 0, 0, 0, 0, K >= 1024 ? 8 : 4);
         else
-            *out = make_sched(64, 64, 32, 32, 32, 32, 32, 2, 2, 4, 0);
+            *out = make_sched(16, 16, 32, 16, 16, 16, 16, 4, 0, 0, 0, 0, 4);
     } else {
         if (tiles(256, 256) >= cus)
             *out = make_sched(256, 256, 32, 128, 64, 32, 32, 16, 4, -1, 0);

@@ -66,7 +66,8 @@ constexpr int kConvMaxK = 4096;
 
 // Fills the fields of a schedule descriptor.
 inline xtc_sched make_sched(int bm, int bn, int bk, int wm, int wn, int mm, int mn, int mk,
-                            int stages, int pad, int unroll, int k_order = 0) {
+                            int stages, int pad, int unroll, int k_order = 0,
+                            int k_split = 1) {
     xtc_sched s;
     s.size = (int32_t)sizeof(xtc_sched);
     s.block_m = bm; s.block_n = bn; s.block_k = bk;
@@ -75,6 +76,7 @@ inline xtc_sched make_sched(int bm, int bn, int bk, int wm, int wn, int mm, int 
     s.lds_stages = stages; s.lds_pad = pad; s.unroll_k = unroll;
     s.raster = 0; s.xcd_remap = 1;
     s.k_order = k_order;
+    s.k_split = k_split;
     return s;
 }
 

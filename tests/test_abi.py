@@ -124,7 +124,8 @@ def _base(x, dt=0):
 @pytest.mark.parametrize("field,value", [
     ("block_m", 96), ("block_n", 0), ("wave_m", 512), ("mfma_m", 8), ("mfma_k", 16),
     ("lds_stages", 0), ("lds_pad", -2), ("raster", -1), ("xcd_remap", 2), ("block_k", 4),
-    ("size", 12), ("k_order", 1), ("k_order", -1),
+    ("size", 12), ("k_order", 1), ("k_order", -1), ("k_split", 0), ("k_split", 3),
+    ("k_split", 16),
 ])
 def test_sched_illegal_fields(x, field, value):
     s = _base(x)
@@ -181,3 +182,23 @@ def test_one_hip_runtime_whatever_the_import_order():
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT)
     assert r.returncode == 0, r.stderr
     assert r.stdout.strip().splitlines()[-1] == "1"
+
+
+def test_k_split_rules(x):
+    ks = [s for s in x.xtc_sched_list(0, 0) if s.k_split > 1]
+    assert ks, "no reduction-split fp32 instance compiled"
+    s = x.Sched(**ks[0].as_dict())
+    assert x.xtc_sched_check(0, 0, s) == 0
+    bad = x.Sched(**s.as_dict())
+    bad.wave_m = s.block_m // 2            # split waves must cover the whole tile
+    assert x.xtc_sched_check(0, 0, bad) == 5
+    bad = x.Sched(**s.as_dict())
+    bad.lds_stages = 2                     # the split kernels stage nothing in LDS
+    assert x.xtc_sched_check(0, 0, bad) == 5
+    bad = x.Sched(**s.as_dict())
+    bad.k_split = 2                        # legal value, not compiled
+    assert x.xtc_sched_check(0, 0, bad) in (0, 6)
+    conv = x.Sched(**x.xtc_sched_list(1, 0)[0].as_dict())
+    conv.k_split = 2
+    assert x.xtc_sched_check(1, 0, conv) == 5
+    assert x.Sched().k_split == 1          # the Python default
