@@ -218,6 +218,21 @@ xtc_status xtc_sched_check(xtc_op op, xtc_dtype dtype, const xtc_sched *s);
  */
 int32_t xtc_sched_list(xtc_op op, xtc_dtype dtype, xtc_sched *out, int32_t cap);
 
+/*
+ * xtc_sched_occupancy -- how many workgroups of the kernel instance `s`
+ * names one CU holds at once (the hardware limit set by the kernel's
+ * registers, LDS and threads), for reduction length K (matmul: K; conv2d:
+ * C*R*S, which sizes the conv kernels' LDS k-offset table).  For a conv
+ * tap-major instance the figure is that of the tap-major kernel itself, not
+ * of the channel-major kernel it falls back to when C % 32 != 0.  Queries
+ * the current HIP device; enqueues nothing.  Errors: XTC_ERR_NULL_POINTER,
+ * the codes of xtc_sched_check, XTC_ERR_BAD_SHAPE (K < 0),
+ * XTC_ERR_TOO_LARGE (conv K above xtc_conv_max_k(), or K > 2^30),
+ * XTC_ERR_HIP.
+ */
+xtc_status xtc_sched_occupancy(xtc_op op, xtc_dtype dtype, int64_t K,
+                               const xtc_sched *s, int32_t *wg_per_cu);
+
 /* Static description of a status code. */
 const char *xtc_status_str(xtc_status s);
 

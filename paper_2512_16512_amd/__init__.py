@@ -99,6 +99,8 @@ def _load():
     lib.xtc_default_schedule.restype = i32
     lib.xtc_sched_check.argtypes = [i32, i32, sp]
     lib.xtc_sched_check.restype = i32
+    lib.xtc_sched_occupancy.argtypes = [i32, i32, i64, sp, ctypes.POINTER(i32)]
+    lib.xtc_sched_occupancy.restype = i32
     lib.xtc_sched_list.argtypes = [i32, i32, sp, i32]
     lib.xtc_sched_list.restype = i32
     lib.xtc_status_str.argtypes = [i32]
@@ -116,7 +118,7 @@ _lib = _load()
 
 # Every symbol include/xtc.h declares.
 EXPORTS = ("xtc_matmul", "xtc_conv2d_nchw", "xtc_matmul_relu", "xtc_conv2d_nchw_relu",
-           "xtc_default_schedule", "xtc_sched_check",
+           "xtc_default_schedule", "xtc_sched_occupancy", "xtc_sched_check",
            "xtc_sched_list", "xtc_status_str", "xtc_last_hip_error", "xtc_conv_max_k",
            "xtc_version")
 
@@ -158,6 +160,15 @@ def xtc_default_schedule(op, dtype, M, N, K) -> Sched:
 
 def xtc_sched_check(op, dtype, sched) -> int:
     return _lib.xtc_sched_check(op, dtype, _sp(sched))
+
+
+def xtc_sched_occupancy(op, dtype, K, sched) -> int:
+    """Workgroups of the instance ``sched`` names that one CU holds at once."""
+    n = ctypes.c_int32(0)
+    st = _lib.xtc_sched_occupancy(op, dtype, K, _sp(sched), ctypes.byref(n))
+    if st != XTC_OK:
+        raise XtcError(st, "xtc_sched_occupancy")
+    return n.value
 
 
 def xtc_sched_list(op, dtype):

@@ -754,20 +754,26 @@ hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
 #define XTC_CONV_INSTANCE(BM, BN, BK, WM, WN, MI, PAD)                                        \
     ConvInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 2 : 4), 2, PAD, 0),                 \
-            &launch_conv_f32<BM, BN, BK, WM, WN, MI, PAD>                                     \
+            &launch_conv_f32<BM, BN, BK, WM, WN, MI, PAD>,                                    \
+            &occupancy_of<&conv2d_f32_kernel<BM, BN, BK, WM, WN, MI, PAD, true>,              \
+                          (BM / WM) * (BN / WN) * 64, (int)sizeof(int2)>                      \
     }
 
 #define XTC_CONV_DMA_INSTANCE(BM, BN, BK, WM, WN, STAGES)                                     \
     ConvInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, 32, 32, 2, STAGES, -1, 0),                             \
-            &launch_conv_f32_dma<BM, BN, BK, WM, WN, STAGES>                                  \
+            &launch_conv_f32_dma<BM, BN, BK, WM, WN, STAGES>,                                 \
+            &occupancy_of<&conv2d_f32_dma_kernel<BM, BN, BK, WM, WN, STAGES>,                 \
+                          (BM / WM) * (BN / WN) * 64, (int)sizeof(int2)>                      \
     }
 
 // Tap-major direct-to-LDS instances (k_order = 1).
 #define XTC_CONV_TAP_INSTANCE(BM, BN, WM, WN, STAGES, FB)                                     \
     ConvInstance {                                                                            \
         make_sched(BM, BN, 32, WM, WN, 32, 32, 2, STAGES, -1, 0, 1),                          \
-            &launch_conv_f32_tap<BM, BN, WM, WN, STAGES, FB>                                  \
+            &launch_conv_f32_tap<BM, BN, WM, WN, STAGES, FB>,                                 \
+            &occupancy_of<&conv2d_f32_tap_kernel<BM, BN, WM, WN, STAGES>,                     \
+                          (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
 const ConvInstance kConvInstances[] = {

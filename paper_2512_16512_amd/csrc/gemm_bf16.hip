@@ -549,7 +549,9 @@ hipError_t launch_bf16(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), 2, PAD, 0),               \
             &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, true>,                                  \
-            &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, false>, false                           \
+            &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, false>, false,                          \
+            &occupancy_of<&gemm_bf16_kernel<BM, BN, BK, WM, WN, MI, PAD, true>,               \
+                          (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
 // Direct-to-LDS ring (lds_pad = -1: swizzled, unpadded LDS rows), b128 A
@@ -560,7 +562,9 @@ hipError_t launch_bf16(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), STAGES, -1, 0),           \
             &launch_bf16_dma<BM, BN, BK, WM, WN, MI, STAGES, 0, 1>,                           \
-            &launch_bf16<BM, BN, BK, WM, WN, MI, 8, false>, true                              \
+            &launch_bf16<BM, BN, BK, WM, WN, MI, 8, false>, true,                             \
+            &occupancy_of<&gemm_bf16_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES, 0, 1>,        \
+                          (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
 const GemmInstance kBf16Instances[] = {

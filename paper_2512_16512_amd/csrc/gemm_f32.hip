@@ -572,7 +572,9 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 2 : 4), 2, PAD, 0),                 \
             &launch_f32<BM, BN, BK, WM, WN, MI, PAD, true>,                                   \
-            &launch_f32<BM, BN, BK, WM, WN, MI, PAD, false>, false                            \
+            &launch_f32<BM, BN, BK, WM, WN, MI, PAD, false>, false,                           \
+            &occupancy_of<&gemm_f32_kernel<BM, BN, BK, WM, WN, MI, PAD, true>,                \
+                          (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
 // Direct-to-LDS ring (lds_pad = -1); register-staged fallback, same tiles.
@@ -580,7 +582,9 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, 32, 32, 2, STAGES, -1, 0),                             \
             &launch_f32_dma<BM, BN, BK, WM, WN, STAGES>,                                      \
-            &launch_f32<BM, BN, BK, WM, WN, 32, 4, false>, true                               \
+            &launch_f32<BM, BN, BK, WM, WN, 32, 4, false>, true,                              \
+            &occupancy_of<&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, STAGES>,                   \
+                          (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
 // Reduction-split instances: KS waves per MI*TM x MI*TN tile, U fragment
@@ -590,7 +594,8 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
         make_sched(MI * TM, MI * TN, U * 4 * (64 / MI), MI * TM, MI * TN, MI, MI,             \
                    (MI == 32 ? 2 : 4), 0, 0, 0, 0, KS),                                       \
             &launch_f32_ksplit<MI, TM, TN, KS, U, D, true>,                                   \
-            &launch_f32_ksplit<MI, TM, TN, KS, U, D, false>, true                             \
+            &launch_f32_ksplit<MI, TM, TN, KS, U, D, false>, true,                            \
+            &occupancy_of<&gemm_f32_ksplit_kernel<MI, TM, TN, KS, U, D, true>, KS * 64, 0>    \
     }
 
 const GemmInstance kF32Instances[] = {

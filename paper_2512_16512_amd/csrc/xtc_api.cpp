@@ -184,6 +184,22 @@ xtc_status xtc_sched_check(xtc_op op, xtc_dtype dt, const xtc_sched *s) {
     return find_conv(*s) ? XTC_OK : XTC_ERR_UNSUPPORTED_SCHEDULE;
 }
 
+xtc_status xtc_sched_occupancy(xtc_op op, xtc_dtype dt, int64_t K, const xtc_sched *s,
+                               int32_t *wg_per_cu) {
+    if (!s || !wg_per_cu) return XTC_ERR_NULL_POINTER;
+    const xtc_status st = xtc_sched_check(op, dt, s);
+    if (st != XTC_OK) return st;
+    if (K < 0) return XTC_ERR_BAD_SHAPE;
+    if (op == XTC_OP_CONV2D && K > kConvMaxK) return XTC_ERR_TOO_LARGE;
+    if (K > (int64_t)1 << 30) return XTC_ERR_TOO_LARGE;
+    OccupancyFn fn = op == XTC_OP_MATMUL ? find_gemm(dt, *s)->occupancy : find_conv(*s)->occupancy;
+    int n = 0;
+    const xtc_status hs = hip_status(fn((int)K, &n));
+    if (hs != XTC_OK) return hs;
+    *wg_per_cu = n;
+    return XTC_OK;
+}
+
 int32_t xtc_sched_list(xtc_op op, xtc_dtype dt, xtc_sched *out, int32_t cap) {
     int n = 0;
     if (op == XTC_OP_MATMUL && dt == XTC_F32) {

@@ -41,6 +41,17 @@ struct ConvArgs {
 using GemmLaunch = hipError_t (*)(const GemmArgs &, hipStream_t);
 using ConvLaunch = hipError_t (*)(const ConvArgs &, hipStream_t);
 
+// Resident workgroups per CU of one kernel (the hardware limit set by its
+// registers, LDS and threads) at reduction length K, which sizes the dynamic
+// LDS of the conv kernels' k-offset table.
+using OccupancyFn = hipError_t (*)(int K, int *wg_per_cu);
+template <auto KERNEL, int THREADS, int DYN_BYTES_PER_K>
+hipError_t occupancy_of(int K, int *wg_per_cu) {
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        wg_per_cu, reinterpret_cast<const void *>(KERNEL), THREADS,
+        (size_t)DYN_BYTES_PER_K * (size_t)K);
+}
+
 // One compiled kernel instance.  `vec_launch` requires 16-byte aligned
 // operand rows (base pointers and leading dimensions) and, when
 // `vec_whole_chunks` is set, also K and N to be multiples of 16 bytes of
@@ -50,11 +61,13 @@ struct GemmInstance {
     GemmLaunch vec_launch;
     GemmLaunch any_launch;
     bool vec_whole_chunks;
+    OccupancyFn occupancy;  // of the kernel vec_launch runs
 };
 
 struct ConvInstance {
     xtc_sched sched;
     ConvLaunch launch;
+    OccupancyFn occupancy;  // of the instance's own kernel (not its fallbacks)
 };
 
 const GemmInstance *gemm_f32_instances(int *count);

@@ -1,0 +1,208 @@
+"""Analytic model of the HBM traffic of a matmul schedule, and its evaluation
+against hardware counters.
+
+The GPU counterpart of the paper's cache-model study (Sec. 6.3, Fig. 13,
+Table 2): a model predicts, for every schedule of a design space, the misses
+of one cache level; the schedules are run under the counter profiler and the
+prediction is compared with the counter by Pearson's r and Spearman's rho.
+The paper models the L1 of a CPU core as one fully associative cache; here the
+level that decides HBM traffic is the L2 of each of the MI355X's 8 XCDs
+(4 MiB each, private), which the L2 miss counters (FETCH_SIZE) measure.
+
+Model.  The dispatcher hands workgroup ids to the XCDs round-robin (id % 8)
+and each XCD runs its ids in order, ``occupancy`` workgroups per CU on its 32
+CUs at once, so each XCD works through consecutive groups of
+``32 * occupancy`` of its tiles (the workgroup -> tile map is the library's
+raster order and XCD remap).  Workgroups of one group advance through K at
+about the same pace, so an A row-panel or B column-panel shared by several of
+them is fetched from HBM once per group; nothing is assumed to survive from
+one group to the next, unless everything the XCD touches fits in its L2,
+in which case every panel is fetched once per XCD.  Predicted read bytes are
+the sum over XCDs and groups of (distinct A row-panels) x rows x K x elt +
+(distinct B column-panels) x columns x K x elt; the output is written once
+(M x N x 4 bytes).  The model ignores cache-line granularity, the replacement
+policy, and timing skew between workgroups.
+
+Usage (the measurement step runs under rocprofv3; see ``run``)::
+
+    rocprofv3 --pmc FETCH_SIZE -f csv -d OUT -o run -- \\
+        python3 -m paper_2512_16512_amd.traffic_model run f32 4096 4096 4096 --order ORDER.json
+    python -m paper_2512_16512_amd.traffic_model correlate ORDER.json OUT/run_counter_collection.csv \\
+        --fetch-scale 2.0
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import sys
+
+XCDS = 8
+CUS_PER_XCD = 32
+L2_BYTES = 4 << 20
+
+
+def tile_coords(bid: int, grid: int, tiles_m: int, tiles_n: int, raster: int, xcd_remap: int):
+    """Tile (tm, tn) of workgroup ``bid``: the same map the kernels apply
+    (XCD remap into contiguous bands per XCD, then the raster order)."""
+    if xcd_remap and grid >= XCDS:
+        x, q, rem = bid % XCDS, grid // XCDS, grid % XCDS
+        bid = x * q + min(x, rem) + bid // XCDS
+    if raster == 1:
+        return bid % tiles_m, bid // tiles_m
+    if raster >= 2:
+        per = raster * tiles_n
+        grp = bid // per
+        first = grp * raster
+        gsz = min(tiles_m - first, raster)
+        r = bid - grp * per
+        return first + r % gsz, r // gsz
+    return bid // tiles_n, bid % tiles_n
+
+
+def predict(M: int, N: int, K: int, elt: int, block_m: int, block_n: int, raster: int,
+            xcd_remap: int, occupancy: int, l2_bytes: int = L2_BYTES):
+    """Predicted HBM (read, write) bytes of one launch."""
+    tiles_m = -(-M // block_m)
+    tiles_n = -(-N // block_n)
+    grid = tiles_m * tiles_n
+    rows = [min(block_m, M - t * block_m) for t in range(tiles_m)]
+    cols = [min(block_n, N - t * block_n) for t in range(tiles_n)]
+    conc = max(1, CUS_PER_XCD * max(1, occupancy))
+    read = 0
+    for x in range(XCDS):
+        ids = range(x, grid, XCDS)
+        tiles = [tile_coords(b, grid, tiles_m, tiles_n, raster, xcd_remap) for b in ids]
+        all_m = {t[0] for t in tiles}
+        all_n = {t[1] for t in tiles}
+        footprint = (sum(rows[m] for m in all_m) + sum(cols[n] for n in all_n)) * K * elt
+        if footprint <= l2_bytes:
+            read += footprint
+            continue
+        for g0 in range(0, len(tiles), conc):
+            grp = tiles[g0:g0 + conc]
+            read += (sum(rows[m] for m in {t[0] for t in grp}) +
+                     sum(cols[n] for n in {t[1] for t in grp})) * K * elt
+    return read, 4 * M * N
+
+
+def _ranks(v):
+    """Ranks 1..n with ties given their average rank."""
+    order = sorted(range(len(v)), key=lambda i: v[i])
+    r = [0.0] * len(v)
+    i = 0
+    while i < len(order):
+        j = i
+        while j + 1 < len(order) and v[order[j + 1]] == v[order[i]]:
+            j += 1
+        avg = (i + j) / 2.0 + 1.0
+        for k in range(i, j + 1):
+            r[order[k]] = avg
+        i = j + 1
+    return r
+
+
+def pearson(x, y) -> float:
+    n = len(x)
+    mx, my = sum(x) / n, sum(y) / n
+    sxy = sum((a - mx) * (b - my) for a, b in zip(x, y))
+    sxx = sum((a - mx) ** 2 for a in x)
+    syy = sum((b - my) ** 2 for b in y)
+    if sxx == 0 or syy == 0:
+        return float("nan")   # undefined for a constant series
+    return sxy / (sxx * syy) ** 0.5
+
+
+def spearman(x, y) -> float:
+    return pearson(_ranks(x), _ranks(y))
+
+
+# ---------------------------------------------------------------- measuring
+
+
+def run(dtype: str, M: int, N: int, K: int, order_path: str, reps: int = 2, rasters=(0, 1, 4, 8, 16)):
+    """Launch every schedule of the design space ``reps`` times, in a fixed
+    order, and write that order (with each schedule's occupancy) to
+    ``order_path``, so that the profiler's per-dispatch counter rows can be
+    matched to schedules afterwards."""
+    import torch
+
+    import paper_2512_16512_amd as xtc
+    from paper_2512_16512_amd import tune
+    p = tune.Problem("matmul", dtype, (M, N, K))
+    space = tune.design_space(xtc.XTC_OP_MATMUL, p.code, rasters=rasters)
+    entries = []
+    stream = torch.cuda.current_stream().cuda_stream
+    for s in space:
+        occ = xtc.xtc_sched_occupancy(xtc.XTC_OP_MATMUL, p.code, K, s)
+        for _ in range(reps):
+            p.launch(s, stream)
+        torch.cuda.synchronize()
+        entries.append({"sched": s.as_dict(), "occupancy": occ})
+    with open(order_path, "w") as f:
+        json.dump({"dtype": dtype, "M": M, "N": N, "K": K, "reps": reps, "schedules": entries}, f)
+    print("launched %d schedules x %d" % (len(entries), reps), flush=True)
+
+
+def _counter_rows(csv_path: str, counter: str):
+    import csv
+    rows = {}
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] != counter or "xtc::" not in r["Kernel_Name"]:
+            continue
+        d = int(r["Dispatch_Id"])
+        rows[d] = rows.get(d, 0.0) + float(r["Counter_Value"])
+    return [rows[d] for d in sorted(rows)]
+
+
+def correlate(order_path: str, fetch_csv: str, fetch_scale: float):
+    """Predicted vs measured (FETCH_SIZE x 1024 x fetch_scale) bytes per
+    schedule; returns the table rows and the two correlation statistics."""
+    o = json.load(open(order_path))
+    vals = _counter_rows(fetch_csv, "FETCH_SIZE")
+    reps = o["reps"]
+    if len(vals) != reps * len(o["schedules"]):
+        raise ValueError("%d counter rows for %d schedules x %d launches"
+                         % (len(vals), len(o["schedules"]), reps))
+    elt = 4 if o["dtype"] == "f32" else 2
+    table = []
+    for i, e in enumerate(o["schedules"]):
+        s = e["sched"]
+        meas = sum(vals[i * reps:(i + 1) * reps]) / reps * 1024 * fetch_scale
+        pred, _ = predict(o["M"], o["N"], o["K"], elt, s["block_m"], s["block_n"], s["raster"],
+                          s["xcd_remap"], e["occupancy"])
+        table.append({"sched": s, "occupancy": e["occupancy"], "predicted": pred,
+                      "measured": meas})
+    x = [t["predicted"] for t in table]
+    y = [t["measured"] for t in table]
+    return table, pearson(x, y), spearman(x, y)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    r = sub.add_parser("run")
+    r.add_argument("dtype", choices=["f32", "bf16"])
+    r.add_argument("M", type=int)
+    r.add_argument("N", type=int)
+    r.add_argument("K", type=int)
+    r.add_argument("--order", required=True)
+    r.add_argument("--reps", type=int, default=2)
+    c = sub.add_parser("correlate")
+    c.add_argument("order")
+    c.add_argument("fetch_csv")
+    c.add_argument("--fetch-scale", type=float, required=True)
+    c.add_argument("--json", default=None)
+    a = ap.parse_args(argv)
+    if a.cmd == "run":
+        run(a.dtype, a.M, a.N, a.K, a.order, a.reps)
+        return 0
+    table, r_, rho = correlate(a.order, a.fetch_csv, a.fetch_scale)
+    print("schedules %d  Pearson r = %.3f  Spearman rho = %.3f" % (len(table), r_, rho))
+    if a.json:
+        with open(a.json, "w") as f:
+            json.dump({"pearson": r_, "spearman": rho, "rows": table}, f, indent=1)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -202,3 +202,19 @@ def test_k_split_rules(x):
     conv.k_split = 2
     assert x.xtc_sched_check(1, 0, conv) == 5
     assert x.Sched().k_split == 1          # the Python default
+
+
+def test_occupancy_query_validation(x):
+    import ctypes
+    s = x.xtc_sched_list(0, 0)[0]
+    n = ctypes.c_int32(-1)
+    lib = x._lib
+    assert lib.xtc_sched_occupancy(0, 0, 64, None, ctypes.byref(n)) == 1
+    assert lib.xtc_sched_occupancy(0, 0, 64, ctypes.byref(s), None) == 1
+    assert lib.xtc_sched_occupancy(0, 0, -1, ctypes.byref(s), ctypes.byref(n)) == 2
+    bad = x.Sched(**s.as_dict())
+    bad.block_m = 96
+    assert lib.xtc_sched_occupancy(0, 0, 64, ctypes.byref(bad), ctypes.byref(n)) == 5
+    c = x.xtc_sched_list(1, 0)[0]
+    assert lib.xtc_sched_occupancy(1, 0, 5000, ctypes.byref(c), ctypes.byref(n)) == 7
+    assert n.value == -1                  # nothing written on an error

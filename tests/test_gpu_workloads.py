@@ -199,3 +199,14 @@ def test_graph_replay_matches_eager(x):
         assert torch.equal(c, eager), "replay %d differs from the eager result" % rep
     ref = oracle.relu(oracle.matmul(A, B))
     assert_parity(to_host(c), ref, "f32", "graph replay")
+
+
+def test_every_instance_fits_on_a_cu(x):
+    # the occupancy query: every compiled instance has at least one resident
+    # workgroup per CU at the reduction lengths it is used with
+    for op, dt in ((x.XTC_OP_MATMUL, x.XTC_F32), (x.XTC_OP_MATMUL, x.XTC_BF16),
+                   (x.XTC_OP_CONV2D, x.XTC_F32)):
+        for s in x.xtc_sched_list(op, dt):
+            for K in (1, 576, 4096):
+                n = x.xtc_sched_occupancy(op, dt, K, s)
+                assert 1 <= n <= 32, (op, dt, K, s, n)
