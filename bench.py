@@ -39,9 +39,9 @@ METRIC = "matmul TFLOP/s (fp32, bf16) and % of MI355X MFMA peak at 1 GPU"
 PEAK = {"f32": 157.3, "bf16": 2516.6}
 HBM_GBS = 8000.0
 KERNEL_SOURCES = {
-    "f32": ["gemm_f32.hip", "mfma_f32.h", "tile_map.h"],
-    "bf16": ["gemm_bf16.hip", "tile_map.h"],
-    "conv": ["conv2d_f32.hip", "mfma_f32.h", "tile_map.h"],
+    "f32": ["gemm_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h"],
+    "bf16": ["gemm_bf16.hip", "tile_map.h", "lds_dma.h"],
+    "conv": ["conv2d_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h"],
 }
 
 
