@@ -86,7 +86,12 @@ typedef enum {
  *                (ic, kh, kw).  0: channel-major, k = (ic*R + kh)*S + kw (the
  *                OIHW weight layout); 1: tap-major, k = (kh*S + kw)*C + ic
  *                (needs C % 32 == 0, else the channel-major kernel with the
- *                same tiles runs).  Results differ only by rounding order.
+ *                same tiles runs); 2: chunks of 8 channels, and inside a
+ *                chunk the R*S taps, k = ((ic/8)*R*S + kh*S + kw)*8 + ic%8,
+ *                with each chunk's input patch staged once for all taps
+ *                (3x3, stride 1, C % 16 == 0, W + pad_w <= 60 and OW >= 51;
+ *                other shapes run the tap-major kernel with the same tiles).
+ *                Results differ only by rounding order.
  *  k_split       waves that share one workgroup tile, each reducing every
  *                k_split-th group of block_k reduction steps (a parallel
  *                split of the reduction for problems with too few tiles to

@@ -16,6 +16,8 @@
 // mapping k to (ic*H*W + kh*W + kw, kh, kw), so the gather needs no integer
 // division in the main loop: an element (k, q) is X[base(q) + off(k)] when
 // 0 <= ih0(q) + kh < H and 0 <= iw0(q) + kw < W, else zero.
+#include <type_traits>
+
 #include "lds_dma.h"
 #include "mfma_f32.h"
 #include "tile_map.h"
@@ -738,6 +740,250 @@ hipError_t launch_conv_f32_tap(const ConvArgs &a, hipStream_t s) {
                            dim3(tiles), dim3(G::NT), kargs, 0, s);
 }
 
+// ---------------------------------------------------------------------------
+// Halo-tiled kernel (k_order = 2) for stride-1 3x3 convolutions of rows about
+// 56 pixels wide.  The tap-major kernel gathers every input value once per
+// tap (nine gather copies per input value for 3x3); here a stage holds an
+// 8-channel input patch that all nine taps read from LDS:
+//  - a workgroup computes 64 output channels x 256 consecutive output pixels
+//    of one image (flat oh*OW + ow order, four 64x64 waves).  Those pixels
+//    span at most 6 output rows when OW >= 51, so their inputs fit in a patch
+//    of PR = 8 input rows per channel;
+//  - the patch stores input row ih of channel c at LDS row (c, ih - ih0),
+//    64 columns wide, input column iw at column iw + 4 (left and right
+//    padding and rows outside the image read as zero).  One dword copy of 64
+//    lanes fills one patch row: lane l fetches column l - 4, a fixed vector
+//    offset, and (image, channel, row) go into the scalar offset;
+//  - the stage's weights W[oc][c0 .. c0+7][kh][kw] are a dword gather into
+//    [tap][oc][8 channels] (one 16-byte read per MFMA A fragment, as in the
+//    tap-major kernel);
+//  - the reduction runs over channel chunks, and inside a chunk over the nine
+//    taps: a tap is one MFMA k-step of 8 channels.  An output pixel's B value
+//    for (channel, tap) is patch[(c, r + kh, ow - pw + kw + 4)], so every
+//    B fragment read is one ds_read_b32 at a per-lane base plus a constant.
+// Patch planes are 8*64 + 8 floats apart, which puts the two lane groups of
+// a fragment read (channels c and c + 4) 32 banks apart.
+namespace halo {
+constexpr int BM = 64, BN = 256, WM = 64, WN = 64, NWAVES = 4, NT = 256;
+constexpr int MI = 32, TM = WM / MI, TN = WN / MI;
+constexpr int CC = 8;                         // channels per stage
+constexpr int NTAP = 9;                       // 3x3 taps, one MFMA k-step each
+constexpr int PR = 8;                         // patch rows per channel
+constexpr int PLANE = PR * 64 + 8;            // floats per channel plane
+constexpr int A_FLOATS = NTAP * BM * CC;      // [tap][oc][c]
+constexpr int A_BYTES = A_FLOATS * 4;
+constexpr int B_BYTES = CC * PLANE * 4;
+constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+constexpr int A_COPIES = A_FLOATS / 64;       // 72
+constexpr int A_PER_WAVE = A_COPIES / NWAVES; // 18
+constexpr int B_COPIES = CC * PR;             // 64
+constexpr int B_PER_WAVE = B_COPIES / NWAVES; // 16: two channels x eight rows
+constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;
+constexpr int CO = 4;                         // LDS column of input column 0
+constexpr unsigned kOffNone = 0x80000000u;    // scalar offset that puts any lane out of range
+static_assert(A_PER_WAVE * NWAVES == A_COPIES && B_PER_WAVE * NWAVES == B_COPIES, "copy split");
+static_assert((PLANE * 4) % 64 == 32, "lane groups 32 banks apart");
+}  // namespace halo
+
+template <int STAGES>
+__global__ void __launch_bounds__(halo::NT)
+conv2d_f32_halo_kernel(ConvArgs p) {
+    using namespace halo;
+    typedef F32Mfma<MI> MF;
+    static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
+    static_assert(STAGES * STAGE_BYTES <= 80 * 1024, "two workgroups per CU");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * STAGE_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int lrow = lane % MI, lgrp = lane / MI;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+
+    const int C = p.C, H = p.H, Wd = p.W;
+    const int OC = p.OC, OW = p.OW, OHW = p.OH * p.OW;
+    const int chunks = (OHW + BN - 1) / BN;   // per image
+    const int tiles_m = (OC + BM - 1) / BM, tiles_n = p.Nb * chunks;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM;
+    const int img = tn / chunks, p0 = (tn - img * chunks) * BN;
+    const int oh0 = p0 / OW;                  // first output row of the tile
+    const int ih0 = oh0 - p.ph;               // input row of patch row 0
+    const int KT = C / CC;                    // stages (even: C % 16 == 0)
+
+    const i32x4 rw = make_rsrc(p.Wt, OC * C * NTAP * 4);
+    const i32x4 rx = make_rsrc(p.X, p.Nb * C * H * Wd * 4);
+    const unsigned smem_base = lds_address(smem);
+
+    // Copy offsets.  Every copy's address is a fixed per-lane vector offset
+    // plus a scalar offset that moves by a constant per stage, so a stage's
+    // copies need one scalar add each and no conditions:
+    //  - weights: lane l fills slot (oc = 8*ocb + l/8, channel l%8) of a copy;
+    //    a row past OC reads zero through the buffer range check;
+    //  - patch: lane l fills column l (input column l - CO, zero outside the
+    //    row); a patch row outside the image uses the out-of-range vector
+    //    offset (its scalar offset is clamped to a real row so the sum stays
+    //    below 2^32).
+    // Stages past the end (the ring's tail) load whatever their offsets hit
+    // -- in range or zero, never outside the buffers -- and are never used.
+    const int voffA = ((lane >> 3) * C * NTAP + (lane & 7) * NTAP) * 4;
+    const int iwl = lane - CO;
+    const int voffB = (iwl >= 0 && iwl < Wd) ? iwl * 4 : kOOB;
+    int voffR[PR];
+#pragma unroll
+    for (int r = 0; r < PR; ++r) voffR[r] = (ih0 + r >= 0 && ih0 + r < H) ? voffB : kOOB;
+    const int HW4 = H * Wd * 4;
+    const int a_stage = CC * NTAP * 4;       // scalar-offset step per stage
+    const int b_stage = CC * HW4;
+    const int a_base0 = (m0 * C * NTAP) * 4;
+    const int b_base0 = (img * C + wave_u * (CC / NWAVES)) * HW4;
+
+    int so_a = a_base0, so_b = b_base0;      // offsets of the next stage to fire
+    auto fire = [&](int st) {
+        const unsigned base = smem_base + st * STAGE_BYTES;
+#pragma unroll
+        for (int q = 0; q < A_PER_WAVE; ++q) {
+            const int cq = wave_u * A_PER_WAVE + q;          // copy index: tap-major
+            const int tap = cq / 8, ocb = cq % 8;
+            dma4_so(rw, base + (tap * BM * CC + ocb * 64) * 4, voffA,
+                    so_a + (ocb * 8 * C * NTAP + tap) * 4);
+        }
+#pragma unroll
+        for (int q = 0; q < B_PER_WAVE; ++q) {
+            const int cl = q / PR, row = q % PR;             // channel of this wave, patch row
+            const int ihc = min(max(ih0 + row, 0), H - 1);
+            dma4_so(rx, base + A_BYTES + ((wave_u * (CC / NWAVES) + cl) * PLANE + row * 64) * 4,
+                    voffR[row], so_b + cl * HW4 + ihc * Wd * 4);
+        }
+        so_a += a_stage;
+        so_b += b_stage;
+    };
+
+    // Per-lane fragment bases.  A: row (i*32 + lrow), channels 4*lgrp .. +3.
+    // B: this lane's pixel of column block j (clamped to patch position 0 when
+    // past the image; such columns are not stored).
+    const int a_base = ((lrow * CC) + 4 * lgrp) * 4;
+    int b_base[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int pix = p0 + wave * WN + j * MI + lrow;
+        int off = 0;
+        if (pix < OHW) {
+            const int oh = pix / OW, ow = pix - oh * OW;
+            off = (oh - oh0) * 64 + ow - p.pw + CO;
+        }
+        b_base[j] = (4 * lgrp * PLANE + off) * 4;
+    }
+
+    typename MF::acc_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[i][j][r] = 0.f;
+
+    f32x4 af[2][TM];
+    float bfr[2][TN][4];
+    auto load_frags = [&](int st, int tap, int buf) {
+        const unsigned char *As = smem + st * STAGE_BYTES;
+        const unsigned char *Bs = As + A_BYTES;
+        const int kh = tap / 3, kw = tap - 3 * kh;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+            af[buf][i] = *reinterpret_cast<const f32x4 *>(As + a_base + (tap * BM * CC + i * MI * CC) * 4);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            // an opaque base per column block keeps the compiler from pairing
+            // the two blocks' reads into ds_read2_b32, whose second address
+            // would collide with the other lane group's banks
+            int bb = b_base[j];
+            asm volatile("" : "+v"(bb));
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+                bfr[buf][j][s] = *reinterpret_cast<const float *>(Bs + bb + (s * PLANE + kh * 64 + kw) * 4);
+        }
+    };
+    auto mfmas = [&](int buf) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
+    };
+
+    // One stage: nine taps, fragments of tap t + 1 read while tap t runs;
+    // the barrier that frees this stage's slot sits before the last tap.  P
+    // is the fragment buffer of the stage's first tap: with nine taps it
+    // alternates between stages, so the loop body runs two stages.
+    auto stage = [&](int kt, auto par) {
+        constexpr int P = decltype(par)::value;
+        const int st = kt % STAGES;
+#pragma unroll
+        for (int t = 0; t + 1 < NTAP; ++t) {
+            load_frags(st, t + 1, (P + t + 1) & 1);
+            mfmas((P + t) & 1);
+        }
+        wait_vmcnt<(STAGES - 2) * LOADS>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        fire(st);
+        load_frags((kt + 1) % STAGES, 0, (P + NTAP) & 1);
+        mfmas((P + NTAP - 1) & 1);
+    };
+
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s) fire(s);
+    wait_vmcnt<(STAGES - 1) * LOADS>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    load_frags(0, 0, 0);
+    for (int kt = 0; kt < KT; kt += 2) {
+        stage(kt, std::integral_constant<int, 0>());
+        stage(kt + 1, std::integral_constant<int, NTAP & 1>());
+    }
+    wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
+
+    float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int pix = p0 + wave * WN + j * MI + lrow;
+        if (pix >= OHW) continue;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int oc = m0 + i * MI + MF::row(lane, r);
+                if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
+            }
+    }
+}
+
+// Shapes the halo kernel covers; anything else runs the tap-major kernel
+// with the same 64x256 tiles.
+inline bool halo_eligible(const ConvArgs &a) {
+    using namespace halo;
+    if (a.R != 3 || a.S != 3 || a.sh != 1 || a.sw != 1) return false;
+    if (a.C % (2 * CC) != 0 || a.pw > CO) return false;
+    if (a.OW - a.pw + 5 > 63) return false;              // last patch column used (W + pw <= 60)
+    const int span = (BN - 1 + a.OW - 1) / a.OW + 1;      // output rows a tile can touch
+    return span + 2 <= PR;
+}
+
+template <int STAGES>
+hipError_t launch_conv_f32_halo(const ConvArgs &a, hipStream_t s) {
+    if (!halo_eligible(a)) return launch_conv_f32_tap<64, 256, 64, 64, 2, 2>(a, s);
+    const int OHW = a.OH * a.OW;
+    const unsigned tiles = (unsigned)(((a.OC + halo::BM - 1) / halo::BM) * a.Nb *
+                                      ((OHW + halo::BN - 1) / halo::BN));
+    ConvArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_halo_kernel<STAGES>),
+                           dim3(tiles), dim3(halo::NT), kargs, 0, s);
+}
+
 template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD>
 hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
     const int M = a.OC, N = a.Nb * a.OH * a.OW, K = a.C * a.R * a.S;
@@ -777,6 +1023,9 @@ hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
     }
 
 const ConvInstance kConvInstances[] = {
+    ConvInstance{make_sched(64, 256, 8, 64, 64, 32, 32, 2, 2, -1, 0, 2),   // halo, 3x3 stride 1
+                 &launch_conv_f32_halo<2>,
+                 &occupancy_of<&conv2d_f32_halo_kernel<2>, halo::NT, 0>},
     XTC_CONV_TAP_INSTANCE(64, 256, 64, 64, 2, 2),    // default for OC <= 64
     XTC_CONV_TAP_INSTANCE(64, 128, 32, 64, 2, 3),
     XTC_CONV_TAP_INSTANCE(64, 64, 32, 32, 2, 4),

@@ -62,7 +62,7 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     if (s.lds_pad < -1 || s.lds_pad > 64) return XTC_ERR_BAD_SCHEDULE;
     if (s.unroll_k < 0) return XTC_ERR_BAD_SCHEDULE;
     if (s.raster < 0 || s.xcd_remap < 0 || s.xcd_remap > 1) return XTC_ERR_BAD_SCHEDULE;
-    if (s.k_order < 0 || s.k_order > 1 || (op == XTC_OP_MATMUL && s.k_order != 0))
+    if (s.k_order < 0 || s.k_order > 2 || (op == XTC_OP_MATMUL && s.k_order != 0))
         return XTC_ERR_BAD_SCHEDULE;
     // LDS budget of the staged tiles
     const int elt = dt == XTC_F32 ? 4 : 2;
@@ -135,10 +135,12 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     if (op == XTC_OP_CONV2D) {
         if (dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
         // 64x256 tiles of 4 waves (64x64 each) with a two-stage ring: two
-        // workgroups per CU, so up to 512 tiles run in a single wave.  When
+        // workgroups per CU, so up to 512 tiles run in a single wave; the
+        // halo-tiled kernel where the shape allows it (3x3, stride 1, rows
+        // of about 56 pixels), else the tap-major kernel.  When
         // that leaves CUs idle (a small image batch), 64x64 tiles of four
         // 32x32 waves give four times as many workgroups.
-        *out = make_sched(64, 256, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
+        *out = make_sched(64, 256, 8, 64, 64, 32, 32, 2, 2, -1, 0, 2);
         if (M > 64)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
         else if (tiles(64, 256) < cus)

@@ -105,6 +105,10 @@ def test_small_int_exact_every_instance(x, dtype, M, N, K):
     (2, 64, 9, 10, 40, 3, 3, 1, 1),     # C % 32 == 0: tap-major kernel, OC < 64
     (1, 32, 12, 12, 64, 3, 3, 2, 1),    # tap-major, stride 2
     (2, 96, 7, 7, 70, 1, 1, 1, 0),      # tap-major 1x1, three channel chunks, OC > 64
+    (1, 16, 56, 56, 64, 3, 3, 1, 1),    # halo-tiled kernel: 56-wide rows, last tile ragged
+    (2, 32, 54, 53, 70, 3, 3, 1, 1),    # halo: odd width, OC > 64 with a ragged weight tile
+    (1, 16, 57, 55, 20, 3, 3, 1, 0),    # halo: no padding (53 x 55 output)
+    (1, 48, 56, 56, 16, 3, 3, 1, 2),    # halo: pad 2 (58-wide output rows), six stages
 ])
 def test_conv_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape
