@@ -94,6 +94,24 @@ def time_launches(fn, steps: int, warmup: int):
     return start.elapsed_time(end) / steps
 
 
+def launch_stats(fn, n: int):
+    """Per-launch times of ``n`` further launches, each between its own pair
+    of HIP events on the launch stream: median, min and 90th percentile in
+    ms (reported beside ``value``, which is the bracketed whole-run figure)."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(n)]
+    torch.cuda.synchronize()
+    for e0, e1 in evs:
+        e0.record()
+        fn()
+        e1.record()
+    torch.cuda.synchronize()
+    t = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    return {"median_ms": round(t[len(t) // 2], 4), "min_ms": round(t[0], 4),
+            "p90_ms": round(t[min(len(t) - 1, (9 * len(t)) // 10)], 4), "n": n}
+
+
 def run_matmul(cfg, steps, warmup):
     import torch
     import paper_2512_16512_amd as xtc
@@ -114,13 +132,14 @@ def run_matmul(cfg, steps, warmup):
             raise xtc.XtcError(st, "xtc_matmul")
 
     ms = time_launches(launch, steps, warmup)
+    stats = launch_stats(launch, steps)
     flops = 2.0 * cfg["M"] * cfg["N"] * cfg["K"]
     elt = 4 if cfg["dtype"] == "f32" else 2
     alg_bytes = elt * (cfg["M"] * cfg["K"] + cfg["K"] * cfg["N"]) + 4 * cfg["M"] * cfg["N"]
     i, j = xi.sample_indices_matmul(xi.seed(cfg["index"], 3), cfg["M"], cfg["N"], cfg["check"])
     sampled = c[torch.from_numpy(i).cuda(), torch.from_numpy(j).cuda()].cpu().numpy()
     return dict(ms=ms, flops=flops, alg_bytes=alg_bytes, sched=repr(sched), A=A, B=B, I=i, J=j,
-                sampled=sampled)
+                sampled=sampled, stats=stats)
 
 
 def run_conv(cfg, steps, warmup):
@@ -144,11 +163,12 @@ def run_conv(cfg, steps, warmup):
             raise xtc.XtcError(st, "xtc_conv2d_nchw")
 
     ms = time_launches(launch, steps, warmup)
+    stats = launch_stats(launch, steps)
     F = xi.sample_indices_flat(xi.seed(cfg["index"], 3), y.numel(), cfg["check"])
     sampled = y.reshape(-1)[torch.from_numpy(F).cuda()].cpu().numpy()
     alg_bytes = 4 * (X.size + W.size + y.numel())
     return dict(ms=ms, flops=2.0 * Mg * Ng * Kg, alg_bytes=alg_bytes, sched=repr(sched), X=X, W=W,
-                F=F, sampled=sampled, gemm=(Mg, Ng, Kg))
+                F=F, sampled=sampled, gemm=(Mg, Ng, Kg), stats=stats)
 
 
 def _paper_launcher(xtc, cfg):
@@ -239,6 +259,7 @@ def summary(kind, cfg, r, workload):
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "ms_per_launch": round(r["ms"], 4),
+        "launch_stats": r["stats"],
         "frac_of_peak": round(tflops / PEAK["bf16" if kind == "bf16" else "f32"], 4),
         "schedule": r["sched"],
         "roofline": {
@@ -283,16 +304,27 @@ def cpu_baseline_leg(results, budget_s: float):
         }
     parity = {}
     for kind, r in results.items():
+        t0 = time.perf_counter()
         if kind == "conv":
             ref = oracle.conv2d_sampled(r["X"], r["W"], r["F"], stride=1, pad=1)
             tol = 1e-5
         else:
             ref = oracle.matmul_sampled(r["A"], r["B"], r["I"], r["J"])
             tol = 1e-5 if kind == "fp32" else 1e-2
+        dt = time.perf_counter() - t0
         err = oracle.rel_fro(r["sampled"], ref)
         parity[kind] = {"rel_fro": float("%.3e" % err), "tol": tol, "samples": int(len(ref)),
-                        "ok": bool(err <= tol)}
+                        "max_abs": float("%.3e" % np.max(np.abs(r["sampled"] - ref))),
+                        "check_s": round(dt, 4), "ok": bool(err <= tol)}
     out["parity"] = parity
+    # the oracle on one thread for the two small configs (full products)
+    single = {}
+    for cfg in xi.CONFIGS[:2]:
+        A, B = xi.matmul_inputs(cfg)
+        _, dt = oracle.timed(oracle.matmul, A, B, nthreads=1)
+        single["matmul_f32_%dx%dx%d" % (cfg["M"], cfg["N"], cfg["K"])] = {
+            "s": round(dt, 4), "GFLOP/s": round(2.0 * cfg["M"] * cfg["N"] * cfg["K"] / dt / 1e9, 2)}
+    out["oracle_single_thread"] = single
     return out
 
 
@@ -394,7 +426,11 @@ def main():
                   flush=True)
         summaries["paper"] = {k: v["line"] for k, v in paper.items()}
 
-    head_kind = "fp32" if "fp32" in summaries else kinds[0]
+    heads = [k for k in ("fp32", "bf16", "conv") if k in summaries]
+    if not heads:
+        print("bench.py: --only must name at least one of fp32, bf16, conv", file=sys.stderr)
+        sys.exit(2)
+    head_kind = heads[0]
     head = summaries[head_kind]
     line = {
         "metric": METRIC,
@@ -414,7 +450,9 @@ def main():
             "M": 4096, "N": 4096, "K": 4096, "layout": "row-major A[M,K], B[K,N], C[M,N]",
             "schedule": head["schedule"],
             "device": torch.cuda.get_device_name(0),
+            "hip": torch.version.hip,
         },
+        "launch_stats": head["launch_stats"],
         "roofline": head["roofline"],
         "frac_of_peak": head["frac_of_peak"],
         "also": {k: v for k, v in summaries.items() if k != head_kind},
@@ -425,6 +463,8 @@ def main():
             line["cpu_baseline"] = extra["cpu_baseline"]
         line["parity"] = extra["parity"]
         line["parity"].update(paper_parity(paper))
+        if "cpu_baseline" in line:
+            line["cpu_baseline"]["single_thread"] = extra["oracle_single_thread"]
     print(json.dumps(line), flush=True)
 
 

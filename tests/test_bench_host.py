@@ -1,0 +1,39 @@
+"""Host-side logic of bench.py that needs no GPU: the one-GPU rule and the
+rule that measured traffic is reported only for the kernel sources it was
+measured on."""
+import os
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+
+
+def test_traffic_only_for_the_measured_kernel_source(monkeypatch):
+    import json
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    rec = json.load(open(path))
+    for workload, kind in (("matmul_f32_4096x4096x4096", "f32"),
+                           ("matmul_bf16_8192x8192x8192", "bf16"),
+                           ("conv2d_f32_n32c64h56w56_oc64_r3s3", "conv")):
+        assert workload in rec
+        monkeypatch.setattr(bench, "kernel_hash", lambda k: rec[workload]["kernel_hash"])
+        assert bench.measured_traffic(kind, workload) == rec[workload]["hbm_bytes_per_launch"]
+        monkeypatch.setattr(bench, "kernel_hash", lambda k: "0" * 16)
+        assert bench.measured_traffic(kind, workload) is None
+
+
+def test_kernel_hash_covers_every_source_of_the_kernel():
+    for kind, files in bench.KERNEL_SOURCES.items():
+        assert "tile_map.h" in files and "lds_dma.h" in files
+        for f in files:
+            assert os.path.exists(os.path.join(ROOT, "paper_2512_16512_amd", "csrc", f))
+        assert bench.kernel_hash(kind) == bench.kernel_hash(kind)
