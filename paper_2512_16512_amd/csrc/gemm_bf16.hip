@@ -549,7 +549,7 @@ hipError_t launch_bf16(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), 2, PAD, 0),               \
             &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, true>,                                  \
-            &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, false>, false,                          \
+            &launch_bf16<BM, BN, BK, WM, WN, MI, PAD, false>, kRowsAligned,                   \
             &occupancy_of<&gemm_bf16_kernel<BM, BN, BK, WM, WN, MI, PAD, true>,               \
                           (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
@@ -562,7 +562,7 @@ hipError_t launch_bf16(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), STAGES, -1, 0),           \
             &launch_bf16_dma<BM, BN, BK, WM, WN, MI, STAGES, 0, 1>,                           \
-            &launch_bf16<BM, BN, BK, WM, WN, MI, 8, false>, true,                             \
+            &launch_bf16<BM, BN, BK, WM, WN, MI, 8, false>, kWholeChunks,                     \
             &occupancy_of<&gemm_bf16_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES, 0, 1>,        \
                           (BM / WM) * (BN / WN) * 64, 0>                                      \
     }

@@ -439,7 +439,7 @@ gemm_f32_ksplit_kernel(GemmArgs p) {
 
     // Branch-free loads: buffer loads whose offset is moved past the end of
     // the operand (kOOB) when the element lies outside the matrix read zero.
-    // VEC (K a multiple of 4, 16-byte aligned rows): one 16-byte load per A
+    // VEC (K a multiple of 4, 16-byte aligned A rows): one 16-byte load per A
     // row segment; otherwise one 4-byte load per element.
     const __amdgpu_buffer_rsrc_t ra =
         __builtin_amdgcn_make_buffer_rsrc((void *)A, (short)0, ((M - 1) * lda + K) * 4, 0x00020000);
@@ -572,7 +572,7 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 2 : 4), 2, PAD, 0),                 \
             &launch_f32<BM, BN, BK, WM, WN, MI, PAD, true>,                                   \
-            &launch_f32<BM, BN, BK, WM, WN, MI, PAD, false>, false,                           \
+            &launch_f32<BM, BN, BK, WM, WN, MI, PAD, false>, kRowsAligned,                    \
             &occupancy_of<&gemm_f32_kernel<BM, BN, BK, WM, WN, MI, PAD, true>,                \
                           (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
@@ -582,7 +582,7 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, 32, 32, 2, STAGES, -1, 0),                             \
             &launch_f32_dma<BM, BN, BK, WM, WN, STAGES>,                                      \
-            &launch_f32<BM, BN, BK, WM, WN, 32, 4, false>, true,                              \
+            &launch_f32<BM, BN, BK, WM, WN, 32, 4, false>, kWholeChunks,                      \
             &occupancy_of<&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, STAGES>,                   \
                           (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
@@ -594,7 +594,7 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
         make_sched(MI * TM, MI * TN, U * 4 * (64 / MI), MI * TM, MI * TN, MI, MI,             \
                    (MI == 32 ? 2 : 4), 0, 0, 0, 0, KS),                                       \
             &launch_f32_ksplit<MI, TM, TN, KS, U, D, true>,                                   \
-            &launch_f32_ksplit<MI, TM, TN, KS, U, D, false>, true,                            \
+            &launch_f32_ksplit<MI, TM, TN, KS, U, D, false>, kARowsOnly,                      \
             &occupancy_of<&gemm_f32_ksplit_kernel<MI, TM, TN, KS, U, D, true>, KS * 64, 0>    \
     }
 

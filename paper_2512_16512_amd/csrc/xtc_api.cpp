@@ -253,9 +253,16 @@ xtc_status matmul_impl(int64_t M, int64_t N, int64_t K, const void *A, int64_t l
     a.A = A; a.lda = (int)lda; a.B = B; a.ldb = (int)ldb; a.C = C; a.ldc = (int)ldc;
     a.raster = s.raster; a.xcd_remap = s.xcd_remap;
     a.relu = relu;
-    bool vec = K == 0 || (aligned16(A) && aligned16(B) && (lda * elt) % 16 == 0 &&
-                          (ldb * elt) % 16 == 0);
-    if (inst->vec_whole_chunks && ((K * elt) % 16 != 0 || (N * elt) % 16 != 0)) vec = false;
+    const bool a_rows = aligned16(A) && (lda * elt) % 16 == 0;
+    const bool b_rows = aligned16(B) && (ldb * elt) % 16 == 0;
+    bool vec;
+    switch (inst->vec_rule) {
+        case kARowsOnly: vec = K == 0 || (a_rows && (K * elt) % 16 == 0); break;
+        case kWholeChunks:
+            vec = K == 0 || (a_rows && b_rows && (K * elt) % 16 == 0 && (N * elt) % 16 == 0);
+            break;
+        default: vec = K == 0 || (a_rows && b_rows); break;
+    }
     const GemmLaunch fn = vec ? inst->vec_launch : inst->any_launch;
     return hip_status(fn(a, static_cast<hipStream_t>(stream)));
 }

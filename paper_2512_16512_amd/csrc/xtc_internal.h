@@ -52,15 +52,20 @@ hipError_t occupancy_of(int K, int *wg_per_cu) {
         (size_t)DYN_BYTES_PER_K * (size_t)K);
 }
 
-// One compiled kernel instance.  `vec_launch` requires 16-byte aligned
-// operand rows (base pointers and leading dimensions) and, when
-// `vec_whole_chunks` is set, also K and N to be multiples of 16 bytes of
-// elements; `any_launch` has no such requirement.
+// What `vec_launch` of an instance requires; `any_launch` has no
+// requirement.
+enum VecRule {
+    kRowsAligned = 0,  // 16-byte aligned A and B rows (base pointers and leading dimensions)
+    kWholeChunks = 1,  // that, and K and N multiples of 16 bytes of elements
+    kARowsOnly = 2,    // 16-byte aligned A rows and K a multiple of 16 bytes (B read per element)
+};
+
+// One compiled kernel instance.
 struct GemmInstance {
     xtc_sched sched;
     GemmLaunch vec_launch;
     GemmLaunch any_launch;
-    bool vec_whole_chunks;
+    VecRule vec_rule;
     OccupancyFn occupancy;  // of the kernel vec_launch runs
 };
 
