@@ -6,8 +6,9 @@ already resident in HBM).  ``value`` is its TFLOP/s (2*M*N*K per launch over
 the HIP-event time of exactly ``--steps`` launches, after ``--warmup``
 untimed ones).  The same line also reports, timed the same way, the bf16
 matmul 8192^3 (fp32 accumulate and output) and the fp32 conv2d 32x64x56x56
--> 64, 3x3, stride 1, pad 1 as an implicit GEMM, each with its fraction of
-the MI355X matrix-core peak; the paper's other, smaller workloads (matmuls
+-> 64, 3x3, stride 1, pad 1 as an implicit GEMM (also with bf16 inputs), each
+with its fraction of the MI355X matrix-core peak; the paper's other, smaller
+workloads (matmuls
 1024^3, [512,128]x[128,1024], matmul+relu [256,128]x[128,1024], 256x258x512,
 and the 7x7 stride-2 conv2d 3 -> 16 channels at 224x224), timed as replays of
 a HIP graph of launches; and the fp64 CPU oracle timed on the host cores on a
@@ -16,7 +17,7 @@ sampled outputs of every timed launch (every output of the small workloads)
 against the oracle.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--only fp32,bf16,conv,paper] [--no-cpu-baseline]
+                       [--only fp32,bf16,conv,conv_bf16,paper] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -40,7 +41,7 @@ PEAK = {"f32": 157.3, "bf16": 2516.6}
 HBM_GBS = 8000.0
 KERNEL_SOURCES = {
     "f32": ["gemm_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h"],
-    "bf16": ["gemm_bf16.hip", "tile_map.h", "lds_dma.h"],
+    "bf16": ["gemm_bf16.hip", "mfma_bf16.h", "tile_map.h", "lds_dma.h"],
     "conv": ["conv2d_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h"],
 }
 
@@ -142,19 +143,22 @@ def run_matmul(cfg, steps, warmup):
                 sampled=sampled, stats=stats)
 
 
-def run_conv(cfg, steps, warmup):
+def run_conv(cfg, steps, warmup, dtype="f32"):
     import torch
     import paper_2512_16512_amd as xtc
     X, W = xi.conv_inputs(cfg)
+    if dtype == "bf16":
+        X, W = xi.f32_to_bf16_bits(X), xi.f32_to_bf16_bits(W)
+    code = xtc.XTC_F32 if dtype == "f32" else xtc.XTC_BF16
     xd, wd = to_dev(X), to_dev(W)
     OH, OW = xi.conv_out_hw(cfg["H"], cfg["W"], cfg["R"], cfg["S"], cfg["stride"], cfg["stride"],
                             cfg["pad"], cfg["pad"])
     y = torch.empty((cfg["N"], cfg["OC"], OH, OW), dtype=torch.float32, device="cuda")
     Mg, Ng, Kg = cfg["OC"], cfg["N"] * OH * OW, cfg["C"] * cfg["R"] * cfg["S"]
-    sched = xtc.xtc_default_schedule(xtc.XTC_OP_CONV2D, xtc.XTC_F32, Mg, Ng, Kg)
+    sched = xtc.xtc_default_schedule(xtc.XTC_OP_CONV2D, code, Mg, Ng, Kg)
     st_, pd = cfg["stride"], cfg["pad"]
     args = (cfg["N"], cfg["C"], cfg["H"], cfg["W"], cfg["OC"], cfg["R"], cfg["S"], st_, st_, pd, pd,
-            xd.data_ptr(), wd.data_ptr(), y.data_ptr(), xtc.XTC_F32, sched,
+            xd.data_ptr(), wd.data_ptr(), y.data_ptr(), code, sched,
             torch.cuda.current_stream().cuda_stream)
 
     def launch():
@@ -166,7 +170,7 @@ def run_conv(cfg, steps, warmup):
     stats = launch_stats(launch, steps)
     F = xi.sample_indices_flat(xi.seed(cfg["index"], 3), y.numel(), cfg["check"])
     sampled = y.reshape(-1)[torch.from_numpy(F).cuda()].cpu().numpy()
-    alg_bytes = 4 * (X.size + W.size + y.numel())
+    alg_bytes = X.itemsize * (X.size + W.size) + 4 * y.numel()
     return dict(ms=ms, flops=2.0 * Mg * Ng * Kg, alg_bytes=alg_bytes, sched=repr(sched), X=X, W=W,
                 F=F, sampled=sampled, gemm=(Mg, Ng, Kg), stats=stats)
 
@@ -253,21 +257,21 @@ def run_paper(cfg, steps, warmup, per_graph=50):
 
 def summary(kind, cfg, r, workload):
     tflops = r["flops"] / (r["ms"] * 1e-3) / 1e12
-    traffic = measured_traffic(kind, workload)
+    traffic = measured_traffic(kind, workload) if kind in KERNEL_SOURCES else None
     return {
         "workload": workload,
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "ms_per_launch": round(r["ms"], 4),
         "launch_stats": r["stats"],
-        "frac_of_peak": round(tflops / PEAK["bf16" if kind == "bf16" else "f32"], 4),
+        "frac_of_peak": round(tflops / PEAK["bf16" if kind in ("bf16", "conv_bf16") else "f32"], 4),
         "schedule": r["sched"],
         "roofline": {
             "bound": "mfma",
             "achieved": round(tflops, 2),
-            "peak": PEAK["bf16" if kind == "bf16" else "f32"],
+            "peak": PEAK["bf16" if kind in ("bf16", "conv_bf16") else "f32"],
             "unit": "TFLOP/s",
-            "frac": round(tflops / PEAK["bf16" if kind == "bf16" else "f32"], 4),
+            "frac": round(tflops / PEAK["bf16" if kind in ("bf16", "conv_bf16") else "f32"], 4),
             "traffic": traffic,
             "alg_bytes": r["alg_bytes"],
             "alg_hbm_GBps": round(r["alg_bytes"] / (r["ms"] * 1e-3) / 1e9, 1),
@@ -305,9 +309,9 @@ def cpu_baseline_leg(results, budget_s: float):
     parity = {}
     for kind, r in results.items():
         t0 = time.perf_counter()
-        if kind == "conv":
+        if kind in ("conv", "conv_bf16"):
             ref = oracle.conv2d_sampled(r["X"], r["W"], r["F"], stride=1, pad=1)
-            tol = 1e-5
+            tol = 1e-5 if kind == "conv" else 1e-2
         else:
             ref = oracle.matmul_sampled(r["A"], r["B"], r["I"], r["J"])
             tol = 1e-5 if kind == "fp32" else 1e-2
@@ -363,7 +367,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--only", default="fp32,bf16,conv,paper")
+    ap.add_argument("--only", default="fp32,bf16,conv,conv_bf16,paper")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -409,6 +413,13 @@ def main():
         results["conv"] = run_conv(cfg, args.steps, args.warmup)
         summaries["conv"] = summary("conv", cfg, results["conv"], "conv2d_f32_n32c64h56w56_oc64_r3s3")
         print("# conv: %.4f ms/launch" % results["conv"]["ms"], file=sys.stderr, flush=True)
+    if "conv_bf16" in kinds:
+        cfg = xi.CONFIGS[4]
+        results["conv_bf16"] = run_conv(cfg, args.steps, args.warmup, dtype="bf16")
+        summaries["conv_bf16"] = summary("conv_bf16", cfg, results["conv_bf16"],
+                                         "conv2d_bf16_n32c64h56w56_oc64_r3s3")
+        print("# conv bf16: %.4f ms/launch" % results["conv_bf16"]["ms"], file=sys.stderr,
+              flush=True)
 
     paper = {}
     if "paper" in kinds:

@@ -159,11 +159,14 @@ xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K,
  * Computed as an implicit GEMM (no im2col buffer): M = OC, N = N*OH*OW,
  * K = C*R*S, reduced in the order the schedule's k_order selects.
  *
- *  X    device, NCHW contiguous fp32.      Wt  device, OIHW contiguous fp32.
+ *  X    device, NCHW contiguous; Wt device, OIHW contiguous; both fp32
+ *       (XTC_F32) or both bf16 bit patterns (XTC_BF16, products exact in
+ *       fp32, fp32 accumulation).
  *  Y    device, N x OC x OH x OW contiguous fp32 (overwritten).
  *  N, C, H, W, OC, R, S >= 1 except that N == 0 or OC == 0 is a no-op;
  *  stride >= 1, pad >= 0, OH >= 1 and OW >= 1, else XTC_ERR_BAD_SHAPE.
- *  dtype must be XTC_F32 (else XTC_ERR_BAD_DTYPE).
+ *  dtype XTC_F32 or XTC_BF16 (else XTC_ERR_BAD_DTYPE); the bf16 kernels
+ *  reduce in OIHW order (k_order 0).
  *  sched NULL selects the default conv schedule.
  * Errors as for xtc_matmul; XTC_ERR_TOO_LARGE also when C*R*S exceeds the
  * kernel's k-offset table capacity (xtc_conv_max_k()).

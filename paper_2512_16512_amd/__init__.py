@@ -249,12 +249,14 @@ def matmul(a, b, out=None, sched=None, relu=False):
 
 
 def conv2d_nchw(x, w, stride=1, pad=0, out=None, sched=None, relu=False):
-    """Zero-padded cross-correlation of NCHW ``x`` with OIHW ``w`` (float32,
-    contiguous CUDA tensors) into a float32 NCHW ``out`` (relu fused into the
-    epilogue when ``relu``)."""
+    """Zero-padded cross-correlation of NCHW ``x`` with OIHW ``w`` (both
+    float32 or both bfloat16, contiguous CUDA tensors) into a float32 NCHW
+    ``out`` (relu fused into the epilogue when ``relu``)."""
     import torch
     if x.dim() != 4 or w.dim() != 4 or not x.is_contiguous() or not w.is_contiguous():
         raise ValueError("x and w must be contiguous 4-D tensors")
+    if x.dtype != w.dtype:
+        raise TypeError("x and w must have the same dtype")
     N, C, H, W = x.shape
     OC, C2, R, S = w.shape
     if C2 != C:

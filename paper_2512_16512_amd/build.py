@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libxtc.so")
 OBJDIR = os.path.join(HERE, "_build")
 
-SOURCES = ["gemm_f32.hip", "gemm_bf16.hip", "conv2d_f32.hip", "xtc_api.cpp"]
+SOURCES = ["gemm_f32.hip", "gemm_bf16.hip", "conv2d_f32.hip", "conv2d_bf16.hip", "xtc_api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -18,65 +18,12 @@
 // B[k0 .. k0+3][n0+a]: four consecutive k of its own column, which is the
 // MFMA B-operand layout.  Two such reads (k0 and k0+4) give the 8 values.
 #include "lds_dma.h"
+#include "mfma_bf16.h"
 #include "tile_map.h"
 #include "xtc_internal.h"
 
 namespace xtc {
 namespace {
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
-typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-
-// Transpose read of 4 x 16 bits (see the file comment for the lane mapping).
-__device__ __forceinline__ u16x4 ds_read_tr16(const unsigned short *p) {
-    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p));
-    return __builtin_bit_cast(u16x4, v);
-}
-
-template <int MI>
-struct Bf16Mfma;
-
-template <>
-struct Bf16Mfma<32> {
-    static constexpr int KG = 2;     // lane groups along k
-    static constexpr int NACC = 16;
-    typedef f32x16 acc_t;
-    static __device__ __forceinline__ acc_t mma(const u16x8 &a, const u16x8 &b, const acc_t &c) {
-        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ int row(int lane, int r) {
-        return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    }
-};
-
-template <>
-struct Bf16Mfma<16> {
-    static constexpr int KG = 4;
-    static constexpr int NACC = 4;
-    typedef f32x4 acc_t;
-    static __device__ __forceinline__ acc_t mma(const u16x8 &a, const u16x8 &b, const acc_t &c) {
-        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ int row(int lane, int r) { return 4 * (lane >> 4) + r; }
-};
-
-template <int W>
-struct VecU16;
-template <>
-struct VecU16<8> {
-    typedef u16x8 t;
-};
-template <>
-struct VecU16<1> {
-    typedef unsigned short t;
-};
 
 template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD, bool VEC>
 struct GemmBf16Cfg {
@@ -101,24 +48,6 @@ struct GemmBf16Cfg {
     static_assert(B_LOADS * W * NT == BK * BN, "B tile must split evenly over threads");
     static_assert(PAD % 8 == 0, "padding must keep 16-byte alignment");
 };
-
-template <int W>
-__device__ __forceinline__ typename VecU16<W>::t load_pred_u16(const unsigned short *p, int valid);
-
-template <>
-__device__ __forceinline__ u16x8 load_pred_u16<8>(const unsigned short *p, int valid) {
-    if (valid >= 8) return *reinterpret_cast<const u16x8 *>(p);
-    u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-    for (int e = 0; e < 7; ++e)
-        if (e < valid) v[e] = p[e];
-    return v;
-}
-
-template <>
-__device__ __forceinline__ unsigned short load_pred_u16<1>(const unsigned short *p, int valid) {
-    return valid > 0 ? *p : (unsigned short)0;
-}
 
 template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD, bool VEC>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)

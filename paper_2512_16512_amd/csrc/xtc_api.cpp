@@ -71,7 +71,6 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
                   ((int64_t)s.block_m * (s.block_k + pad) + (int64_t)s.block_n * (s.block_k + 8));
     if (s.k_split > 1) lds += (int64_t)s.k_split * s.block_m * s.block_n * 4;  // partial sums
     if (lds > kLdsBytes) return XTC_ERR_BAD_SCHEDULE;
-    if (op == XTC_OP_CONV2D && dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
     return XTC_OK;
 }
 
@@ -83,9 +82,9 @@ const GemmInstance *find_gemm(xtc_dtype dt, const xtc_sched &s) {
     return nullptr;
 }
 
-const ConvInstance *find_conv(const xtc_sched &s) {
+const ConvInstance *find_conv(xtc_dtype dt, const xtc_sched &s) {
     int n = 0;
-    const ConvInstance *tab = conv2d_f32_instances(&n);
+    const ConvInstance *tab = dt == XTC_F32 ? conv2d_f32_instances(&n) : conv2d_bf16_instances(&n);
     for (int i = 0; i < n; ++i)
         if (same_instance(tab[i].sched, s)) return &tab[i];
     return nullptr;
@@ -132,8 +131,18 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     if (M < 0 || N < 0 || K < 0) return XTC_ERR_BAD_SHAPE;
     const int64_t cus = 256;
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
+    if (op == XTC_OP_CONV2D && dt == XTC_BF16) {
+        // register-staged implicit GEMM: 64x128 tiles, 128x128 for more than
+        // 64 output channels, 64x64 when 64x128 tiles leave CUs idle
+        *out = make_sched(64, 128, 32, 32, 64, 32, 32, 16, 2, 8, 0);
+        if (M > 64)
+            *out = make_sched(128, 128, 32, 64, 64, 32, 32, 16, 2, 8, 0);
+        else if (tiles(64, 128) < cus)
+            *out = make_sched(64, 64, 32, 32, 32, 32, 32, 16, 2, 8, 0);
+        out->raster = 0;
+        return XTC_OK;
+    }
     if (op == XTC_OP_CONV2D) {
-        if (dt != XTC_F32) return XTC_ERR_BAD_DTYPE;
         // 64x256 tiles of 4 waves (64x64 each) with a two-stage ring: two
         // workgroups per CU, so up to 512 tiles run in a single wave; the
         // halo-tiled kernel where the shape allows it (3x3, stride 1, rows
@@ -183,7 +192,7 @@ xtc_status xtc_sched_check(xtc_op op, xtc_dtype dt, const xtc_sched *s) {
     const xtc_status st = legal(op, dt, *s);
     if (st != XTC_OK) return st;
     if (op == XTC_OP_MATMUL) return find_gemm(dt, *s) ? XTC_OK : XTC_ERR_UNSUPPORTED_SCHEDULE;
-    return find_conv(*s) ? XTC_OK : XTC_ERR_UNSUPPORTED_SCHEDULE;
+    return find_conv(dt, *s) ? XTC_OK : XTC_ERR_UNSUPPORTED_SCHEDULE;
 }
 
 xtc_status xtc_sched_occupancy(xtc_op op, xtc_dtype dt, int64_t K, const xtc_sched *s,
@@ -194,7 +203,8 @@ xtc_status xtc_sched_occupancy(xtc_op op, xtc_dtype dt, int64_t K, const xtc_sch
     if (K < 0) return XTC_ERR_BAD_SHAPE;
     if (op == XTC_OP_CONV2D && K > kConvMaxK) return XTC_ERR_TOO_LARGE;
     if (K > (int64_t)1 << 30) return XTC_ERR_TOO_LARGE;
-    OccupancyFn fn = op == XTC_OP_MATMUL ? find_gemm(dt, *s)->occupancy : find_conv(*s)->occupancy;
+    OccupancyFn fn =
+        op == XTC_OP_MATMUL ? find_gemm(dt, *s)->occupancy : find_conv(dt, *s)->occupancy;
     int n = 0;
     const xtc_status hs = hip_status(fn((int)K, &n));
     if (hs != XTC_OK) return hs;
@@ -210,8 +220,8 @@ int32_t xtc_sched_list(xtc_op op, xtc_dtype dt, xtc_sched *out, int32_t cap) {
     } else if (op == XTC_OP_MATMUL && dt == XTC_BF16) {
         const GemmInstance *t = gemm_bf16_instances(&n);
         for (int i = 0; i < n && i < cap && out; ++i) out[i] = t[i].sched;
-    } else if (op == XTC_OP_CONV2D && dt == XTC_F32) {
-        const ConvInstance *t = conv2d_f32_instances(&n);
+    } else if (op == XTC_OP_CONV2D && (dt == XTC_F32 || dt == XTC_BF16)) {
+        const ConvInstance *t = dt == XTC_F32 ? conv2d_f32_instances(&n) : conv2d_bf16_instances(&n);
         for (int i = 0; i < n && i < cap && out; ++i) out[i] = t[i].sched;
     } else {
         return -1;
@@ -272,7 +282,6 @@ xtc_status conv_impl(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int
                      const void *X, const void *Wt, float *Y, xtc_dtype dtype,
                      const xtc_sched *sched, void *stream, int relu) {
     if (dtype != XTC_F32 && dtype != XTC_BF16) return XTC_ERR_BAD_DTYPE;
-    if (dtype != XTC_F32) return XTC_ERR_BAD_DTYPE;
     if (N < 0 || OC < 0 || C < 1 || H < 1 || W < 1 || R < 1 || S < 1 || stride_h < 1 ||
         stride_w < 1 || pad_h < 0 || pad_w < 0)
         return XTC_ERR_BAD_SHAPE;
@@ -290,10 +299,12 @@ xtc_status conv_impl(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int
     }
     if (N == 0 || OC == 0) return XTC_OK;
     if (!X || !Wt || !Y) return XTC_ERR_NULL_POINTER;
-    if (N * C * H * W * 4 > kMaxSpan || OC * Kg * 4 > kMaxSpan || N * OC * OH * OW * 4 > kMaxSpan)
+    const int64_t elt = dtype == XTC_F32 ? 4 : 2;
+    if (N * C * H * W * elt > kMaxSpan || OC * Kg * elt > kMaxSpan ||
+        N * OC * OH * OW * 4 > kMaxSpan)
         return XTC_ERR_TOO_LARGE;
     if (Kg > kConvMaxK) return XTC_ERR_TOO_LARGE;
-    const ConvInstance *inst = find_conv(s);
+    const ConvInstance *inst = find_conv(dtype, s);
     if (!inst) return XTC_ERR_UNSUPPORTED_SCHEDULE;
 
     ConvArgs a;

@@ -30,8 +30,8 @@ struct ConvArgs {
     int Nb, C, H, W, OC, R, S;
     int sh, sw, ph, pw;
     int OH, OW;
-    const float *X;
-    const float *Wt;
+    const float *X;   // bf16 bit patterns for the bf16 kernels
+    const float *Wt;  // (the kernels reinterpret the pointers)
     float *Y;
     int raster;
     int xcd_remap;
@@ -78,6 +78,7 @@ struct ConvInstance {
 const GemmInstance *gemm_f32_instances(int *count);
 const GemmInstance *gemm_bf16_instances(int *count);
 const ConvInstance *conv2d_f32_instances(int *count);
+const ConvInstance *conv2d_bf16_instances(int *count);
 
 // Largest implicit-GEMM K the conv kernels' LDS k-offset table holds.
 constexpr int kConvMaxK = 4096;

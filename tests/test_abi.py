@@ -82,7 +82,8 @@ def test_matmul_empty_is_noop(x):
 
 
 @pytest.mark.parametrize("args,expected", [
-    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 1), 4),     # bf16 conv not offered
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, 0, BAD, BAD, 1), 1),       # bf16 conv, X NULL
+    ((1, 1024, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 1), 7),  # bf16: C*R*S > table capacity
     ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 5), 4),     # unknown dtype
     ((1, 0, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 0), 2),     # C = 0
     ((1, 3, 8, 8, 4, 3, 3, 0, 1, 1, 1, BAD, BAD, BAD, 0), 2),     # stride 0
@@ -104,7 +105,7 @@ def test_conv_empty_is_noop(x):
 
 
 def test_sched_list_and_check(x):
-    for op, dt in ((0, 0), (0, 1), (1, 0)):
+    for op, dt in ((0, 0), (0, 1), (1, 0), (1, 1)):
         lst = x.xtc_sched_list(op, dt)
         assert len(lst) >= 3
         for s in lst:
@@ -114,7 +115,7 @@ def test_sched_list_and_check(x):
                 s2.raster = r
                 s2.xcd_remap = r & 1
                 assert x.xtc_sched_check(op, dt, s2) == 0
-    assert x.xtc_sched_list(1, 1) == []
+    assert x.xtc_sched_list(1, 2) == [] and x.xtc_sched_list(2, 0) == []
 
 
 def _base(x, dt=0):
@@ -159,11 +160,12 @@ def test_default_schedules_are_compiled(x):
     for (op, dt, M, N, K) in [(0, 0, 4096, 4096, 4096), (0, 0, 256, 256, 256), (0, 0, 1, 1, 1),
                               (0, 1, 8192, 8192, 8192), (0, 1, 100, 100, 100), (0, 1, 2048, 2048, 64),
                               (1, 0, 64, 100352, 576), (1, 0, 256, 1000, 2304),
-                              (1, 0, 16, 12544, 147)]:
+                              (1, 0, 16, 12544, 147), (1, 1, 64, 100352, 576), (1, 1, 16, 12544, 147),
+                              (1, 1, 256, 1000, 2304)]:
         s = x.xtc_default_schedule(op, dt, M, N, K)
         assert x.xtc_sched_check(op, dt, s) == 0, (op, dt, M, N, K, s)
     with pytest.raises(x.XtcError):
-        x.xtc_default_schedule(1, 1, 64, 64, 64)
+        x.xtc_default_schedule(1, 2, 64, 64, 64)
 
 
 def test_no_hip_error_recorded_by_validation(x):

@@ -66,6 +66,43 @@ def test_matmul_config_parity(x, ci):
     say("  rel_fro = %.3e" % err)
 
 
+@pytest.mark.parametrize("shape", [
+    (3, 5, 13, 11, 7, 3, 3, 1, 1),      # C*R*S = 45: scalar weight loads
+    (2, 8, 17, 19, 70, 3, 3, 1, 1),     # C*R*S = 72, OC = 70: ragged weight rows, pixel tail
+    (3, 16, 9, 14, 64, 3, 3, 2, 1),     # stride 2
+    (1, 4, 20, 20, 33, 5, 5, 1, 2),     # 5x5, pad 2
+    (2, 12, 11, 7, 16, 1, 1, 1, 0),     # 1x1
+    (1, 3, 30, 30, 16, 7, 7, 2, 3),     # the 7x7 stride-2 shape, scaled down
+    (1, 64, 12, 12, 130, 3, 3, 1, 1),   # OC > 128: several weight tiles
+])
+def test_conv_bf16_small_int_exact_every_instance(x, shape):
+    N, C, H, W_, OC, R, S, stride, pad = shape
+    X = xi.f32_to_bf16_bits(xi.small_int_f32(11, (N, C, H, W_)))
+    W = xi.f32_to_bf16_bits(xi.small_int_f32(12, (OC, C, R, S)))
+    ref = oracle.conv2d(X, W, stride=stride, pad=pad)
+    for s in x.xtc_sched_list(x.XTC_OP_CONV2D, x.XTC_BF16):
+        for raster in (0, 8):
+            s.raster = raster
+            say("conv bf16 exact", shape, s)
+            got = to_host(x.conv2d_nchw(to_dev(X), to_dev(W), stride=stride, pad=pad, sched=s))
+            assert np.array_equal(got, ref), "conv bf16 %s %s: not bit-exact" % (shape, s)
+
+
+def test_conv_bf16_config_shape_parity(x):
+    # the 32x64x56x56 -> 64 layer with bf16 inputs, checked on sampled outputs
+    import torch
+    cfg = xi.CONFIGS[4]
+    X, W = xi.conv_inputs(cfg)
+    Xb, Wb = xi.f32_to_bf16_bits(X), xi.f32_to_bf16_bits(W)
+    say("conv bf16 config shape")
+    y = x.conv2d_nchw(to_dev(Xb), to_dev(Wb), stride=cfg["stride"], pad=cfg["pad"])
+    F = xi.sample_indices_flat(xi.seed(4, 3), y.numel(), cfg["check"])
+    ref = oracle.conv2d_sampled(Xb, Wb, F, stride=cfg["stride"], pad=cfg["pad"])
+    got = to_host(y.reshape(-1)[torch.from_numpy(F).cuda()])
+    err = assert_parity(got, ref, "bf16", "conv bf16 32x64x56x56")
+    say("  rel_fro = %.3e" % err)
+
+
 def test_conv_config_parity(x):
     import torch
     cfg = xi.CONFIGS[4]

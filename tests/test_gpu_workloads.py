@@ -64,13 +64,16 @@ def test_matmul_relu_exact_every_instance(x, dtype, M, N, K):
     (1, 3, 30, 30, 16, 7, 7, 2, 3),     # the 7x7 stride-2 shape, scaled down
     (1, 16, 56, 56, 40, 3, 3, 1, 1),    # halo-tiled kernel
 ])
-def test_conv_relu_exact_every_instance(x, shape):
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_conv_relu_exact_every_instance(x, shape, dtype):
     N, C, H, W_, OC, R, S, stride, pad = shape
     X = xi.small_int_f32(23, (N, C, H, W_))
     W = xi.small_int_f32(24, (OC, C, R, S))
+    X, W = _prep(X, W, dtype)
     ref = oracle.relu(oracle.conv2d(X, W, stride=stride, pad=pad))
-    for s in x.xtc_sched_list(x.XTC_OP_CONV2D, x.XTC_F32):
-        say("conv relu", shape, s)
+    code = x.XTC_F32 if dtype == "f32" else x.XTC_BF16
+    for s in x.xtc_sched_list(x.XTC_OP_CONV2D, code):
+        say("conv relu", dtype, shape, s)
         got = to_host(x.conv2d_nchw(to_dev(X), to_dev(W), stride=stride, pad=pad, sched=s,
                                     relu=True))
         assert np.array_equal(got, ref), "conv relu %s %s: not bit-exact" % (shape, s)
@@ -148,16 +151,16 @@ def _workload_ids():
 def test_paper_workload_parity(x, wi, dtype):
     cfg = next(c for c in xi.PAPER_WORKLOADS if c["index"] == wi)
     if cfg["op"] == "conv2d":
-        if dtype == "bf16":
-            pytest.skip("conv2d is offered in fp32 only")
         X, W = xi.conv_inputs(cfg)
-        say("workload", cfg["name"])
+        if dtype == "bf16":
+            X, W = xi.f32_to_bf16_bits(X), xi.f32_to_bf16_bits(W)
+        say("workload", cfg["name"], dtype)
         y = x.conv2d_nchw(to_dev(X), to_dev(W), stride=cfg["stride"], pad=cfg["pad"])
         ref = oracle.conv2d(X, W, stride=cfg["stride"], pad=cfg["pad"])
-        err = assert_parity(to_host(y), ref, "f32", cfg["name"])
+        err = assert_parity(to_host(y), ref, dtype, cfg["name"])
         say("  rel_fro = %.3e" % err)
         yr = x.conv2d_nchw(to_dev(X), to_dev(W), stride=cfg["stride"], pad=cfg["pad"], relu=True)
-        err = assert_parity(to_host(yr), oracle.relu(ref), "f32", cfg["name"] + " + relu")
+        err = assert_parity(to_host(yr), oracle.relu(ref), dtype, cfg["name"] + " + relu")
         return
     A, B = _prep(*xi.matmul_inputs(cfg), dtype)
     relu = cfg["op"] == "matmul_relu"
