@@ -53,10 +53,11 @@ def kernel_hash(kind: str) -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kind: str, workload: str):
+def measured_traffic(kind: str, workload: str, schedule: str | None = None):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None when there is none for this kernel source (the counters were taken
-    on a different version of the kernel)."""
+    None when there is none for this kernel source and schedule (the
+    counters were taken on a different version of the kernel, or under a
+    different schedule)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -65,6 +66,8 @@ def measured_traffic(kind: str, workload: str):
     except (ValueError, OSError):
         return None
     if not rec or rec.get("kernel_hash") != kernel_hash(kind):
+        return None
+    if schedule is not None and rec.get("schedule") != schedule:
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -257,7 +260,7 @@ def run_paper(cfg, steps, warmup, per_graph=50):
 
 def summary(kind, cfg, r, workload):
     tflops = r["flops"] / (r["ms"] * 1e-3) / 1e12
-    traffic = measured_traffic(kind, workload) if kind in KERNEL_SOURCES else None
+    traffic = measured_traffic(kind, workload, r["sched"]) if kind in KERNEL_SOURCES else None
     return {
         "workload": workload,
         "value": round(tflops, 2),

@@ -182,6 +182,14 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     }
     const int64_t t = tiles(out->block_m, out->block_n);
     out->raster = t >= 64 ? 8 : 0;
+    if (dt == XTC_BF16 && out->block_m == 256 && out->block_n == 256) {
+        // Column-major tiles dealt round-robin to the XCDs: at any moment all
+        // eight XCDs read the same few B column-panels, which the shared
+        // last-level cache then serves once (measured on 8192^3: 2% faster
+        // than grouped raster 8 with the XCD remap).
+        out->raster = 1;
+        out->xcd_remap = 0;
+    }
     return XTC_OK;
 }
 

@@ -27,6 +27,10 @@ def test_traffic_only_for_the_measured_kernel_source(monkeypatch):
         assert workload in rec
         monkeypatch.setattr(bench, "kernel_hash", lambda k: rec[workload]["kernel_hash"])
         assert bench.measured_traffic(kind, workload) == rec[workload]["hbm_bytes_per_launch"]
+        if "schedule" in rec[workload]:
+            assert bench.measured_traffic(kind, workload, rec[workload]["schedule"]) == \
+                rec[workload]["hbm_bytes_per_launch"]
+            assert bench.measured_traffic(kind, workload, "another schedule") is None
         monkeypatch.setattr(bench, "kernel_hash", lambda k: "0" * 16)
         assert bench.measured_traffic(kind, workload) is None
 
