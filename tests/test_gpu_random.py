@@ -1,0 +1,121 @@
+"""Seeded randomized parity and concurrency checks through the C ABI.
+
+- Random shapes (ragged in every dimension, leading dimensions with padding)
+  paired with random compiled instances, raster orders and the relu flag;
+  small-integer inputs make every correct result bit-exact.
+- Several host threads, each on its own stream, launching different
+  contractions at once: the library keeps no state shared between calls, so
+  every result must equal its single-threaded one.
+"""
+import threading
+
+import numpy as np
+import pytest
+
+import oracle
+import xtc_inputs as xi
+from _helpers import say, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def x():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2512_16512_amd as mod
+    return mod
+
+
+def _strided(arr, ld):
+    """Copy of a 2-D array inside rows of length ``ld``; the padding holds
+    NaN (fp32 NaN, or the bf16 quiet-NaN pattern for bf16 bits), so a read of
+    it would poison the result."""
+    if arr.dtype == np.uint16:
+        out = np.full((arr.shape[0], ld), 0x7FC0, dtype=np.uint16)
+    else:
+        out = np.full((arr.shape[0], ld), np.nan, dtype=np.float32)
+    out[:, :arr.shape[1]] = arr
+    return out
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_random_shapes_instances_and_leading_dims(x, dtype):
+    import torch
+    rng = np.random.default_rng(20261202 + (dtype == "bf16"))
+    code = x.XTC_F32 if dtype == "f32" else x.XTC_BF16
+    scheds = x.xtc_sched_list(x.XTC_OP_MATMUL, code)
+    for case in range(24):
+        M, N, K = (int(v) for v in rng.integers(1, 300, size=3))
+        pa, pb, pc = (int(v) for v in rng.integers(0, 9, size=3))
+        s = scheds[int(rng.integers(len(scheds)))]
+        s.raster = int(rng.choice([0, 1, 4, 8]))
+        s.xcd_remap = int(rng.integers(2))
+        relu = bool(rng.integers(2))
+        A = xi.small_int_f32(100 + case, (M, K))
+        B = xi.small_int_f32(200 + case, (K, N))
+        if dtype == "bf16":
+            A, B = xi.f32_to_bf16_bits(A), xi.f32_to_bf16_bits(B)
+        ref = oracle.matmul(A, B)
+        if relu:
+            ref = oracle.relu(ref)
+        lda, ldb, ldc = K + pa, N + pb, N + pc
+        Ad, Bd = to_dev(_strided(A, lda)), to_dev(_strided(B, ldb))
+        Cd = torch.full((M, ldc), 7.0, dtype=torch.float32, device="cuda")
+        fn = x.xtc_matmul_relu if relu else x.xtc_matmul
+        say("random", dtype, case, (M, N, K), (lda, ldb, ldc), relu, s)
+        st = fn(M, N, K, Ad.data_ptr(), lda, Bd.data_ptr(), ldb, Cd.data_ptr(), ldc, code, s,
+                torch.cuda.current_stream().cuda_stream)
+        assert st == 0, x.xtc_status_str(st)
+        got = to_host(Cd)
+        assert np.array_equal(got[:, :N], ref), (case, M, N, K, s)
+        assert np.all(got[:, N:] == 7.0), "columns past N were written"
+
+
+def test_concurrent_host_threads_on_separate_streams(x):
+    import torch
+    jobs = []
+    for t in range(4):
+        M, N, K = 200 + 37 * t, 150 + 19 * t, 300 + 11 * t
+        jobs.append(("mm", xi.small_int_f32(300 + t, (M, K)), xi.small_int_f32(400 + t, (K, N))))
+    jobs.append(("conv", xi.small_int_f32(500, (2, 16, 20, 22)), xi.small_int_f32(501, (24, 16, 3, 3))))
+    jobs.append(("bf16", xi.f32_to_bf16_bits(xi.small_int_f32(600, (333, 129))),
+                 xi.f32_to_bf16_bits(xi.small_int_f32(601, (129, 257)))))
+    refs = []
+    for kind, a, b in jobs:
+        if kind == "conv":
+            refs.append(oracle.conv2d(a, b, stride=1, pad=1))
+        else:
+            refs.append(oracle.relu(oracle.matmul(a, b)) if kind == "mm" else oracle.matmul(a, b))
+    results = [None] * len(jobs)
+    errors = []
+
+    def worker(i):
+        try:
+            stream = torch.cuda.Stream()
+            kind, a, b = jobs[i]
+            with torch.cuda.stream(stream):
+                ad, bd = to_dev(a), to_dev(b)
+                outs = []
+                for _ in range(5):   # repeated launches overlap with the other threads'
+                    if kind == "conv":
+                        outs.append(x.conv2d_nchw(ad, bd, stride=1, pad=1))
+                    else:
+                        outs.append(x.matmul(ad, bd, relu=(kind == "mm")))
+                stream.synchronize()
+                results[i] = [o.cpu().numpy() for o in outs]
+        except Exception as e:  # reported by the main thread
+            errors.append(repr(e))
+
+    say("concurrent", len(jobs), "threads")
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(len(jobs))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not errors, errors
+    for i, ref in enumerate(refs):
+        assert results[i] is not None
+        for got in results[i]:
+            assert np.array_equal(got, ref), "job %d" % i
