@@ -1026,7 +1026,7 @@ const ConvInstance kConvInstances[] = {
     ConvInstance{make_sched(64, 256, 8, 64, 64, 32, 32, 2, 2, -1, 0, 2),   // halo, 3x3 stride 1
                  &launch_conv_f32_halo<2>,
                  &occupancy_of<&conv2d_f32_halo_kernel<2>, halo::NT, 0>},
-    XTC_CONV_TAP_INSTANCE(64, 256, 64, 64, 2, 2),    // default for OC <= 64
+    XTC_CONV_TAP_INSTANCE(64, 256, 64, 64, 2, 2),    // the halo instance's fallback
     XTC_CONV_TAP_INSTANCE(64, 128, 32, 64, 2, 3),
     XTC_CONV_TAP_INSTANCE(64, 64, 32, 32, 2, 4),
     XTC_CONV_TAP_INSTANCE(128, 128, 64, 64, 2, 3),   // default for OC > 64
