@@ -1,0 +1,64 @@
+"""Property tests of the host-side validation in libxtc.so (no GPU needed):
+arbitrary schedule fields and shapes never crash the checks, every answer is
+one of the documented status codes, a schedule the check accepts is one of
+the compiled instances, and invalid calls are refused before any device
+work (dummy pointers that a kernel would fault on)."""
+import pytest
+from hypothesis import HealthCheck, given, settings
+from hypothesis import strategies as st
+
+I32 = st.one_of(st.integers(-2 ** 31, 2 ** 31 - 1), st.sampled_from([0, 1, 2, 4, 8, 16, 32, 64, 128, 256, 512, -1]))
+FIELDS = ("block_m", "block_n", "block_k", "wave_m", "wave_n", "mfma_m", "mfma_n", "mfma_k",
+          "lds_stages", "lds_pad", "unroll_k", "raster", "xcd_remap", "k_order", "k_split")
+
+
+@pytest.fixture(scope="module")
+def x():
+    import paper_2512_16512_amd as mod
+    return mod
+
+
+@settings(max_examples=400, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
+@given(vals=st.fixed_dictionaries({f: I32 for f in FIELDS}), op=st.sampled_from([0, 1]),
+       dt=st.sampled_from([0, 1]))
+def test_sched_check_total_and_sound(x, vals, op, dt):
+    s = x.Sched(**vals)
+    st_ = x.xtc_sched_check(op, dt, s)
+    assert st_ in (0, 4, 5, 6)
+    if st_ == 0:
+        keys = {tuple(sorted(c.as_dict().items())) for c in x.xtc_sched_list(op, dt)}
+        d = s.as_dict()
+        d["raster"], d["xcd_remap"] = 0, 1
+        assert tuple(sorted(d.items())) in keys
+
+
+@settings(max_examples=300, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
+@given(M=st.integers(-5, 2 ** 40), N=st.integers(-5, 2 ** 40), K=st.integers(-5, 2 ** 40),
+       dt=st.sampled_from([0, 1]))
+def test_huge_or_negative_shapes_refused_before_launch(x, M, N, K, dt):
+    # leading dimensions equal to the extents; pointers are dummies, so only
+    # the no-op (M or N == 0) or a refusal may come back
+    BAD = 0x10
+    lda, ldb, ldc = max(K, 1), max(N, 1), max(N, 1)
+    # Only calls that are clearly invalid are made: negative or zero extents,
+    # or an operand span of at least twice the 2^31-byte limit.  Anything
+    # near the limit is skipped, so that no call can reach a launch on the
+    # dummy pointers.
+    spans = [(max(M, 1) - 1) * lda + K, (max(K, 1) - 1) * ldb + N, (max(M, 1) - 1) * ldc + N]
+    clearly_large = max(spans) * 2 >= 2 ** 32
+    if not (M < 0 or N < 0 or K < 0 or M == 0 or N == 0 or clearly_large):
+        return
+    st_ = x.xtc_matmul(M, N, K, BAD, lda, BAD, ldb, BAD, ldc, dt)
+    assert st_ in (0, 2, 3, 7)
+    if M < 0 or N < 0 or K < 0:
+        assert st_ == 2
+    elif M == 0 or N == 0:
+        assert st_ == 0
+
+
+@settings(max_examples=200, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
+@given(op=st.sampled_from([0, 1]), dt=st.sampled_from([0, 1]),
+       M=st.integers(0, 1 << 20), N=st.integers(0, 1 << 24), K=st.integers(0, 1 << 16))
+def test_default_schedule_is_always_compiled(x, op, dt, M, N, K):
+    s = x.xtc_default_schedule(op, dt, M, N, K)
+    assert x.xtc_sched_check(op, dt, s) == 0
