@@ -603,6 +603,9 @@ const GemmInstance kF32Instances[] = {
     XTC_F32_DMA_INSTANCE(256, 128, 32, 128, 64, 2),
     XTC_F32_DMA_INSTANCE(128, 128, 32, 64, 64, 2),
     XTC_F32_DMA_INSTANCE(128, 128, 16, 64, 64, 4),
+    XTC_F32_DMA_INSTANCE(64, 128, 32, 32, 64, 3),    // mid-size problems
+    XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 4),
+    XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 2),
     XTC_F32_INSTANCE(128, 128, 32, 64, 64, 32, 4),
     XTC_F32_INSTANCE(128, 128, 16, 64, 64, 32, 4),
     XTC_F32_INSTANCE(64, 64, 32, 32, 32, 32, 4),     // small problems: more tiles
