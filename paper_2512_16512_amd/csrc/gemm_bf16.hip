@@ -502,6 +502,8 @@ const GemmInstance kBf16Instances[] = {
     XTC_BF16_DMA_INSTANCE(256, 256, 64, 128, 128, 32, 2), // 4 waves of 128x128
     XTC_BF16_DMA_INSTANCE(256, 128, 32, 128, 64, 32, 3),
     XTC_BF16_DMA_INSTANCE(128, 128, 32, 64, 64, 32, 4),   // medium problems
+    XTC_BF16_DMA_INSTANCE(64, 128, 32, 32, 64, 32, 4),
+    XTC_BF16_DMA_INSTANCE(64, 128, 64, 32, 64, 32, 2),
     XTC_BF16_DMA_INSTANCE(128, 128, 64, 64, 64, 16, 2),
     XTC_BF16_INSTANCE(256, 256, 64, 128, 64, 32, 8),
     XTC_BF16_INSTANCE(128, 128, 64, 64, 64, 32, 8),

@@ -179,10 +179,14 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
         else
             *out = make_sched(16, 16, 32, 16, 16, 16, 16, 4, 0, 0, 0, 0, 4);
     } else {
+        // direct-to-LDS tiles from 256x256 down to 64x128 (half a tile per
+        // CU), then the register-staged 64x64 tiles
         if (tiles(256, 256) >= cus)
             *out = make_sched(256, 256, 32, 128, 64, 32, 32, 16, 4, -1, 0);
         else if (tiles(128, 128) >= cus)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 16, 4, -1, 0);
+        else if (tiles(64, 128) >= cus / 2)
+            *out = make_sched(64, 128, 64, 32, 64, 32, 32, 16, 2, -1, 0);
         else
             *out = make_sched(64, 64, 64, 32, 32, 32, 32, 16, 2, 8, 0);
     }

@@ -41,6 +41,7 @@ def test_sample_is_seeded_and_distinct(t):
     ("matmul", "f32", (200, 300, 96)),
     ("matmul_relu", "bf16", (130, 260, 64)),
     ("conv2d", "f32", (1, 3, 40, 40, 16, 7, 7, 2, 3)),
+    ("conv2d_relu", "bf16", (2, 16, 20, 20, 24, 3, 3, 1, 1)),
 ])
 def test_explore_small_problem(t, op, dtype, dims):
     import torch
