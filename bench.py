@@ -373,6 +373,9 @@ def main():
     ap.add_argument("--only", default="fp32,bf16,conv,conv_bf16,paper")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--vendor", action="store_true",
+                    help="also time the vendor libraries behind torch (hipBLASLt matmul, MIOpen "
+                         "conv2d) on the same workloads, as a second JSON line (comparison only)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy (the reference kernel "
                          "for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -480,6 +483,40 @@ def main():
         if "cpu_baseline" in line:
             line["cpu_baseline"]["single_thread"] = extra["oracle_single_thread"]
     print(json.dumps(line), flush=True)
+    if args.vendor:
+        print(json.dumps(vendor_line(args.steps, args.warmup, line)), flush=True)
+
+
+def vendor_line(steps: int, warmup: int, ours: dict):
+    """The same workloads through torch's vendor libraries (hipBLASLt for
+    matmul, MIOpen for conv2d), timed exactly as ours: a comparison point,
+    not part of the measured path."""
+    import torch
+    torch.backends.cuda.matmul.allow_tf32 = False
+    torch.backends.cudnn.allow_tf32 = False
+    out = {"vendor": "torch %s, HIP %s" % (torch.__version__, torch.version.hip)}
+    for kind, cfg in (("fp32", xi.CONFIGS[2]), ("bf16", xi.CONFIGS[3])):
+        A, B = xi.matmul_inputs(cfg)
+        a, b = to_dev(A), to_dev(B)
+        c = torch.empty((cfg["M"], cfg["N"]), dtype=a.dtype, device="cuda")
+        ms = time_launches(lambda: torch.matmul(a, b, out=c), steps, warmup)
+        tf = 2.0 * cfg["M"] * cfg["N"] * cfg["K"] / (ms * 1e-3) / 1e12
+        mine = ours["value"] if kind == "fp32" else ours["also"].get("bf16", {}).get("value")
+        out[kind] = {"workload": cfg["name"], "ms_per_launch": round(ms, 4), "TFLOP/s": round(tf, 2),
+                     "ours_TFLOP/s": mine, "output_dtype": str(c.dtype).replace("torch.", "")}
+        del a, b, c
+    cfg = xi.CONFIGS[4]
+    X, W = xi.conv_inputs(cfg)
+    xd, wd = to_dev(X), to_dev(W)
+    f = lambda: torch.nn.functional.conv2d(xd, wd, stride=cfg["stride"], padding=cfg["pad"])
+    ms = time_launches(f, steps, warmup)
+    OH, OW = xi.conv_out_hw(cfg["H"], cfg["W"], cfg["R"], cfg["S"], cfg["stride"], cfg["stride"],
+                            cfg["pad"], cfg["pad"])
+    flops = 2.0 * cfg["OC"] * cfg["N"] * OH * OW * cfg["C"] * cfg["R"] * cfg["S"]
+    out["conv"] = {"workload": cfg["name"], "ms_per_launch": round(ms, 4),
+                   "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2),
+                   "ours_TFLOP/s": ours["also"].get("conv", {}).get("value")}
+    return out
 
 
 if __name__ == "__main__":
