@@ -504,6 +504,18 @@ def vendor_line(steps: int, warmup: int, ours: dict):
         mine = ours["value"] if kind == "fp32" else ours["also"].get("bf16", {}).get("value")
         out[kind] = {"workload": cfg["name"], "ms_per_launch": round(ms, 4), "TFLOP/s": round(tf, 2),
                      "ours_TFLOP/s": mine, "output_dtype": str(c.dtype).replace("torch.", "")}
+        if kind == "bf16":
+            # the same operation as ours: bf16 inputs, fp32 accumulation and fp32 output
+            c32 = torch.empty((cfg["M"], cfg["N"]), dtype=torch.float32, device="cuda")
+            try:
+                ms = time_launches(lambda: torch.mm(a, b, out_dtype=torch.float32, out=c32), steps, warmup)
+                tf = 2.0 * cfg["M"] * cfg["N"] * cfg["K"] / (ms * 1e-3) / 1e12
+                out["bf16_f32_out"] = {"workload": cfg["name"], "ms_per_launch": round(ms, 4),
+                                       "TFLOP/s": round(tf, 2), "ours_TFLOP/s": mine,
+                                       "output_dtype": "float32"}
+            except (RuntimeError, TypeError) as e:
+                out["bf16_f32_out"] = {"error": str(e)[:200]}
+            del c32
         del a, b, c
     cfg = xi.CONFIGS[4]
     X, W = xi.conv_inputs(cfg)

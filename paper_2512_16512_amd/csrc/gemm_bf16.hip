@@ -387,6 +387,34 @@ gemm_bf16_dma_kernel(GemmArgs p) {
             for (int j = 0; j < G::TN; ++j) acc[i][j] = MF::mma(af[buf][i], bfr[buf][j], acc[i][j]);
     };
 
+    // The last k-step of a stage: its MFMAs with the copies of the stage
+    // STAGES ahead spread between them, so that the copies of all waves do
+    // not queue at the texture unit at once right after the barrier (which
+    // stalls the issuing waves, MFMAs included); the fences keep the
+    // compiler from regrouping them.
+    auto mfmas_with_copies = [&](int buf, int st) {
+        const unsigned base = smem_base + st * G::STAGE_BYTES;
+        constexpr int NM = G::TM * G::TN;
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            acc[m / G::TN][m % G::TN] =
+                MF::mma(af[buf][m / G::TN], bfr[buf][m % G::TN], acc[m / G::TN][m % G::TN]);
+            const int q0 = m * G::LOADS / NM, q1 = (m + 1) * G::LOADS / NM;
+            if (q1 > q0) {
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int q = q0; q < q1; ++q) {
+                    if (q < G::A_PER_WAVE)
+                        dma16(ra, base + (wave_u * G::A_PER_WAVE + q) * 1024, offA[q]);
+                    else
+                        dma16(rb, base + G::A_BYTES + (wave_u * G::B_PER_WAVE + q - G::A_PER_WAVE) * 1024,
+                              offB[q - G::A_PER_WAVE]);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    };
+
     // One MFMA followed by its share of the next step's LDS reads.
     auto interleave = [&]() {
         if constexpr (SCHED == 1) {
@@ -429,10 +457,8 @@ gemm_bf16_dma_kernel(GemmArgs p) {
         wait_vmcnt<(STAGES - 2) * G::LOADS>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        fire(st);
         load_frags((kt + 1) % STAGES, 0, 0);
-        mfmas((G::NS - 1) & 1);
-        interleave();
+        mfmas_with_copies((G::NS - 1) & 1, st);
     }
     wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
 
@@ -446,7 +472,9 @@ gemm_bf16_dma_kernel(GemmArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
-                if (row < M && col < N) C[row * ldc + col] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
+                if (row < M && col < N)
+                    __builtin_nontemporal_store((p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r],
+                                                &C[row * ldc + col]);
             }
         }
 }

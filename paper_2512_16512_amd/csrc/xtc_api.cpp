@@ -67,8 +67,10 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     // LDS budget of the staged tiles
     const int elt = dt == XTC_F32 ? 4 : 2;
     const int pad = s.lds_pad > 0 ? s.lds_pad : 0;
+    // swizzled unpadded rows (lds_pad = -1) or rows padded by lds_pad (A) and 8 (B)
+    const int bpad = s.lds_pad < 0 ? 0 : 8;
     int64_t lds = (int64_t)s.lds_stages * elt *
-                  ((int64_t)s.block_m * (s.block_k + pad) + (int64_t)s.block_n * (s.block_k + 8));
+                  ((int64_t)s.block_m * (s.block_k + pad) + (int64_t)s.block_n * (s.block_k + bpad));
     if (s.k_split > 1) lds += (int64_t)s.k_split * s.block_m * s.block_n * 4;  // partial sums
     if (lds > kLdsBytes) return XTC_ERR_BAD_SCHEDULE;
     return XTC_OK;
