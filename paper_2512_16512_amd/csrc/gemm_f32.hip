@@ -346,6 +346,33 @@ gemm_f32_dma_kernel(GemmArgs p) {
                     acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
     };
 
+    // The last fragment set of a stage: its MFMAs with the copies of the
+    // stage STAGES ahead spread between them (copies issued all at once by
+    // every wave right after the barrier queue at the texture unit and
+    // stall the issuing waves); the fences keep the order.
+    auto mfmas_with_copies = [&](int buf, int st) {
+        const unsigned base = smem_base + st * G::STAGE_BYTES;
+        constexpr int NM = 4 * G::TM * G::TN;
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            const int s = m / (G::TM * G::TN), i = (m / G::TN) % G::TM, j = m % G::TN;
+            acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
+            const int q0 = m * G::LOADS / NM, q1 = (m + 1) * G::LOADS / NM;
+            if (q1 > q0) {
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int q = q0; q < q1; ++q) {
+                    if (q < G::A_PER_WAVE)
+                        dma16(ra, base + (wave_u * G::A_PER_WAVE + q) * 1024, offA[q]);
+                    else
+                        dma16(rb, base + G::A_BYTES + (wave_u * G::B_PER_WAVE + q - G::A_PER_WAVE) * 1024,
+                              offB[q - G::A_PER_WAVE]);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    };
+
     // Branch-free main loop: every stage index issues LOADS copies per wave
     // (zero-fill copies past the end of K), so one vmcnt value is exact in
     // every iteration and the compiler's LDS waits stay tight.
@@ -370,9 +397,8 @@ gemm_f32_dma_kernel(GemmArgs p) {
         wait_vmcnt<(STAGES - 2) * G::LOADS>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        fire(st);
         load_frags((kt + 1) % STAGES, 0, 0);
-        mfmas((G::NS - 1) & 1);
+        mfmas_with_copies((G::NS - 1) & 1, st);
     }
     wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
 
@@ -386,7 +412,9 @@ gemm_f32_dma_kernel(GemmArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
-                if (row < M && col < N) C[row * ldc + col] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
+                if (row < M && col < N)
+                    __builtin_nontemporal_store((p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r],
+                                                &C[row * ldc + col]);
             }
         }
 }
