@@ -262,8 +262,9 @@ gemm_bf16_dma_kernel(GemmArgs p) {
 
     const int M = p.M, N = p.N, K = p.K;
     const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-    const int ntiles = tiles_m * tiles_n;
-    const int KT = (K + BK - 1) / BK;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
 
     const i32x4 ra = make_rsrc(p.A, ((M - 1) * p.lda + K) * 2);
     const i32x4 rb = make_rsrc(p.B, ((K - 1) * p.ldb + N) * 2);
@@ -293,40 +294,18 @@ gemm_bf16_dma_kernel(GemmArgs p) {
     // them once the target slot is free.  Every stage index issues exactly
     // LOADS copies per wave, so the number of copies in flight is the same in
     // every iteration and one vmcnt value is exact throughout.
-    //
-    // The workgroup computes tiles blockIdx.x, blockIdx.x + gridDim.x, ...
-    // (one tile when the grid has a workgroup per tile; several when the
-    // grid is limited to the workgroups the chip holds at once).  The copy
-    // ring runs on across tiles: a prefetch cursor (tile pf_t, K-stage pf_k)
-    // names the next stage to copy, so the last iterations of one tile
-    // already copy the first stages of the next, and past the workgroup's
-    // last tile the copies read zeros.
     int offA[G::A_PER_WAVE], offB[G::B_PER_WAVE];
-    int pf_t = blockIdx.x, pf_k = 0, pf_m0 = 0, pf_n0 = 0;
-    auto pf_coords = [&]() {
-        int a = 0, b = 0;
-        if (pf_t < ntiles) tile_coords(pf_t, ntiles, tiles_m, tiles_n, p.raster, p.xcd_remap, a, b);
-        pf_m0 = a * BM;
-        pf_n0 = b * BN;
-    };
-    pf_coords();
-    auto prepare = [&]() {
-        const int k0 = pf_k * BK;
-        const int mlim = pf_t < ntiles ? M : 0;  // past the last tile: zero fill
+    auto prepare = [&](int kt) {
+        const int k0 = kt * BK;
 #pragma unroll
         for (int q = 0; q < G::A_PER_WAVE; ++q) {
-            const int gm = pf_m0 + a_row[q], gk = k0 + a_col[q];
-            offA[q] = (gm < mlim && gk < K) ? (gm * p.lda + gk) * 2 : kOOB;
+            const int gm = m0 + a_row[q], gk = k0 + a_col[q];
+            offA[q] = (gm < M && gk < K) ? (gm * p.lda + gk) * 2 : kOOB;
         }
 #pragma unroll
         for (int q = 0; q < G::B_PER_WAVE; ++q) {
-            const int gk = k0 + b_row[q], gn = pf_n0 + b_col[q];
-            offB[q] = (mlim > 0 && gk < K && gn < N) ? (gk * p.ldb + gn) * 2 : kOOB;
-        }
-        if (++pf_k == KT) {
-            pf_k = 0;
-            pf_t += gridDim.x;
-            pf_coords();
+            const int gk = k0 + b_row[q], gn = n0 + b_col[q];
+            offB[q] = (gk < K && gn < N) ? (gk * p.ldb + gn) * 2 : kOOB;
         }
     };
     auto fire = [&](int st) {
@@ -450,64 +429,54 @@ gemm_bf16_dma_kernel(GemmArgs p) {
         }
     };
 
-    // The K loop is branch-free apart from the uniform cursor update: the
-    // tail iterations copy zeros into slots nobody reads any more and read
-    // fragments they do not use, which keeps the compiler's LDS-wait
-    // analysis exact (no conservative waits at control-flow merges in front
-    // of the last k-step's MFMAs).
+    // The loop body is branch-free: the tail iterations copy zeros into
+    // slots nobody reads any more and read fragments they do not use, which
+    // keeps the compiler's LDS-wait analysis exact (no conservative waits at
+    // control-flow merges in front of the last k-step's MFMAs).
+    const int KT = (K + BK - 1) / BK;
 #pragma unroll
     for (int s = 0; s < STAGES; ++s) {
-        prepare();
+        prepare(s);
         fire(s);
     }
     wait_vmcnt<(STAGES - 1) * G::LOADS>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     load_frags(0, 0, 0);
-    int slot = 0;  // ring slot of the stage being consumed
-    float *__restrict__ C = p.C;
-    const int ldc = p.ldc;
-    for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
-        for (int kt = 0; kt < KT; ++kt) {
-            const int st = slot;
-            prepare();
+    for (int kt = 0; kt < KT; ++kt) {
+        const int st = kt % STAGES;
+        prepare(kt + STAGES);
 #pragma unroll
-            for (int s = 0; s + 1 < G::NS; ++s) {
-                load_frags(st, s + 1, (s + 1) & 1);
-                mfmas(s & 1);
-                interleave();
-            }
-            // the next stage has landed (this wave's copies, then everyone's;
-            // loads complete in order, so C stores issued in between only
-            // make this wait longer); the barrier also frees slot st, whose
-            // fragments are all in registers
-            wait_vmcnt<(STAGES - 2) * G::LOADS>();
-            __builtin_amdgcn_s_barrier();
-            asm volatile("" ::: "memory");
-            slot = slot + 1 == STAGES ? 0 : slot + 1;
-            load_frags(slot, 0, 0);
-            mfmas_with_copies((G::NS - 1) & 1, st);
+        for (int s = 0; s + 1 < G::NS; ++s) {
+            load_frags(st, s + 1, (s + 1) & 1);
+            mfmas(s & 1);
+            interleave();
         }
-
-        int tm, tn;
-        tile_coords(t, ntiles, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
-        const int m0 = tm * BM, n0 = tn * BN;
-#pragma unroll
-        for (int i = 0; i < G::TM; ++i)
-#pragma unroll
-            for (int j = 0; j < G::TN; ++j) {
-                const int col = n0 + wn * WN + j * MI + lrow;
-#pragma unroll
-                for (int r = 0; r < MF::NACC; ++r) {
-                    const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
-                    if (row < M && col < N)
-                        __builtin_nontemporal_store(
-                            (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r], &C[row * ldc + col]);
-                    acc[i][j][r] = 0.f;
-                }
-            }
+        // stage kt+1 has landed (this wave's copies, then everyone's); the
+        // barrier also frees slot st, whose fragments are all in registers
+        wait_vmcnt<(STAGES - 2) * G::LOADS>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        load_frags((kt + 1) % STAGES, 0, 0);
+        mfmas_with_copies((G::NS - 1) & 1, st);
     }
     wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
+
+    float *__restrict__ C = p.C;
+    const int ldc = p.ldc;
+#pragma unroll
+    for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < G::TN; ++j) {
+            const int col = n0 + wn * WN + j * MI + lrow;
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
+                if (row < M && col < N)
+                    __builtin_nontemporal_store((p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r],
+                                                &C[row * ldc + col]);
+            }
+        }
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES, int AMODE, int SCHED>
