@@ -839,24 +839,30 @@ conv2d_f32_halo_kernel(ConvArgs p) {
     const int b_base0 = (img * C + wave_u * (CC / NWAVES)) * HW4;
 
     int so_a = a_base0, so_b = b_base0;      // offsets of the next stage to fire
-    auto fire = [&](int st) {
+    // Copy q (0 .. LOADS-1) of the stage in slot st: weights first, then the
+    // patch rows.
+    auto copy = [&](int st, int q) __attribute__((always_inline)) {
         const unsigned base = smem_base + st * STAGE_BYTES;
-#pragma unroll
-        for (int q = 0; q < A_PER_WAVE; ++q) {
+        if (q < A_PER_WAVE) {
             const int cq = wave_u * A_PER_WAVE + q;          // copy index: tap-major
             const int tap = cq / 8, ocb = cq % 8;
             dma4_so(rw, base + (tap * BM * CC + ocb * 64) * 4, voffA,
                     so_a + (ocb * 8 * C * NTAP + tap) * 4);
-        }
-#pragma unroll
-        for (int q = 0; q < B_PER_WAVE; ++q) {
-            const int cl = q / PR, row = q % PR;             // channel of this wave, patch row
+        } else {
+            const int cl = (q - A_PER_WAVE) / PR, row = (q - A_PER_WAVE) % PR;  // channel, patch row
             const int ihc = min(max(ih0 + row, 0), H - 1);
             dma4_so(rx, base + A_BYTES + ((wave_u * (CC / NWAVES) + cl) * PLANE + row * 64) * 4,
                     voffR[row], so_b + cl * HW4 + ihc * Wd * 4);
         }
+    };
+    auto advance = [&]() {
         so_a += a_stage;
         so_b += b_stage;
+    };
+    auto fire = [&](int st) {
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) copy(st, q);
+        advance();
     };
 
     // Per-lane fragment bases.  A: row (i*32 + lrow), channels 4*lgrp .. +3.
@@ -913,6 +919,23 @@ conv2d_f32_halo_kernel(ConvArgs p) {
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
     };
+    // The last tap's MFMAs with the copies of the stage STAGES ahead spread
+    // between them: issued all at once right after the barrier, the copies of
+    // every wave queue at the texture unit and stall the issuing waves.
+    auto mfmas_with_copies = [&](int buf, int st) __attribute__((always_inline)) {
+        constexpr int NM = 4 * TM * TN;
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            const int s = m / (TM * TN), i = (m / TN) % TM, j = m % TN;
+            acc[i][j] = MF::mma(af[buf][i][s], bfr[buf][j][s], acc[i][j]);
+            const int q0 = m * LOADS / NM, q1 = (m + 1) * LOADS / NM;
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = q0; q < q1; ++q) copy(st, q);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        advance();
+    };
 
     // One stage: nine taps, fragments of tap t + 1 read while tap t runs;
     // the barrier that frees this stage's slot sits before the last tap.  P
@@ -929,9 +952,8 @@ conv2d_f32_halo_kernel(ConvArgs p) {
         wait_vmcnt<(STAGES - 2) * LOADS>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        fire(st);
         load_frags((kt + 1) % STAGES, 0, (P + NTAP) & 1);
-        mfmas((P + NTAP - 1) & 1);
+        mfmas_with_copies((P + NTAP - 1) & 1, st);
     };
 
 #pragma unroll
@@ -956,8 +978,207 @@ conv2d_f32_halo_kernel(ConvArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int oc = m0 + i * MI + MF::row(lane, r);
-                if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
+                if (oc < OC)
+                    __builtin_nontemporal_store((p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r],
+                                                &Y[oc * OHW + pix]);
             }
+    }
+}
+
+// Balanced halo-tiled kernel (k_order = 2, 16x16x4 instruction tile).  The
+// same input-patch staging as the kernel above, with tiles sized so that the
+// workgroups of a launch split evenly over the CUs: a workgroup computes 64
+// output channels x PT consecutive output pixels of one image, where the
+// launcher picks PT <= 208 as OHW divided into the fewest tiles per image
+// (3136 pixels -> 16 tiles of 196; 32 images -> 512 workgroups, two per CU).
+// Each of the four waves owns 16 output channels and all thirteen 16-pixel
+// column blocks, so every wave does the same work whatever PT is; columns
+// past the tile are computed and not stored.  For the 16x16x4 instruction a
+// lane holds the weight of (channel 4s + lane/16, output channel lane%16)
+// and the input value of (channel 4s + lane/16, pixel lane%16), so the four
+// lane groups read four channel planes; planes are 8*64 + 16 floats apart,
+// 16 banks, which keeps the groups on disjoint banks unless a 16-pixel
+// block wraps to the next image row.
+namespace halo16 {
+constexpr int BM = 64, NWAVES = 4, NT = 256;
+constexpr int NB = 13;                        // 16-pixel column blocks per wave
+constexpr int BN = 16 * NB;                   // largest pixel tile (208)
+constexpr int CC = 8, NTAP = 9, PR = 8, CO = 4;
+constexpr int NSTEP = NTAP * CC / 4;          // instruction k-steps per stage (18)
+constexpr int PLANE = PR * 64 + 16;
+constexpr int A_FLOATS = NTAP * BM * CC;      // [tap][oc][c]
+constexpr int A_BYTES = A_FLOATS * 4;
+constexpr int B_BYTES = CC * PLANE * 4;
+constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+constexpr int A_COPIES = A_FLOATS / 64;       // 72
+constexpr int A_PER_WAVE = A_COPIES / NWAVES; // 18
+constexpr int B_COPIES = CC * PR;             // 64
+constexpr int B_PER_WAVE = B_COPIES / NWAVES; // 16: two channels x eight rows
+constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;
+static_assert(A_PER_WAVE * NWAVES == A_COPIES && B_PER_WAVE * NWAVES == B_COPIES, "copy split");
+static_assert((PLANE % 64) == 16, "lane groups 16 banks apart");
+static_assert(NSTEP % 2 == 0, "fragment buffers keep their parity from stage to stage");
+}  // namespace halo16
+
+template <int STAGES>
+__global__ void __launch_bounds__(halo16::NT)
+conv2d_f32_halo16_kernel(ConvArgs p) {
+    using namespace halo16;
+    typedef F32Mfma<16> MF;
+    static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
+    static_assert(STAGES * STAGE_BYTES <= 80 * 1024, "two workgroups per CU");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * STAGE_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int lcol = lane & 15, lgrp = lane >> 4;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+
+    const int C = p.C, H = p.H, Wd = p.W;
+    const int OC = p.OC, OW = p.OW, OHW = p.OH * p.OW;
+    const int PT = p.tile_px;
+    const int chunks = (OHW + PT - 1) / PT;   // per image
+    const int tiles_m = (OC + BM - 1) / BM, tiles_n = p.Nb * chunks;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM;
+    const int img = tn / chunks, p0 = (tn - img * chunks) * PT;
+    const int pend = min(p0 + PT, OHW);
+    const int oh0 = p0 / OW;                  // first output row of the tile
+    const int ih0 = oh0 - p.ph;               // input row of patch row 0
+    const int KT = C / CC;                    // stages
+
+    const i32x4 rw = make_rsrc(p.Wt, OC * C * NTAP * 4);
+    const i32x4 rx = make_rsrc(p.X, p.Nb * C * H * Wd * 4);
+    const unsigned smem_base = lds_address(smem);
+
+    // Copies as in the 64x256 halo kernel: a fixed per-lane vector offset
+    // plus a scalar offset that moves by a constant per stage; padding and
+    // rows outside the image are out-of-range offsets that read zero, and
+    // stages past the end read in range or zero and are never used.
+    const int voffA = ((lane >> 3) * C * NTAP + (lane & 7) * NTAP) * 4;
+    const int iwl = lane - CO;
+    const int voffB = (iwl >= 0 && iwl < Wd) ? iwl * 4 : kOOB;
+    int voffR[PR];
+#pragma unroll
+    for (int r = 0; r < PR; ++r) voffR[r] = (ih0 + r >= 0 && ih0 + r < H) ? voffB : kOOB;
+    const int HW4 = H * Wd * 4;
+    const int a_stage = CC * NTAP * 4;
+    const int b_stage = CC * HW4;
+    int so_a = (m0 * C * NTAP) * 4;
+    int so_b = (img * C + wave_u * (CC / NWAVES)) * HW4;
+    auto copy = [&](int st, int q) __attribute__((always_inline)) {
+        const unsigned base = smem_base + st * STAGE_BYTES;
+        if (q < A_PER_WAVE) {
+            const int cq = wave_u * A_PER_WAVE + q;          // copy index: tap-major
+            const int tap = cq / 8, ocb = cq % 8;
+            dma4_so(rw, base + (tap * BM * CC + ocb * 64) * 4, voffA,
+                    so_a + (ocb * 8 * C * NTAP + tap) * 4);
+        } else {
+            const int cl = (q - A_PER_WAVE) / PR, row = (q - A_PER_WAVE) % PR;
+            const int ihc = min(max(ih0 + row, 0), H - 1);
+            dma4_so(rx, base + A_BYTES + ((wave_u * (CC / NWAVES) + cl) * PLANE + row * 64) * 4,
+                    voffR[row], so_b + cl * HW4 + ihc * Wd * 4);
+        }
+    };
+    auto advance = [&]() {
+        so_a += a_stage;
+        so_b += b_stage;
+    };
+
+    // Fragment bases.  A: output channel 16*wave + lcol, channel lgrp (+4s).
+    // B: pixel p0 + 16j + lcol of the patch (clamped to position 0 past the
+    // tile; such columns are not stored), channel plane lgrp (+4s).
+    const int a_base = ((wave * 16 + lcol) * CC + lgrp) * 4;
+    int b_base[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int pix = p0 + 16 * j + lcol;
+        int off = 0;
+        if (pix < pend) {
+            const int oh = pix / OW, ow = pix - oh * OW;
+            off = (oh - oh0) * 64 + ow - p.pw + CO;
+        }
+        b_base[j] = (lgrp * PLANE + off) * 4;
+    }
+
+    typename MF::acc_t acc[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int r = 0; r < MF::NACC; ++r) acc[j][r] = 0.f;
+
+    float af[2], bfr[2][NB];
+    // k-step t of a stage: tap t / 2, channels 4 * (t % 2) .. + 3
+    auto load_frags = [&](int st, int t, int buf) __attribute__((always_inline)) {
+        const unsigned char *As = smem + st * STAGE_BYTES;
+        const unsigned char *Bs = As + A_BYTES;
+        const int tap = t >> 1, s = t & 1;
+        const int kh = tap / 3, kw = tap - 3 * kh;
+        af[buf] = *reinterpret_cast<const float *>(As + a_base + (tap * BM * CC + 4 * s) * 4);
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+            bfr[buf][j] = *reinterpret_cast<const float *>(Bs + b_base[j] + (4 * s * PLANE + kh * 64 + kw) * 4);
+    };
+    auto mfmas = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) acc[j] = MF::mma(af[buf], bfr[buf][j], acc[j]);
+    };
+    // The last k-step's MFMAs with the copies of the stage STAGES ahead
+    // spread between them (copies issued all at once right after the barrier
+    // queue at the texture unit and stall the issuing waves).
+    auto mfmas_with_copies = [&](int buf, int st) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            acc[j] = MF::mma(af[buf], bfr[buf][j], acc[j]);
+            const int q0 = j * LOADS / NB, q1 = (j + 1) * LOADS / NB;
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = q0; q < q1; ++q) copy(st, q);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        advance();
+    };
+
+#pragma unroll
+    for (int s = 0; s < STAGES; ++s) {
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) copy(s, q);
+        advance();
+    }
+    wait_vmcnt<(STAGES - 1) * LOADS>();
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    load_frags(0, 0, 0);
+    for (int kt = 0; kt < KT; ++kt) {
+        const int st = kt % STAGES;
+#pragma unroll
+        for (int t = 0; t + 1 < NSTEP; ++t) {
+            load_frags(st, t + 1, (t + 1) & 1);
+            mfmas(t & 1);
+        }
+        // the next stage has landed; the barrier also frees slot st, whose
+        // fragments are all in registers
+        wait_vmcnt<(STAGES - 2) * LOADS>();
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        load_frags((kt + 1) % STAGES, 0, 0);
+        mfmas_with_copies((NSTEP - 1) & 1, st);
+    }
+    wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
+
+    float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int pix = p0 + 16 * j + lcol;
+        if (pix >= pend) continue;
+#pragma unroll
+        for (int r = 0; r < MF::NACC; ++r) {
+            const int oc = m0 + 16 * wave + MF::row(lane, r);
+            if (oc < OC)
+                __builtin_nontemporal_store((p.relu && acc[j][r] < 0.f) ? 0.f : acc[j][r],
+                                            &Y[oc * OHW + pix]);
+        }
     }
 }
 
@@ -982,6 +1203,35 @@ hipError_t launch_conv_f32_halo(const ConvArgs &a, hipStream_t s) {
     void *kargs[] = {&args};
     return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_halo_kernel<STAGES>),
                            dim3(tiles), dim3(halo::NT), kargs, 0, s);
+}
+
+// Tiles per image for the balanced halo kernel: the fewest that keep a tile
+// within 208 pixels; 0 when the shape is outside the kernel's class (then
+// the 64x256 halo kernel, or the tap-major kernel, runs).
+inline int halo16_tile_px(const ConvArgs &a) {
+    using namespace halo16;
+    if (a.R != 3 || a.S != 3 || a.sh != 1 || a.sw != 1) return 0;
+    if (a.C % CC != 0 || a.pw > CO) return 0;
+    if (a.OW - a.pw + 5 > 63) return 0;                  // last patch column used (W + pw <= 60)
+    const int OHW = a.OH * a.OW;
+    const int t = (OHW + BN - 1) / BN;
+    const int pt = (OHW + t - 1) / t;
+    const int span = (pt - 1 + a.OW - 1) / a.OW + 1;      // output rows a tile can touch
+    return span + 2 <= PR ? pt : 0;
+}
+
+template <int STAGES>
+hipError_t launch_conv_f32_halo16(const ConvArgs &a, hipStream_t s) {
+    const int pt = halo16_tile_px(a);
+    if (pt == 0) return launch_conv_f32_halo<STAGES>(a, s);
+    ConvArgs args = a;
+    args.tile_px = pt;
+    const int OHW = a.OH * a.OW;
+    const unsigned tiles = (unsigned)(((a.OC + halo16::BM - 1) / halo16::BM) * a.Nb *
+                                      ((OHW + pt - 1) / pt));
+    void *kargs[] = {&args};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_halo16_kernel<STAGES>),
+                           dim3(tiles), dim3(halo16::NT), kargs, 0, s);
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD>
@@ -1023,6 +1273,9 @@ hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
     }
 
 const ConvInstance kConvInstances[] = {
+    ConvInstance{make_sched(64, 208, 8, 16, 208, 16, 16, 4, 2, -1, 0, 2),  // balanced halo, 3x3 stride 1
+                 &launch_conv_f32_halo16<2>,
+                 &occupancy_of<&conv2d_f32_halo16_kernel<2>, halo16::NT, 0>},
     ConvInstance{make_sched(64, 256, 8, 64, 64, 32, 32, 2, 2, -1, 0, 2),   // halo, 3x3 stride 1
                  &launch_conv_f32_halo<2>,
                  &occupancy_of<&conv2d_f32_halo_kernel<2>, halo::NT, 0>},

@@ -35,8 +35,13 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 // was compiled.
 xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     if (s.size != (int32_t)sizeof(xtc_sched)) return XTC_ERR_BAD_SCHEDULE;
-    if (!pow2(s.block_m) || !pow2(s.block_n) || !pow2(s.block_k) || !pow2(s.wave_m) ||
-        !pow2(s.wave_n))
+    // Tile sizes are powers of two, except the pixel dimension of the conv
+    // kernels that stage an input patch (k_order 2), whose workgroups cover
+    // a whole number of 16-pixel instruction blocks.
+    const bool any_n = op == XTC_OP_CONV2D && s.k_order == 2 && s.block_n > 0 && s.block_n % 16 == 0 &&
+                       s.wave_n > 0 && s.wave_n % 16 == 0;
+    if (!pow2(s.block_m) || !pow2(s.block_k) || !pow2(s.wave_m) ||
+        (!any_n && (!pow2(s.block_n) || !pow2(s.wave_n))))
         return XTC_ERR_BAD_SCHEDULE;
     if (s.block_m % s.wave_m || s.block_n % s.wave_n) return XTC_ERR_BAD_SCHEDULE;
     if (s.k_split != 1 && s.k_split != 2 && s.k_split != 4 && s.k_split != 8)
@@ -56,7 +61,11 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
             return XTC_ERR_BAD_SCHEDULE;
     }
     if (s.wave_m % s.mfma_m || s.wave_n % s.mfma_n) return XTC_ERR_BAD_SCHEDULE;
-    const int kchunk = dt == XTC_F32 ? 4 * (64 / s.mfma_m) : s.mfma_k;
+    // block_k: a whole number of fragment sets (fp32: 4 k per lane group);
+    // for the patch-staging conv kernels it counts channels per stage, a
+    // whole number of instruction k-steps
+    const int kchunk = (op == XTC_OP_CONV2D && s.k_order == 2) ? s.mfma_k
+                       : dt == XTC_F32 ? 4 * (64 / s.mfma_m) : s.mfma_k;
     if (s.block_k % kchunk) return XTC_ERR_BAD_SCHEDULE;
     if (s.lds_stages < (s.k_split > 1 ? 0 : 1) || s.lds_stages > 4) return XTC_ERR_BAD_SCHEDULE;
     if (s.lds_pad < -1 || s.lds_pad > 64) return XTC_ERR_BAD_SCHEDULE;
@@ -145,13 +154,15 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
         return XTC_OK;
     }
     if (op == XTC_OP_CONV2D) {
-        // 64x256 tiles of 4 waves (64x64 each) with a two-stage ring: two
-        // workgroups per CU, so up to 512 tiles run in a single wave; the
-        // halo-tiled kernel where the shape allows it (3x3, stride 1, rows
-        // of about 56 pixels), else the tap-major kernel.  When
+        // The balanced halo-tiled kernel where the shape allows it (3x3,
+        // stride 1, rows of about 56 pixels): 64 output channels x at most
+        // 208 pixels per workgroup, the pixel tile sized so that the
+        // workgroups split evenly over the CUs; else the tap-major kernel's
+        // 64x256 tiles of 4 waves (64x64 each) with a two-stage ring, two
+        // workgroups per CU, so up to 512 tiles run in a single wave.  When
         // that leaves CUs idle (a small image batch), 64x64 tiles of four
         // 32x32 waves give four times as many workgroups.
-        *out = make_sched(64, 256, 8, 64, 64, 32, 32, 2, 2, -1, 0, 2);
+        *out = make_sched(64, 208, 8, 16, 208, 16, 16, 4, 2, -1, 0, 2);
         if (M > 64)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
         else if (tiles(64, 256) < cus)
@@ -337,6 +348,7 @@ xtc_status conv_impl(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int
     a.Y = Y;
     a.raster = s.raster; a.xcd_remap = s.xcd_remap;
     a.relu = relu;
+    a.tile_px = 0;
     return hip_status(inst->launch(a, static_cast<hipStream_t>(stream)));
 }
 

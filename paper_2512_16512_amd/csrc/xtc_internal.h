@@ -36,6 +36,7 @@ struct ConvArgs {
     int raster;
     int xcd_remap;
     int relu;       // 1: the epilogue writes relu(acc) = (acc < 0 ? 0 : acc) (fused consumer)
+    int tile_px;    // output pixels per workgroup tile (set by launchers that choose it)
 };
 
 using GemmLaunch = hipError_t (*)(const GemmArgs &, hipStream_t);

@@ -146,6 +146,7 @@ def test_small_int_exact_every_instance(x, dtype, M, N, K):
     (2, 32, 54, 53, 70, 3, 3, 1, 1),    # halo: odd width, OC > 64 with a ragged weight tile
     (1, 16, 57, 55, 20, 3, 3, 1, 0),    # halo: no padding (53 x 55 output)
     (1, 48, 56, 56, 16, 3, 3, 1, 2),    # halo: pad 2 (58-wide output rows), six stages
+    (1, 24, 56, 56, 64, 3, 3, 1, 1),    # balanced halo: 8-channel stages, odd stage count
 ])
 def test_conv_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape
