@@ -365,6 +365,17 @@ def _cpu_model():
     return "unknown"
 
 
+def head_shape(kind: str) -> dict:
+    """Shape and layout keys of a headline workload for the JSON config."""
+    if kind in ("fp32", "bf16"):
+        cfg = xi.CONFIGS[2 if kind == "fp32" else 3]
+        return {"M": cfg["M"], "N": cfg["N"], "K": cfg["K"],
+                "layout": "row-major A[M,K], B[K,N], C[M,N]"}
+    cfg = xi.CONFIGS[4]
+    return {k: cfg[k] for k in ("N", "C", "H", "W", "OC", "R", "S", "stride", "pad")} | {
+        "layout": "X NCHW, W OIHW, Y NCHW"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -462,13 +473,13 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if head_kind != "bf16" else "bf16",
         "data": "synthetic: splitmix64 uniform [-1,1) inputs from fixed seeds, resident in HBM",
-        "config": {
-            "workload": head["workload"],
-            "M": 4096, "N": 4096, "K": 4096, "layout": "row-major A[M,K], B[K,N], C[M,N]",
-            "schedule": head["schedule"],
-            "device": torch.cuda.get_device_name(0),
-            "hip": torch.version.hip,
-        },
+        "config": dict(
+            {"workload": head["workload"]},
+            **head_shape(head_kind),
+            schedule=head["schedule"],
+            device=torch.cuda.get_device_name(0),
+            hip=torch.version.hip,
+        ),
         "launch_stats": head["launch_stats"],
         "roofline": head["roofline"],
         "frac_of_peak": head["frac_of_peak"],

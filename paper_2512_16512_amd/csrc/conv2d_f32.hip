@@ -978,9 +978,7 @@ conv2d_f32_halo_kernel(ConvArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int oc = m0 + i * MI + MF::row(lane, r);
-                if (oc < OC)
-                    __builtin_nontemporal_store((p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r],
-                                                &Y[oc * OHW + pix]);
+                if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
             }
     }
 }
@@ -1175,9 +1173,7 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
 #pragma unroll
         for (int r = 0; r < MF::NACC; ++r) {
             const int oc = m0 + 16 * wave + MF::row(lane, r);
-            if (oc < OC)
-                __builtin_nontemporal_store((p.relu && acc[j][r] < 0.f) ? 0.f : acc[j][r],
-                                            &Y[oc * OHW + pix]);
+            if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[j][r] < 0.f) ? 0.f : acc[j][r];
         }
     }
 }

@@ -412,9 +412,7 @@ gemm_f32_dma_kernel(GemmArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int row = m0 + wm * WM + i * MI + MF::row(lane, r);
-                if (row < M && col < N)
-                    __builtin_nontemporal_store((p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r],
-                                                &C[row * ldc + col]);
+                if (row < M && col < N) C[row * ldc + col] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
             }
         }
 }
