@@ -207,15 +207,17 @@ __device__ __forceinline__ int swz_a_f32(int row) {
     return CA == 4 ? ((row >> 1) ^ (row >> 3)) & 3 : (row ^ (row >> 3)) & 7;
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+template <int BM, int BN, int BK, int WM, int WN, int MI_, int STAGES>
 struct F32DmaCfg {
-    static constexpr int MI = 32;
+    static constexpr int MI = MI_;
     static constexpr int NWM = BM / WM, NWN = BN / WN;
     static constexpr int NWAVES = NWM * NWN;
     static constexpr int NT = NWAVES * 64;
     static constexpr int TM = WM / MI, TN = WN / MI;
     typedef F32Mfma<MI> MF;
-    static constexpr int KCH = 4 * MF::KG;          // k per fragment set (8)
+    static constexpr int KG = MF::KG;               // lane groups along k (2 or 4)
+    static constexpr int KCH = 4 * KG;              // k per fragment set (8 or 16)
+    static constexpr int SWB = 16 / KG;             // B chunk XOR step between lane groups
     static constexpr int NS = BK / KCH;
     static constexpr int RA = BK * 4, CA = BK / 4;  // A row bytes / chunks
     static constexpr int RB = BN * 4, CB = BN / 4;  // B row bytes / chunks
@@ -228,15 +230,16 @@ struct F32DmaCfg {
                   "tiles must split into whole 1 KiB blocks per wave");
     static_assert(CA == 4 || CA == 8, "block_k must be 16 or 32");
     static_assert(CB >= 16 && RB <= 1024, "block_n must be 64..256");
+    static_assert(SWB * (KG - 1) < CB, "B swizzle stays inside a row");
     static_assert(NS % 2 == 0, "an even number of fragment sets per stage");
     static_assert(STAGES >= 2 && STAGES * STAGE_BYTES <= 160 * 1024, "LDS budget");
     static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
 };
 
-template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+template <int BM, int BN, int BK, int WM, int WN, int MI_, int STAGES>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 gemm_f32_dma_kernel(GemmArgs p) {
-    typedef F32DmaCfg<BM, BN, BK, WM, WN, STAGES> G;
+    typedef F32DmaCfg<BM, BN, BK, WM, WN, MI_, STAGES> G;
     typedef typename G::MF MF;
     constexpr int MI = G::MI;
     __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * G::STAGE_BYTES];
@@ -269,7 +272,7 @@ gemm_f32_dma_kernel(GemmArgs p) {
     for (int q = 0; q < G::B_PER_WAVE; ++q) {
         const int row = (wave * G::B_PER_WAVE + q) * (1024 / G::RB) + lane / G::CB;
         b_row[q] = row;
-        b_col[q] = 4 * ((lane % G::CB) ^ (8 * ((row >> 2) & 1)));
+        b_col[q] = 4 * ((lane % G::CB) ^ (G::SWB * ((row >> 2) & (G::KG - 1))));
     }
 
     int offA[G::A_PER_WAVE], offB[G::B_PER_WAVE];
@@ -303,11 +306,11 @@ gemm_f32_dma_kernel(GemmArgs p) {
         a_off[i] = row * G::RA;
         a_swz[i] = swz_a_f32<G::CA>(row);
     }
-    // B row kk + 4*lgrp + s has (row >> 2) & 1 == lgrp & 1 (kk % 8 == 0).
+    // B row kk + 4*lgrp + s has (row >> 2) % KG == lgrp (kk % (4*KG) == 0).
     int b_off[G::TN];
 #pragma unroll
     for (int j = 0; j < G::TN; ++j)
-        b_off[j] = (4 * lgrp * BN + ((wn * WN + j * MI + lrow) ^ (32 * (lgrp & 1)))) * 4;
+        b_off[j] = (4 * lgrp * BN + ((wn * WN + j * MI + lrow) ^ (4 * G::SWB * lgrp))) * 4;
 
     typename MF::acc_t acc[G::TM][G::TN];
 #pragma unroll
@@ -417,14 +420,14 @@ gemm_f32_dma_kernel(GemmArgs p) {
         }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int STAGES>
+template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES>
 hipError_t launch_f32_dma(const GemmArgs &a, hipStream_t s) {
-    typedef F32DmaCfg<BM, BN, BK, WM, WN, STAGES> G;
+    typedef F32DmaCfg<BM, BN, BK, WM, WN, MI, STAGES> G;
     const unsigned tiles = (unsigned)(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
     GemmArgs args = a;
     void *kargs[] = {&args};
     return hipLaunchKernel(
-        reinterpret_cast<const void *>(&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, STAGES>),
+        reinterpret_cast<const void *>(&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES>),
         dim3(tiles), dim3(G::NT), kargs, 0, s);
 }
 
@@ -604,12 +607,13 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
     }
 
 // Direct-to-LDS ring (lds_pad = -1); register-staged fallback, same tiles.
-#define XTC_F32_DMA_INSTANCE(BM, BN, BK, WM, WN, STAGES)                                      \
+#define XTC_F32_DMA_INSTANCE(BM, BN, BK, WM, WN, STAGES) XTC_F32_DMA_MI_INSTANCE(BM, BN, BK, WM, WN, 32, STAGES)
+#define XTC_F32_DMA_MI_INSTANCE(BM, BN, BK, WM, WN, MI, STAGES)                               \
     GemmInstance {                                                                            \
-        make_sched(BM, BN, BK, WM, WN, 32, 32, 2, STAGES, -1, 0),                             \
-            &launch_f32_dma<BM, BN, BK, WM, WN, STAGES>,                                      \
-            &launch_f32<BM, BN, BK, WM, WN, 32, 4, false>, kWholeChunks,                      \
-            &occupancy_of<&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, STAGES>,                   \
+        make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 2 : 4), STAGES, -1, 0),             \
+            &launch_f32_dma<BM, BN, BK, WM, WN, MI, STAGES>,                                  \
+            &launch_f32<BM, BN, BK, WM, WN, MI, 4, false>, kWholeChunks,                      \
+            &occupancy_of<&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES>,               \
                           (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
@@ -629,6 +633,7 @@ const GemmInstance kF32Instances[] = {
     XTC_F32_DMA_INSTANCE(256, 128, 32, 128, 64, 2),
     XTC_F32_DMA_INSTANCE(128, 128, 32, 64, 64, 2),
     XTC_F32_DMA_INSTANCE(128, 128, 16, 64, 64, 4),
+    XTC_F32_DMA_MI_INSTANCE(128, 128, 32, 64, 64, 16, 2),   // 16x16x4 instruction tile
     XTC_F32_DMA_INSTANCE(64, 128, 32, 32, 64, 3),    // mid-size problems
     XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 4),
     XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 2),
