@@ -207,6 +207,229 @@ hipError_t launch_conv_bf16(const ConvArgs &a, hipStream_t s) {
     return hipLaunchKernel(fn, dim3(tiles), dim3((BM / WM) * (BN / WN) * 64), kargs, dyn, s);
 }
 
+// ---------------------------------------------------------------------------
+// Halo-tiled bf16 kernel (k_order = 2) for stride-1 3x3 convolutions of rows
+// of about 56 pixels.  The gather above loads every input value once per
+// tap; here a stage stages a 16-channel input patch once for all nine taps:
+//  - a workgroup computes 64 output channels x 256 consecutive output pixels
+//    of one image (four 64x64 waves of 32x32x16 instructions).  The pixels
+//    span at most 6 output rows when OW >= 51, so their inputs fit in a patch
+//    of PR = 8 input rows;
+//  - the patch is stored channel-innermost, [half][row][column][8 channels],
+//    16 bytes per cell: the B fragment of a lane (8 channels of one pixel at
+//    one tap) is then one 16-byte read of the cell the tap points at, for
+//    any column shift.  Input column iw sits at patch column iw + CO;
+//    columns and rows outside the image hold zeros;
+//  - the patch is filled through registers: a thread loads one dword (two
+//    neighbouring input columns) of each of the 16 channels and repacks them
+//    into the two columns' cells.  NCHW rows of even width keep every pair
+//    dword-aligned;
+//  - the weights of a stage, W[oc][c0 .. c0+15][kh][kw], are 144 contiguous
+//    values per output channel (16-byte aligned when C % 16 == 0); a thread
+//    loads one 8-channel slab (72 values) and repacks it into the
+//    [tap][oc][16 channels] cells of the A fragments;
+//  - the reduction runs over 16-channel chunks and, inside a chunk, over the
+//    taps; an instruction's two k lane groups take channels 0-7 and 8-15 of
+//    the tap.
+namespace halo_bf16 {
+constexpr int BM = 64, BN = 256, WM = 64, WN = 64, NWAVES = 4, NT = 256;
+constexpr int MI = 32, TM = WM / MI, TN = WN / MI;
+constexpr int CC = 16;                        // channels per stage
+constexpr int NTAP = 9;
+constexpr int PR = 8;                         // patch rows
+constexpr int PC = 64;                        // patch columns
+constexpr int CO = 2;                         // patch column of input column 0 (even)
+constexpr int CELL = 16;                      // bytes: 8 channels of one (row, column)
+constexpr int HALF = PR * PC * CELL;          // one 8-channel half of the patch
+constexpr int P_BYTES = 2 * HALF;
+constexpr int W_BYTES = NTAP * BM * CC * 2;   // [tap][oc][16 channels]
+constexpr int STAGE_BYTES = P_BYTES + W_BYTES;
+static_assert(NT == PR * PC / 2, "one patch column pair per thread");
+static_assert(2 * BM <= NT, "one weight slab per thread");
+}  // namespace halo_bf16
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__global__ void __launch_bounds__(halo_bf16::NT)
+conv2d_bf16_halo_kernel(ConvArgs p) {
+    using namespace halo_bf16;
+    typedef Bf16Mfma<MI> MF;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[2 * STAGE_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int lrow = lane % MI, lgrp = lane / MI;   // lgrp: channel half of the fragments
+
+    const int C = p.C, H = p.H, Wd = p.W;
+    const int OC = p.OC, OW = p.OW, OHW = p.OH * p.OW;
+    const int chunks = (OHW + BN - 1) / BN;   // per image
+    const int tiles_m = (OC + BM - 1) / BM, tiles_n = p.Nb * chunks;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM;
+    const int img = tn / chunks, p0 = (tn - img * chunks) * BN;
+    const int oh0 = p0 / OW;                  // first output row of the tile
+    const int ih0 = oh0 - p.ph;               // input row of patch row 0
+    const int KT = C / CC;
+
+    const unsigned *__restrict__ X = reinterpret_cast<const unsigned *>(p.X);    // bf16 pairs
+    const u32x4_t *__restrict__ Wv = reinterpret_cast<const u32x4_t *>(p.Wt);   // 16-byte chunks
+
+    // Patch loads: patch row pr, column pair cp (input columns 2cp - CO, +1).
+    // Out-of-image pairs read a clamped in-range dword and are stored as zero.
+    const int pr = tid >> 5, cp = tid & 31;
+    const int ih = ih0 + pr, iw = 2 * cp - CO;
+    const bool pok = ih >= 0 && ih < H && iw >= 0 && iw + 1 < Wd;
+    const int HW2 = H * Wd / 2;                                     // dwords per channel plane
+    const int pbase = pok ? img * C * HW2 + (ih * Wd + iw) / 2 : 0;
+    // Weight loads (threads 0 .. 2*BM-1): output channel m0 + woc, channels
+    // 8*wh .. 8*wh+7 of the stage, all nine taps: nine 16-byte chunks.
+    const int woc = tid >> 1, wh = tid & 1;
+    const bool wthr = tid < 2 * BM;
+    const bool wok = wthr && m0 + woc < OC;
+    const int wbase = wok ? ((m0 + woc) * C + 8 * wh) / 8 * NTAP : 0;
+
+    unsigned xs[CC];
+    u32x4_t ws[NTAP];
+    auto gload = [&](int kt) __attribute__((always_inline)) {
+        const int c0 = kt * CC;
+#pragma unroll
+        for (int c = 0; c < CC; ++c) xs[c] = X[pbase + (c0 + c) * HW2];
+        if (wthr) {
+#pragma unroll
+            for (int q = 0; q < NTAP; ++q) ws[q] = Wv[wbase + c0 / 8 * NTAP + q];
+        }
+    };
+    // halfword e (0 .. 71) of the weight slab
+    auto wv = [&](int e) __attribute__((always_inline)) {
+        return (ws[e >> 3][(e >> 1) & 3] >> (16 * (e & 1))) & 0xffffu;
+    };
+    auto lstore = [&](int buf) __attribute__((always_inline)) {
+        unsigned char *P = smem + buf * STAGE_BYTES;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            u32x4_t lo, hi;   // columns 2cp and 2cp + 1
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const unsigned a = pok ? xs[8 * h + 2 * j] : 0u, b = pok ? xs[8 * h + 2 * j + 1] : 0u;
+                lo[j] = (a & 0xffffu) | (b << 16);
+                hi[j] = (a >> 16) | (b & 0xffff0000u);
+            }
+            *reinterpret_cast<u32x4_t *>(P + h * HALF + (pr * PC + 2 * cp) * CELL) = lo;
+            *reinterpret_cast<u32x4_t *>(P + h * HALF + (pr * PC + 2 * cp + 1) * CELL) = hi;
+        }
+        if (wthr) {
+            unsigned char *Wl = P + P_BYTES;
+#pragma unroll
+            for (int t = 0; t < NTAP; ++t) {
+                u32x4_t v;
+#pragma unroll
+                for (int d = 0; d < 4; ++d)
+                    v[d] = wok ? (wv(2 * d * NTAP + t) | (wv((2 * d + 1) * NTAP + t) << 16)) : 0u;
+                *reinterpret_cast<u32x4_t *>(Wl + ((t * BM + woc) * CC + 8 * wh) * 2) = v;
+            }
+        }
+    };
+
+    // Fragment bases.  A: output channel i*32 + lrow, channels 8*lgrp .. +7.
+    // B: this lane's pixel of column block j (patch cell 0 past the image).
+    const int a_base = P_BYTES + (lrow * CC + 8 * lgrp) * 2;
+    int b_base[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int pix = p0 + wave * WN + j * MI + lrow;
+        int cell = 0;
+        if (pix < OHW) {
+            const int oh = pix / OW, ow = pix - oh * OW;
+            cell = (oh - oh0) * PC + ow - p.pw + CO;
+        }
+        b_base[j] = lgrp * HALF + cell * CELL;
+    }
+
+    typename MF::acc_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[i][j][r] = 0.f;
+
+    u16x8 af[2][TM], bfr[2][TN];
+    auto load_frags = [&](int buf, int t, int fb) __attribute__((always_inline)) {
+        const unsigned char *P = smem + buf * STAGE_BYTES;
+        const int kh = t / 3, kw = t - 3 * kh;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+            af[fb][i] = *reinterpret_cast<const u16x8 *>(P + a_base + ((t * BM + i * MI) * CC) * 2);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            bfr[fb][j] = *reinterpret_cast<const u16x8 *>(P + b_base[j] + (kh * PC + kw) * CELL);
+    };
+    auto mfmas = [&](int fb) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = MF::mma(af[fb][i], bfr[fb][j], acc[i][j]);
+    };
+
+    // Register-staged double buffer, branch-free: the loads of stage kt + 1
+    // (stage kt again on the last iteration) are issued before the nine taps
+    // of stage kt and stored into the other buffer after them.
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < KT; ++kt) {
+        const int cur = kt & 1;
+        gload(kt + 1 < KT ? kt + 1 : kt);
+        load_frags(cur, 0, 0);
+#pragma unroll
+        for (int t = 0; t < NTAP; ++t) {
+            if (t + 1 < NTAP) load_frags(cur, t + 1, (t + 1) & 1);
+            mfmas(t & 1);
+        }
+        lstore(cur ^ 1);
+        __syncthreads();
+    }
+
+    float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int pix = p0 + wave * WN + j * MI + lrow;
+        if (pix >= OHW) continue;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int oc = m0 + i * MI + MF::row(lane, r);
+                if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
+            }
+    }
+}
+
+// Shapes the halo kernel covers; anything else runs the gather kernel with
+// 64x128 tiles.
+inline bool bf16_halo_eligible(const ConvArgs &a) {
+    using namespace halo_bf16;
+    if (a.R != 3 || a.S != 3 || a.sh != 1 || a.sw != 1) return false;
+    if (a.C % CC != 0 || a.W % 2 != 0 || a.pw > CO) return false;
+    if (a.OW - a.pw + 3 > PC - 1) return false;            // last patch column used
+    if ((reinterpret_cast<uintptr_t>(a.X) & 3) != 0 || (reinterpret_cast<uintptr_t>(a.Wt) & 15) != 0)
+        return false;
+    const int span = (BN - 1 + a.OW - 1) / a.OW + 1;      // output rows a tile can touch
+    return span + 2 <= PR;
+}
+
+hipError_t launch_conv_bf16_halo(const ConvArgs &a, hipStream_t s) {
+    if (!bf16_halo_eligible(a)) return launch_conv_bf16<64, 128, 32, 32, 64, 32, 8>(a, s);
+    const int OHW = a.OH * a.OW;
+    const unsigned tiles = (unsigned)(((a.OC + halo_bf16::BM - 1) / halo_bf16::BM) * a.Nb *
+                                      ((OHW + halo_bf16::BN - 1) / halo_bf16::BN));
+    ConvArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_bf16_halo_kernel), dim3(tiles),
+                           dim3(halo_bf16::NT), kargs, 0, s);
+}
+
 #define XTC_CONV_BF16_INSTANCE(BM, BN, BK, WM, WN, MI, PAD)                                   \
     ConvInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), 2, PAD, 0),               \
@@ -216,6 +439,9 @@ hipError_t launch_conv_bf16(const ConvArgs &a, hipStream_t s) {
     }
 
 const ConvInstance kConvBf16Instances[] = {
+    ConvInstance{make_sched(64, 256, 16, 64, 64, 32, 32, 16, 2, -1, 0, 2),  // halo, 3x3 stride 1
+                 &launch_conv_bf16_halo,
+                 &occupancy_of<&conv2d_bf16_halo_kernel, halo_bf16::NT, 0>},
     XTC_CONV_BF16_INSTANCE(64, 128, 32, 32, 64, 32, 8),   // default for OC <= 64
     XTC_CONV_BF16_INSTANCE(128, 128, 32, 64, 64, 32, 8),  // default for OC > 64
     XTC_CONV_BF16_INSTANCE(64, 64, 32, 32, 32, 32, 8),    // few output pixels

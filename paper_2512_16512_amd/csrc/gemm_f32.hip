@@ -634,6 +634,8 @@ const GemmInstance kF32Instances[] = {
     XTC_F32_DMA_INSTANCE(128, 128, 32, 64, 64, 2),
     XTC_F32_DMA_INSTANCE(128, 128, 16, 64, 64, 4),
     XTC_F32_DMA_MI_INSTANCE(128, 128, 32, 64, 64, 16, 2),   // 16x16x4 instruction tile
+    XTC_F32_DMA_INSTANCE(256, 128, 32, 64, 64, 2),   // 8 waves of 64x64
+    XTC_F32_DMA_INSTANCE(128, 256, 32, 64, 64, 2),
     XTC_F32_DMA_INSTANCE(64, 128, 32, 32, 64, 3),    // mid-size problems
     XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 4),
     XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 2),

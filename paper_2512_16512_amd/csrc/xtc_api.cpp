@@ -143,9 +143,11 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     const int64_t cus = 256;
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     if (op == XTC_OP_CONV2D && dt == XTC_BF16) {
-        // register-staged implicit GEMM: 64x128 tiles, 128x128 for more than
-        // 64 output channels, 64x64 when 64x128 tiles leave CUs idle
-        *out = make_sched(64, 128, 32, 32, 64, 32, 32, 16, 2, 8, 0);
+        // the halo-tiled kernel (64x256 tiles; it runs the 64x128 gather
+        // kernel for shapes outside its class: not 3x3 stride 1, odd widths,
+        // rows far from 56 pixels); the gather kernel with 128x128 tiles for
+        // more than 64 output channels, 64x64 when 64x128 tiles leave CUs idle
+        *out = make_sched(64, 256, 16, 64, 64, 32, 32, 16, 2, -1, 0, 2);
         if (M > 64)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 16, 2, 8, 0);
         else if (tiles(64, 128) < cus)

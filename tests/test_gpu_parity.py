@@ -74,6 +74,10 @@ def test_matmul_config_parity(x, ci):
     (2, 12, 11, 7, 16, 1, 1, 1, 0),     # 1x1
     (1, 3, 30, 30, 16, 7, 7, 2, 3),     # the 7x7 stride-2 shape, scaled down
     (1, 64, 12, 12, 130, 3, 3, 1, 1),   # OC > 128: several weight tiles
+    (1, 16, 56, 56, 64, 3, 3, 1, 1),    # halo-tiled kernel: 56-wide rows, last tile ragged
+    (2, 32, 54, 52, 70, 3, 3, 1, 1),    # halo: OC = 70 (ragged second weight tile), two stages
+    (1, 16, 57, 56, 20, 3, 3, 1, 0),    # halo: no padding (55 x 54 output)
+    (1, 48, 56, 58, 16, 3, 3, 1, 2),    # halo: pad 2 (60-wide output rows), three stages
 ])
 def test_conv_bf16_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape
