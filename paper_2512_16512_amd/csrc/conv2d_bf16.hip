@@ -401,7 +401,9 @@ conv2d_bf16_halo_kernel(ConvArgs p) {
 #pragma unroll
             for (int r = 0; r < MF::NACC; ++r) {
                 const int oc = m0 + i * MI + MF::row(lane, r);
-                if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r];
+                if (oc < OC)
+                    __builtin_nontemporal_store((p.relu && acc[i][j][r] < 0.f) ? 0.f : acc[i][j][r],
+                                                &Y[oc * OHW + pix]);
             }
     }
 }
