@@ -1154,6 +1154,12 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
         for (int t = 0; t + 1 < NSTEP; ++t) {
             load_frags(st, t + 1, (t + 1) & 1);
             mfmas(t & 1);
+            // one MFMA, then one LDS read of the next k-step
+#pragma unroll
+            for (int m = 0; m < NB; ++m) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
         }
         // the next stage has landed; the barrier also frees slot st, whose
         // fragments are all in registers
