@@ -396,6 +396,12 @@ gemm_f32_dma_kernel(GemmArgs p) {
         for (int s = 0; s + 1 < G::NS; ++s) {
             load_frags(st, s + 1, (s + 1) & 1);
             mfmas(s & 1);
+            // one MFMA, then one LDS read of the next fragment set
+#pragma unroll
+            for (int m = 0; m < 4 * G::TM * G::TN; ++m) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                if (m < G::TM + 4 * G::TN) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
         }
         wait_vmcnt<(STAGES - 2) * G::LOADS>();
         __builtin_amdgcn_s_barrier();
