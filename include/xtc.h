@@ -65,7 +65,10 @@ typedef enum {
  *  size          sizeof(xtc_sched) as known to the caller (ABI versioning).
  *  block_m/n/k   workgroup tile: the outer strip-mine of M and N (one
  *                workgroup per tile, parallelized over the CUs) and the
- *                K-step staged in LDS per pipeline stage.
+ *                K-step staged in LDS per pipeline stage (channels per
+ *                stage for the k_order = 2 conv kernels).  Powers of two,
+ *                except block_n and wave_n of the k_order = 2 conv kernels
+ *                (multiples of 16).
  *  wave_m/n      tile of one 64-lane wavefront inside the workgroup tile
  *                (second strip-mine level); the workgroup has
  *                (block_m/wave_m)*(block_n/wave_n) waves.
@@ -86,11 +89,20 @@ typedef enum {
  *                (ic, kh, kw).  0: channel-major, k = (ic*R + kh)*S + kw (the
  *                OIHW weight layout); 1: tap-major, k = (kh*S + kw)*C + ic
  *                (needs C % 32 == 0, else the channel-major kernel with the
- *                same tiles runs); 2: chunks of 8 channels, and inside a
- *                chunk the R*S taps, k = ((ic/8)*R*S + kh*S + kw)*8 + ic%8,
- *                with each chunk's input patch staged once for all taps
- *                (3x3, stride 1, C % 16 == 0, W + pad_w <= 60 and OW >= 51;
- *                other shapes run the tap-major kernel with the same tiles).
+ *                same tiles runs); 2: chunks of channels, and inside a
+ *                chunk the R*S taps, with each chunk's input patch staged
+ *                once for all taps, for 3x3 stride-1 layers with rows of
+ *                about 56 pixels (OW >= 51):
+ *                  fp32: chunks of 8, k = ((ic/8)*R*S + kh*S + kw)*8 + ic%8;
+ *                  block_n = 256 needs C % 16 == 0 and W + pad_w <= 60;
+ *                  block_n = 208 (16x16x4 instructions) needs C % 8 == 0
+ *                  and covers at most 208 pixels per workgroup, the count
+ *                  chosen per launch so that workgroups split evenly;
+ *                  other shapes run the tap-major kernel;
+ *                  bf16: chunks of 16, k = ((ic/16)*R*S + kh*S + kw)*16 +
+ *                  ic%16, needs C % 16 == 0, even W, pad_w <= 2,
+ *                  OW - pad_w <= 60, a 4-byte-aligned X and a 16-byte-
+ *                  aligned W; other shapes run the channel-major kernel.
  *                Results differ only by rounding order.
  *  k_split       waves that share one workgroup tile, each reducing every
  *                k_split-th group of block_k reduction steps (a parallel
