@@ -3,6 +3,8 @@
 - Random shapes (ragged in every dimension, leading dimensions with padding)
   paired with random compiled instances, raster orders and the relu flag;
   small-integer inputs make every correct result bit-exact.
+- Random 3x3 stride-1 layers in and around the class of the patch-staging
+  conv kernels, through every such instance and the default schedule.
 - Several host threads, each on its own stream, launching different
   contractions at once: the library keeps no state shared between calls, so
   every result must equal its single-threaded one.
@@ -71,6 +73,42 @@ def test_random_shapes_instances_and_leading_dims(x, dtype):
         got = to_host(Cd)
         assert np.array_equal(got[:, :N], ref), (case, M, N, K, s)
         assert np.all(got[:, N:] == 7.0), "columns past N were written"
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_random_patch_staging_class_convs(x, dtype):
+    """Seeded random 3x3 stride-1 layers with rows of about 56 pixels -- the
+    class of the kernels that stage an input patch once for all taps
+    (k_order 2) -- through every such instance and the default schedule,
+    with random raster orders and the fused relu.  Widths, heights, padding,
+    channel and output-channel counts vary, so some shapes fall outside a
+    kernel's class and exercise its fallback.  Small-integer inputs: every
+    result is bit-exact."""
+    rng = np.random.default_rng(5656 + (dtype == "bf16"))
+    code = x.XTC_F32 if dtype == "f32" else x.XTC_BF16
+    scheds = [s for s in x.xtc_sched_list(x.XTC_OP_CONV2D, code) if s.k_order == 2] + [None]
+    for case in range(6):
+        N = int(rng.integers(1, 3))
+        C = int(rng.choice([8, 16, 24, 32, 48]))
+        H, W = (int(v) for v in rng.integers(50, 61, size=2))
+        OC = int(rng.integers(1, 131))
+        pad = int(rng.integers(0, 3))
+        relu = bool(rng.integers(2))
+        X = xi.small_int_f32(700 + case, (N, C, H, W))
+        Wt = xi.small_int_f32(800 + case, (OC, C, 3, 3))
+        if dtype == "bf16":
+            X, Wt = xi.f32_to_bf16_bits(X), xi.f32_to_bf16_bits(Wt)
+        ref = oracle.conv2d(X, Wt, stride=1, pad=pad)
+        if relu:
+            ref = oracle.relu(ref)
+        Xd, Wd = to_dev(X), to_dev(Wt)
+        for s in scheds:
+            if s is not None:
+                s.raster = int(rng.choice([0, 1, 8]))
+                s.xcd_remap = int(rng.integers(2))
+            say("random conv", dtype, case, (N, C, H, W, OC, pad), relu, s)
+            got = to_host(x.conv2d_nchw(Xd, Wd, stride=1, pad=pad, sched=s, relu=relu))
+            assert np.array_equal(got, ref), (dtype, case, (N, C, H, W, OC, pad), relu, s)
 
 
 def test_concurrent_host_threads_on_separate_streams(x):
