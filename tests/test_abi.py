@@ -144,6 +144,28 @@ def test_sched_legal_but_not_compiled(x):
     assert x.xtc_matmul(4, 4, 4, BAD, 4, BAD, 4, BAD, 4, 0, s) == 6
 
 
+def test_sched_non_power_of_two_pixel_tiles(x):
+    # A pixel tile that is not a power of two (208 = 13 instruction blocks of
+    # 16) is legal only for the conv kernels that stage an input patch
+    # (k_order 2), whose block_k counts channels per stage; the compiled
+    # balanced halo instance is one such schedule.
+    conv = [s for s in x.xtc_sched_list(x.XTC_OP_CONV2D, x.XTC_F32) if s.block_n == 208]
+    assert len(conv) == 1 and conv[0].k_order == 2 and conv[0].block_k == 8
+    assert x.xtc_sched_check(x.XTC_OP_CONV2D, x.XTC_F32, conv[0]) == 0
+    s = x.Sched(**conv[0].as_dict())
+    s.k_order = 1                       # other reduction orders: powers of two only
+    assert x.xtc_sched_check(x.XTC_OP_CONV2D, x.XTC_F32, s) == 5
+    s = x.Sched(**conv[0].as_dict())
+    s.block_n = s.wave_n = 200          # not a whole number of 16-pixel blocks
+    assert x.xtc_sched_check(x.XTC_OP_CONV2D, x.XTC_F32, s) == 5
+    s = x.Sched(**conv[0].as_dict())
+    s.block_n = s.wave_n = 224          # legal, but not compiled
+    assert x.xtc_sched_check(x.XTC_OP_CONV2D, x.XTC_F32, s) == 6
+    m = _base(x)
+    m.block_n, m.wave_n = 208, 208      # never for matmul
+    assert x.xtc_sched_check(x.XTC_OP_MATMUL, x.XTC_F32, m) == 5
+
+
 def test_sched_lds_budget(x):
     s = _base(x, 1)
     s.block_m = s.block_n = 512
