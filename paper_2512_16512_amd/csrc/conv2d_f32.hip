@@ -17,6 +17,7 @@
 // division in the main loop: an element (k, q) is X[base(q) + off(k)] when
 // 0 <= ih0(q) + kh < H and 0 <= iw0(q) + kw < W, else zero.
 #include <type_traits>
+#include <utility>
 
 #include "lds_dma.h"
 #include "mfma_f32.h"
@@ -997,6 +998,13 @@ conv2d_f32_halo_kernel(ConvArgs p) {
 // lane groups read four channel planes; planes are 8*64 + 16 floats apart,
 // 16 banks, which keeps the groups on disjoint banks unless a 16-pixel
 // block wraps to the next image row.
+// Calls f(std::integral_constant<int, I>()) for I = 0, 1, ...: a loop whose
+// index is a compile-time constant in the body, however large the body.
+template <typename F, int... I>
+__device__ __forceinline__ void each_index(F &&f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>()), ...);
+}
+
 namespace halo16 {
 constexpr int BM = 64, NWAVES = 4, NT = 256;
 constexpr int NB = 13;                        // 16-pixel column blocks per wave
@@ -1122,52 +1130,59 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
 #pragma unroll
         for (int j = 0; j < NB; ++j) acc[j] = MF::mma(af[buf], bfr[buf][j], acc[j]);
     };
-    // The last k-step's MFMAs with the copies of the stage STAGES ahead
-    // spread between them (copies issued all at once right after the barrier
-    // queue at the texture unit and stall the issuing waves).
-    auto mfmas_with_copies = [&](int buf, int st) __attribute__((always_inline)) {
+    // K-step t of the stage in slot st, one MFMA at a time, each followed by
+    // one fragment read of k-step t + 1 and its share of the copies of the
+    // next stage into slot nx.  A stage's copies are spread over its first
+    // CSTEPS k-steps: issued together, the copies of all waves would queue at
+    // the texture unit and stall the issuing waves.  The fences keep the
+    // order (and keep the compiler from hoisting the reads).
+    static_assert(STAGES == 2, "the next stage is copied into the other slot of a two-slot ring");
+    constexpr int CSTEPS = 12;
+    auto step = [&](int st, auto tc, int nx) __attribute__((always_inline)) {
+        constexpr int t = decltype(tc)::value;   // a constant: the copy split is fixed per k-step
+        const int cur = t & 1, nxt = (t + 1) & 1;
+        const unsigned char *As = smem + st * STAGE_BYTES;
+        const unsigned char *Bs = As + A_BYTES;
+        const int tap = (t + 1) >> 1, s = (t + 1) & 1;
+        const int kh = tap / 3, kw = tap - 3 * kh;
+        constexpr int q0 = t < CSTEPS ? t * LOADS / CSTEPS : LOADS;
+        constexpr int q1 = t < CSTEPS ? (t + 1) * LOADS / CSTEPS : LOADS;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-            acc[j] = MF::mma(af[buf], bfr[buf][j], acc[j]);
-            const int q0 = j * LOADS / NB, q1 = (j + 1) * LOADS / NB;
-            __builtin_amdgcn_sched_barrier(0);
+        for (int m = 0; m < NB; ++m) {
+            acc[m] = MF::mma(af[cur], bfr[cur][m], acc[m]);
+            if (m == 0)
+                af[nxt] = *reinterpret_cast<const float *>(As + a_base + (tap * BM * CC + 4 * s) * 4);
+            bfr[nxt][m] =
+                *reinterpret_cast<const float *>(Bs + b_base[m] + (4 * s * PLANE + kh * 64 + kw) * 4);
 #pragma unroll
-            for (int q = q0; q < q1; ++q) copy(st, q);
+            for (int q = q0 + m * (q1 - q0) / NB; q < q0 + (m + 1) * (q1 - q0) / NB; ++q) copy(nx, q);
             __builtin_amdgcn_sched_barrier(0);
         }
-        advance();
     };
 
+    // Stage 0 into slot 0; then every iteration computes stage kt from slot
+    // kt % 2 while copying stage kt + 1 into the other slot (stages past the
+    // end read in range or zero and are never used).
 #pragma unroll
-    for (int s = 0; s < STAGES; ++s) {
-#pragma unroll
-        for (int q = 0; q < LOADS; ++q) copy(s, q);
-        advance();
-    }
-    wait_vmcnt<(STAGES - 1) * LOADS>();
+    for (int q = 0; q < LOADS; ++q) copy(0, q);
+    advance();
+    wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     load_frags(0, 0, 0);
     for (int kt = 0; kt < KT; ++kt) {
-        const int st = kt % STAGES;
-#pragma unroll
-        for (int t = 0; t + 1 < NSTEP; ++t) {
-            load_frags(st, t + 1, (t + 1) & 1);
-            mfmas(t & 1);
-            // one MFMA, then one LDS read of the next k-step
-#pragma unroll
-            for (int m = 0; m < NB; ++m) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            }
-        }
-        // the next stage has landed; the barrier also frees slot st, whose
-        // fragments are all in registers
-        wait_vmcnt<(STAGES - 2) * LOADS>();
+        const int st = kt & 1, nx = st ^ 1;
+        each_index([&](auto tc) __attribute__((always_inline)) { step(st, tc, nx); },
+                   std::make_integer_sequence<int, NSTEP - 1>());
+        advance();
+        // this wave's copies of stage kt + 1 have landed, then everyone's; every
+        // wave has also issued its last read of slot st (k-step NSTEP - 1's
+        // fragments, now in registers)
+        wait_vmcnt<0>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        load_frags((kt + 1) % STAGES, 0, 0);
-        mfmas_with_copies((NSTEP - 1) & 1, st);
+        load_frags(nx, 0, 0);
+        mfmas((NSTEP - 1) & 1);
     }
     wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
 
