@@ -42,7 +42,7 @@ HBM_GBS = 8000.0
 KERNEL_SOURCES = {
     "f32": ["gemm_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h"],
     "bf16": ["gemm_bf16.hip", "mfma_bf16.h", "tile_map.h", "lds_dma.h"],
-    "conv": ["conv2d_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h"],
+    "conv": ["conv2d_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h", "unroll.h"],
 }
 
 

@@ -17,11 +17,11 @@
 // division in the main loop: an element (k, q) is X[base(q) + off(k)] when
 // 0 <= ih0(q) + kh < H and 0 <= iw0(q) + kw < W, else zero.
 #include <type_traits>
-#include <utility>
 
 #include "lds_dma.h"
 #include "mfma_f32.h"
 #include "tile_map.h"
+#include "unroll.h"
 #include "xtc_internal.h"
 
 namespace xtc {
@@ -998,13 +998,6 @@ conv2d_f32_halo_kernel(ConvArgs p) {
 // lane groups read four channel planes; planes are 8*64 + 16 floats apart,
 // 16 banks, which keeps the groups on disjoint banks unless a 16-pixel
 // block wraps to the next image row.
-// Calls f(std::integral_constant<int, I>()) for I = 0, 1, ...: a loop whose
-// index is a compile-time constant in the body, however large the body.
-template <typename F, int... I>
-__device__ __forceinline__ void each_index(F &&f, std::integer_sequence<int, I...>) {
-    (f(std::integral_constant<int, I>()), ...);
-}
-
 namespace halo16 {
 constexpr int BM = 64, NWAVES = 4, NT = 256;
 constexpr int NB = 13;                        // 16-pixel column blocks per wave
