@@ -258,27 +258,38 @@ def run_paper(cfg, steps, warmup, per_graph=50):
                 replay_ok=replay_ok, keep=keep)
 
 
+def roofline_of(flops, alg_bytes, ms, peak_tflops, traffic):
+    """Roofline entry of one launch: bound by the matrix cores when the
+    workload's arithmetic intensity (FLOPs per algorithmic HBM byte) is
+    above the ridge point peak / HBM bandwidth, else by HBM (then
+    ``achieved`` is algorithmic bytes over time against 8 TB/s)."""
+    tflops = flops / (ms * 1e-3) / 1e12
+    gbps = alg_bytes / (ms * 1e-3) / 1e9
+    intensity = flops / alg_bytes
+    ridge = peak_tflops * 1e12 / (HBM_GBS * 1e9)
+    common = {"traffic": traffic, "alg_bytes": alg_bytes, "intensity": round(intensity, 1),
+              "ridge": round(ridge, 1)}
+    if intensity >= ridge:
+        return dict({"bound": "mfma", "achieved": round(tflops, 2), "peak": peak_tflops,
+                     "unit": "TFLOP/s", "frac": round(tflops / peak_tflops, 4)}, **common,
+                    alg_hbm_GBps=round(gbps, 1))
+    return dict({"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_GBS, "unit": "GB/s",
+                 "frac": round(gbps / HBM_GBS, 4)}, **common, tflops=round(tflops, 2))
+
+
 def summary(kind, cfg, r, workload):
     tflops = r["flops"] / (r["ms"] * 1e-3) / 1e12
     traffic = measured_traffic(kind, workload, r["sched"]) if kind in KERNEL_SOURCES else None
+    peak = PEAK["bf16" if kind in ("bf16", "conv_bf16") else "f32"]
     return {
         "workload": workload,
         "value": round(tflops, 2),
         "unit": "TFLOP/s",
         "ms_per_launch": round(r["ms"], 4),
         "launch_stats": r["stats"],
-        "frac_of_peak": round(tflops / PEAK["bf16" if kind in ("bf16", "conv_bf16") else "f32"], 4),
+        "frac_of_peak": round(tflops / peak, 4),
         "schedule": r["sched"],
-        "roofline": {
-            "bound": "mfma",
-            "achieved": round(tflops, 2),
-            "peak": PEAK["bf16" if kind in ("bf16", "conv_bf16") else "f32"],
-            "unit": "TFLOP/s",
-            "frac": round(tflops / PEAK["bf16" if kind in ("bf16", "conv_bf16") else "f32"], 4),
-            "traffic": traffic,
-            "alg_bytes": r["alg_bytes"],
-            "alg_hbm_GBps": round(r["alg_bytes"] / (r["ms"] * 1e-3) / 1e9, 1),
-        },
+        "roofline": roofline_of(r["flops"], r["alg_bytes"], r["ms"], peak, traffic),
     }
 
 

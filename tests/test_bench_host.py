@@ -41,3 +41,20 @@ def test_kernel_hash_covers_every_source_of_the_kernel():
         for f in files:
             assert os.path.exists(os.path.join(ROOT, "paper_2512_16512_amd", "csrc", f))
         assert bench.kernel_hash(kind) == bench.kernel_hash(kind)
+
+
+def test_roofline_bound_follows_the_ridge_point():
+    """A workload whose FLOPs per algorithmic HBM byte fall below peak / 8 TB/s
+    is reported against HBM bandwidth, otherwise against the matrix cores."""
+    # fp32 4096^3: 682.7 FLOP/B, far above the fp32 ridge (19.7)
+    fl, by = 2.0 * 4096 ** 3, 3 * 4096 * 4096 * 4
+    r = bench.roofline_of(fl, by, 1.0, bench.PEAK["f32"], None)
+    assert r["bound"] == "mfma" and r["unit"] == "TFLOP/s"
+    assert abs(r["achieved"] - fl / 1e-3 / 1e12) < 0.01 and abs(r["frac"] - r["achieved"] / 157.3) < 1e-4
+    # bf16-input conv 32x64x56x56 -> 64, 3x3: bf16 X and W, fp32 Y, 191.6 FLOP/B < 314.6
+    fl = 2.0 * 32 * 64 * 56 * 56 * 64 * 9
+    by = 32 * 64 * 56 * 56 * 2 + 64 * 64 * 9 * 2 + 32 * 64 * 56 * 56 * 4
+    r = bench.roofline_of(fl, by, 0.02, bench.PEAK["bf16"], None)
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert abs(r["achieved"] - by / 0.02e-3 / 1e9) < 0.1
+    assert abs(r["ridge"] - 314.6) < 0.1 and r["intensity"] < r["ridge"]
