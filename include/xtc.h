@@ -55,7 +55,9 @@ typedef enum {
     XTC_ERR_BAD_SCHEDULE = 5,         /* illegal field values / combination   */
     XTC_ERR_UNSUPPORTED_SCHEDULE = 6, /* legal but not among compiled ones    */
     XTC_ERR_TOO_LARGE = 7,            /* an operand span is >= 2^31 bytes     */
-    XTC_ERR_HIP = 8                   /* a HIP call failed (see below)        */
+    XTC_ERR_HIP = 8,                  /* a HIP call failed (see below)        */
+    XTC_ERR_MISALIGNED = 9            /* a tensor pointer is not aligned to   */
+                                      /* its element size                     */
 } xtc_status;
 
 /*
@@ -146,12 +148,15 @@ typedef struct {
  *            Only C[i*ldc + j] for i < M, j < N is written; columns
  *            N <= j < ldc are never touched.
  *  dtype     XTC_F32 or XTC_BF16 (applies to A and B; C is always fp32).
+ *            A, B and C are aligned to their element size (4 bytes fp32,
+ *            2 bytes bf16); any row stride is accepted.
  *  sched     NULL selects xtc_default_schedule(); otherwise must pass
  *            xtc_sched_check().
  *  stream    hipStream_t or NULL.
  * Errors: XTC_ERR_NULL_POINTER (A, B or C NULL while M, N > 0),
  * XTC_ERR_BAD_SHAPE (negative extent), XTC_ERR_BAD_LEADING_DIM,
- * XTC_ERR_BAD_DTYPE, XTC_ERR_BAD_SCHEDULE, XTC_ERR_UNSUPPORTED_SCHEDULE,
+ * XTC_ERR_BAD_DTYPE, XTC_ERR_MISALIGNED (a pointer not aligned to its
+ * element size), XTC_ERR_BAD_SCHEDULE, XTC_ERR_UNSUPPORTED_SCHEDULE,
  * XTC_ERR_TOO_LARGE, XTC_ERR_HIP (launch failed).
  */
 xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K,
@@ -175,6 +180,7 @@ xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K,
  *       (XTC_F32) or both bf16 bit patterns (XTC_BF16, products exact in
  *       fp32, fp32 accumulation).
  *  Y    device, N x OC x OH x OW contiguous fp32 (overwritten).
+ *  X, Wt and Y are aligned to their element size (else XTC_ERR_MISALIGNED).
  *  N, C, H, W, OC, R, S >= 1 except that N == 0 or OC == 0 is a no-op;
  *  stride >= 1, pad >= 0, OH >= 1 and OW >= 1, else XTC_ERR_BAD_SHAPE.
  *  dtype XTC_F32 or XTC_BF16 (else XTC_ERR_BAD_DTYPE); the bf16 kernels

@@ -34,6 +34,7 @@ XTC_ERR_BAD_SCHEDULE = 5
 XTC_ERR_UNSUPPORTED_SCHEDULE = 6
 XTC_ERR_TOO_LARGE = 7
 XTC_ERR_HIP = 8
+XTC_ERR_MISALIGNED = 9
 
 
 class Sched(ctypes.Structure):

@@ -433,7 +433,7 @@ conv2d_f32_dma_kernel(ConvArgs p) {
             load_frags(st, s + 1, (s + 1) & 1);
             mfmas(s & 1);
         }
-        wait_vmcnt<(STAGES - 2) * G::LOADS>();
+        wait_vmcnt_and_lds<(STAGES - 2) * G::LOADS>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         fire(st);
@@ -700,7 +700,7 @@ conv2d_f32_tap_kernel(ConvArgs p) {
             load_frags(st, s + 1, (s + 1) & 1);
             mfmas(s & 1);
         }
-        wait_vmcnt<(STAGES - 2) * G::LOADS>();
+        wait_vmcnt_and_lds<(STAGES - 2) * G::LOADS>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         fire(st);
@@ -950,7 +950,7 @@ conv2d_f32_halo_kernel(ConvArgs p) {
             load_frags(st, t + 1, (P + t + 1) & 1);
             mfmas((P + t) & 1);
         }
-        wait_vmcnt<(STAGES - 2) * LOADS>();
+        wait_vmcnt_and_lds<(STAGES - 2) * LOADS>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         load_frags((kt + 1) % STAGES, 0, (P + NTAP) & 1);
@@ -1171,7 +1171,7 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
         // this wave's copies of stage kt + 1 have landed, then everyone's; every
         // wave has also issued its last read of slot st (k-step NSTEP - 1's
         // fragments, now in registers)
-        wait_vmcnt<0>();
+        wait_vmcnt_and_lds<0>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         load_frags(nx, 0, 0);

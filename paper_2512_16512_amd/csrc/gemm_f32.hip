@@ -403,7 +403,7 @@ gemm_f32_dma_kernel(GemmArgs p) {
                 if (m < G::TM + 4 * G::TN) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
         }
-        wait_vmcnt<(STAGES - 2) * G::LOADS>();
+        wait_vmcnt_and_lds<(STAGES - 2) * G::LOADS>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         load_frags((kt + 1) % STAGES, 0, 0);

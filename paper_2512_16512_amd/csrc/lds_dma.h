@@ -55,6 +55,16 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// wait_vmcnt<N> that also waits for every LDS read of this wave (lgkmcnt 0).
+// Used in front of a barrier that frees a ring slot: the reads of the slot
+// have then completed, not only been issued, before any wave's copies into
+// the slot start.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_and_lds() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
 constexpr int kOOB = 0x7FFFFFF0;  // buffer offset beyond any operand (spans are < 2^31 - 1)
 
 // 4-byte-per-lane variant of dma16 (lane i's dword lands at lds_addr + 4*i).

@@ -83,4 +83,47 @@ __device__ __forceinline__ unsigned short load_pred_u16<1>(const unsigned short 
     return valid > 0 ? *p : (unsigned short)0;
 }
 
+// Eight consecutive bf16 values starting at element e of a buffer whose base
+// address is 16-byte aligned, for any position e: the two aligned 16-byte
+// chunks that cover them are loaded (a chunk past the buffer's end reads
+// zero) and funnel-shifted into place.  Values from position `valid` on are
+// zero.  This lets rows that start at any 2-byte boundary be read with
+// 16-byte loads.
+__device__ __forceinline__ u16x8 load_shifted_u16x8(__amdgpu_buffer_rsrc_t rs, int e, int valid) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const int o = 2 * e;
+    const int ob = o & ~15;
+    const u32x4 v0 = __builtin_amdgcn_raw_buffer_load_b128(rs, ob, 0, 0);
+    const u32x4 v1 = __builtin_amdgcn_raw_buffer_load_b128(rs, ob + 16, 0, 0);
+    const unsigned w[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+    const int d = (o >> 2) & 3;  // whole dwords to skip
+    const bool half = (o & 2) != 0;
+    u32x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const unsigned lo = d == 0 ? w[i] : d == 1 ? w[i + 1] : d == 2 ? w[i + 2] : w[i + 3];
+        const unsigned hi = d == 0 ? w[i + 1] : d == 1 ? w[i + 2] : d == 2 ? w[i + 3] : w[i + 4];
+        r[i] = half ? __builtin_amdgcn_alignbyte(hi, lo, 2) : lo;   // (hi:lo) >> 16
+    }
+    u16x8 v = __builtin_bit_cast(u16x8, r);
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+        if (k >= valid) v[k] = 0;
+    return v;
+}
+
+// Buffer resource covering `bytes` bytes from p, with its base rounded down
+// and its end rounded up to 16 bytes, so a 16-byte chunk holding any of the
+// bytes is wholly inside it (such a chunk never crosses a page, so it is
+// mapped) and a chunk past the end reads zero; *first receives p's position
+// in elements of `elt` bytes from that base.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t aligned_rsrc(const void *p, long long bytes,
+                                                               int elt, int *first) {
+    const unsigned long long a = reinterpret_cast<unsigned long long>(p);
+    const unsigned mis = (unsigned)(a & 15);
+    *first = (int)(mis / elt);
+    return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void *>(a - mis), 0,
+                                             (int)((bytes + mis + 15) & ~15ll), 0x00020000);
+}
+
 }  // namespace xtc

@@ -108,6 +108,9 @@ xtc_status hip_status(hipError_t e) {
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+bool aligned_to(const void *p, int64_t bytes) {
+    return (reinterpret_cast<uintptr_t>(p) & (uintptr_t)(bytes - 1)) == 0;
+}
 
 }  // namespace
 
@@ -124,6 +127,7 @@ const char *xtc_status_str(xtc_status s) {
         case XTC_ERR_UNSUPPORTED_SCHEDULE: return "schedule not among the compiled instances";
         case XTC_ERR_TOO_LARGE: return "operand too large for 32-bit offsets";
         case XTC_ERR_HIP: return "HIP error";
+        case XTC_ERR_MISALIGNED: return "pointer not aligned to its element size";
     }
     return "unknown status";
 }
@@ -289,6 +293,7 @@ xtc_status matmul_impl(int64_t M, int64_t N, int64_t K, const void *A, int64_t l
     if (M == 0 || N == 0) return XTC_OK;
     if (!C || (K > 0 && (!A || !B))) return XTC_ERR_NULL_POINTER;
     const int64_t elt = dtype == XTC_F32 ? 4 : 2;
+    if (!aligned_to(A, elt) || !aligned_to(B, elt) || !aligned_to(C, 4)) return XTC_ERR_MISALIGNED;
     if (span_bytes(M, K, lda, elt) > kMaxSpan || span_bytes(K, N, ldb, elt) > kMaxSpan ||
         span_bytes(M, N, ldc, 4) > kMaxSpan || lda > kMaxSpan / elt || ldb > kMaxSpan / elt ||
         ldc > kMaxSpan / 4)
@@ -337,6 +342,8 @@ xtc_status conv_impl(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int
     }
     if (N == 0 || OC == 0) return XTC_OK;
     if (!X || !Wt || !Y) return XTC_ERR_NULL_POINTER;
+    const int64_t xelt = dtype == XTC_F32 ? 4 : 2;
+    if (!aligned_to(X, xelt) || !aligned_to(Wt, xelt) || !aligned_to(Y, 4)) return XTC_ERR_MISALIGNED;
     const int64_t elt = dtype == XTC_F32 ? 4 : 2;
     if (N * C * H * W * elt > kMaxSpan || OC * Kg * elt > kMaxSpan ||
         N * OC * OH * OW * 4 > kMaxSpan)

@@ -46,7 +46,7 @@ def test_sched_struct_size_matches_header(x):
 
 
 def test_status_strings(x):
-    for st in range(0, 9):
+    for st in range(0, 10):
         s = x.xtc_status_str(st)
         assert s and s != "unknown status"
     assert x.xtc_status_str(99) == "unknown status"
@@ -68,6 +68,9 @@ BAD = 0x10  # a dummy non-NULL pointer: dereferencing it would fault
     ((4, 4, 4, BAD, 4, BAD, 4, 0, 4, 0), 1),             # C NULL
     ((1 << 16, 1 << 15, 1 << 15, BAD, 1 << 15, BAD, 1 << 15, BAD, 1 << 15, 0), 7),  # span >= 2^31
     ((3, 3, 1 << 30, BAD, 1 << 30, BAD, 3, BAD, 3, 1), 7),
+    ((4, 4, 4, BAD + 2, 4, BAD, 4, BAD, 4, 0), 9),       # fp32 A on a 2-byte boundary
+    ((4, 4, 4, BAD, 4, BAD + 1, 4, BAD, 4, 1), 9),       # bf16 B on an odd byte
+    ((4, 4, 4, BAD, 4, BAD, 4, BAD + 2, 4, 1), 9),       # C (fp32) on a 2-byte boundary
 ])
 def test_matmul_validation(x, args, expected):
     assert x.xtc_matmul(*args) == expected
@@ -93,6 +96,9 @@ def test_matmul_empty_is_noop(x):
     ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, 0, BAD, 0), 1),       # W NULL
     ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, 0, 0), 1),       # Y NULL
     ((1, 1024, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD, 0), 7),  # C*R*S > table capacity
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD + 2, BAD, BAD, 0), 9),  # fp32 X on a 2-byte boundary
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD + 1, BAD, 1), 9),  # bf16 W on an odd byte
+    ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD + 2, 1), 9),  # Y on a 2-byte boundary
 ])
 def test_conv_validation(x, args, expected):
     assert x.xtc_conv2d_nchw(*args) == expected

@@ -111,6 +111,42 @@ def test_random_patch_staging_class_convs(x, dtype):
             assert np.array_equal(got, ref), (dtype, case, (N, C, H, W, OC, pad), relu, s)
 
 
+def test_bf16_rows_at_any_two_byte_boundary(x):
+    """bf16 operands whose base pointers sit 1..7 elements past a 16-byte
+    boundary, with odd row strides: every row starts at a different 2-byte
+    offset, so the register-staged kernels read them with 16-byte loads of
+    the covering aligned chunks shifted into place.  Every compiled instance
+    and the default schedule, on small integers (bit-exact).  The elements
+    around each operand and in the row padding hold the bf16 NaN pattern, so
+    a value taken from outside the operand would poison the result."""
+    import torch
+    rng = np.random.default_rng(97)
+    scheds = x.xtc_sched_list(x.XTC_OP_MATMUL, x.XTC_BF16) + [None]
+    for case, (M, N, K) in enumerate([(131, 77, 203), (300, 257, 9), (65, 129, 1000)]):
+        A = xi.f32_to_bf16_bits(xi.small_int_f32(900 + case, (M, K)))
+        B = xi.f32_to_bf16_bits(xi.small_int_f32(950 + case, (K, N)))
+        ref = oracle.matmul(A, B)
+        lda, ldb = K + int(rng.integers(0, 3)) * 2 + (K % 2 == 0), N + (N % 2 == 0)
+        oa, ob = (int(v) for v in rng.integers(1, 8, size=2))
+
+        def place(arr, ld, off):
+            rows = arr.shape[0]
+            flat = np.full(off + rows * ld + 16, 0x7FC0, dtype=np.uint16)
+            flat[off:off + rows * ld] = _strided(arr, ld).ravel()
+            return to_dev(flat)
+
+        Ad, Bd = place(A, lda, oa), place(B, ldb, ob)
+        pa, pb = Ad.data_ptr() + 2 * oa, Bd.data_ptr() + 2 * ob
+        assert pa % 16 and pb % 16
+        for s in scheds:
+            Cd = torch.full((M, N), 7.0, dtype=torch.float32, device="cuda")
+            say("bf16 offset rows", (M, N, K), (lda, ldb), (oa, ob), s)
+            st = x.xtc_matmul(M, N, K, pa, lda, pb, ldb, Cd.data_ptr(), N, x.XTC_BF16, s,
+                              torch.cuda.current_stream().cuda_stream)
+            assert st == 0, x.xtc_status_str(st)
+            assert np.array_equal(to_host(Cd), ref), ((M, N, K), (lda, ldb), (oa, ob), s)
+
+
 def test_concurrent_host_threads_on_separate_streams(x):
     import torch
     jobs = []
