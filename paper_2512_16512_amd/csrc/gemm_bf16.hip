@@ -36,8 +36,9 @@ struct GemmBf16Cfg {
     static constexpr int AS = BK + PAD;     // LDS row stride of the A tile (elements)
     static constexpr int BS = BN + 32;      // LDS row stride of the B tile (elements)
     static constexpr int W = 8;             // elements per global load
-    static constexpr int A_CPR = BK / W;
+    static constexpr int A_CPR = BK / W;    // 16-byte chunks per tile row
     static constexpr int B_CPR = BN / W;
+    static_assert(64 % A_CPR == 0 && 64 % B_CPR == 0, "a tile row's chunks stay in one wave");
     static constexpr int A_LOADS = BM * BK / (W * NT);
     static constexpr int B_LOADS = BK * BN / (W * NT);
     typedef typename VecU16<W>::t vec_t;
@@ -91,11 +92,14 @@ gemm_bf16_kernel(GemmArgs p) {
             const int r = idx / G::A_CPR, c = (idx % G::A_CPR) * W;
             const int gm = m0 + r, gk = k0 + c;
             const int valid = gm < M ? K - gk : 0;
-            const int e = valid > 0 ? gm * lda + gk : 0;
-            if constexpr (VEC)
-                ra[i] = load_pred_u16<W>(A + e, valid);
-            else
-                ra[i] = load_shifted_u16x8(rsa, a_first + e, valid);
+            if constexpr (VEC) {
+                ra[i] = load_pred_u16<W>(A + (valid > 0 ? gm * lda + gk : 0), valid);
+            } else {
+                // a run is one tile row: its lanes' chunks are consecutive,
+                // also past K (those values are read but zeroed)
+                const int e = gm < M ? gm * lda + gk : 0;
+                ra[i] = load_shifted_u16x8(rsa, a_first + e, valid, idx % G::A_CPR == G::A_CPR - 1);
+            }
         }
 #pragma unroll
         for (int i = 0; i < G::B_LOADS; ++i) {
@@ -103,11 +107,12 @@ gemm_bf16_kernel(GemmArgs p) {
             const int r = idx / G::B_CPR, c = (idx % G::B_CPR) * W;
             const int gk = k0 + r, gn = n0 + c;
             const int valid = gk < K ? N - gn : 0;
-            const int e = valid > 0 ? gk * ldb + gn : 0;
-            if constexpr (VEC)
-                rb[i] = load_pred_u16<W>(B + e, valid);
-            else
-                rb[i] = load_shifted_u16x8(rsb, b_first + e, valid);
+            if constexpr (VEC) {
+                rb[i] = load_pred_u16<W>(B + (valid > 0 ? gk * ldb + gn : 0), valid);
+            } else {
+                const int e = gk < K ? gk * ldb + gn : 0;
+                rb[i] = load_shifted_u16x8(rsb, b_first + e, valid, idx % G::B_CPR == G::B_CPR - 1);
+            }
         }
     };
 

@@ -85,31 +85,49 @@ __device__ __forceinline__ unsigned short load_pred_u16<1>(const unsigned short 
 
 // Eight consecutive bf16 values starting at element e of a buffer whose base
 // address is 16-byte aligned, for any position e: the two aligned 16-byte
-// chunks that cover them are loaded (a chunk past the buffer's end reads
-// zero) and funnel-shifted into place.  Values from position `valid` on are
-// zero.  This lets rows that start at any 2-byte boundary be read with
-// 16-byte loads.
-__device__ __forceinline__ u16x8 load_shifted_u16x8(__amdgpu_buffer_rsrc_t rs, int e, int valid) {
+// chunks that cover them are funnel-shifted into place.  Values from
+// position `valid` on are zero.  This lets rows that start at any 2-byte
+// boundary be read with 16-byte loads.
+//
+// Lanes call it in runs: within a run, lane l + 1 asks for the eight values
+// after lane l's, so lane l's second chunk is lane l + 1's first and comes
+// from that lane; only the last lane of a run (`run_end`, which must hold
+// for lane 63) loads it itself.  Loads past the buffer's end read zero.
+__device__ __forceinline__ u16x8 load_shifted_u16x8(__amdgpu_buffer_rsrc_t rs, int e, int valid,
+                                                    bool run_end) {
     typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
     const int o = 2 * e;
     const int ob = o & ~15;
     const u32x4 v0 = __builtin_amdgcn_raw_buffer_load_b128(rs, ob, 0, 0);
-    const u32x4 v1 = __builtin_amdgcn_raw_buffer_load_b128(rs, ob + 16, 0, 0);
+    // lanes inside a run ask for an offset past any buffer (zero, no fetch)
+    const u32x4 own = __builtin_amdgcn_raw_buffer_load_b128(rs, run_end ? ob + 16 : 0x7FFFFFF0, 0, 0);
+    // the shuffle runs in every lane (a lane reading an inactive lane gets
+    // nothing), and only then is the lane's own load chosen where it applies
+    u32x4 v1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const unsigned next = (unsigned)__shfl_down((int)v0[q], 1, 64);
+        v1[q] = run_end ? own[q] : next;
+    }
     const unsigned w[8] = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-    const int d = (o >> 2) & 3;  // whole dwords to skip
-    const bool half = (o & 2) != 0;
+    // Shift right by (o & 15) bytes: 8, then 4 bytes as the position asks
+    // (bitwise selects, no branches), then 2 bytes with v_alignbyte, whose
+    // shift is 0 or 2.
+    const unsigned m8 = (o & 8) ? ~0u : 0u, m4 = (o & 4) ? ~0u : 0u;
+    unsigned w1[6], w2[5];
+#pragma unroll
+    for (int i = 0; i < 6; ++i) w1[i] = w[i] ^ ((w[i] ^ w[i + 2]) & m8);
+#pragma unroll
+    for (int i = 0; i < 5; ++i) w2[i] = w1[i] ^ ((w1[i] ^ w1[i + 1]) & m4);
+    const unsigned sh = (unsigned)(o & 2);
     u32x4 r;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const unsigned lo = d == 0 ? w[i] : d == 1 ? w[i + 1] : d == 2 ? w[i + 2] : w[i + 3];
-        const unsigned hi = d == 0 ? w[i + 1] : d == 1 ? w[i + 2] : d == 2 ? w[i + 3] : w[i + 4];
-        r[i] = half ? __builtin_amdgcn_alignbyte(hi, lo, 2) : lo;   // (hi:lo) >> 16
+        // values 2i and 2i + 1 kept only below `valid`
+        const unsigned keep = (2 * i < valid ? 0xFFFFu : 0u) | (2 * i + 1 < valid ? 0xFFFF0000u : 0u);
+        r[i] = __builtin_amdgcn_alignbyte(w2[i + 1], w2[i], sh) & keep;   // (hi:lo) >> 8*sh
     }
-    u16x8 v = __builtin_bit_cast(u16x8, r);
-#pragma unroll
-    for (int k = 0; k < 8; ++k)
-        if (k >= valid) v[k] = 0;
-    return v;
+    return __builtin_bit_cast(u16x8, r);
 }
 
 // Buffer resource covering `bytes` bytes from p, with its base rounded down
