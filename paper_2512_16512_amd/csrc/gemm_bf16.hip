@@ -207,19 +207,11 @@ gemm_bf16_kernel(GemmArgs p) {
 // the register-staged kernel above runs.
 
 // A rows hold CA = BK/8 chunks of 16 bytes; chunk c of row m sits at slot
-// c ^ swz_a(m).  Two ways of reading an A fragment (16 bytes per lane) are
-// compiled (AMODE):
-//  0: one ds_read_b128.  On gfx950 a wave-wide ds_read_b128 keeps the LDS
-//     busy for 16 cycles even when it is contiguous; the swizzle keeps it at
-//     that floor (unswizzled 64-byte rows cost 3.5 times more).
-//  1: two ds_read_b64, each conflict-free (2 LDS cycles): rows sharing a
-//     256-byte window are spread over the CA slots, and the first read of
-//     lanes whose row has bit 4 set takes the high half of the chunk, so the
-//     32 lanes served together hit 32 distinct 8-byte bank pairs.  A per-lane
-//     select restores k order.
-template <int CA, int AMODE>
+// c ^ swz_a(m), and an A fragment (16 bytes per lane) is one ds_read_b128.
+// The swizzle spreads the rows that one read serves over distinct banks
+// (unswizzled 64-byte rows cost 3.5 times more LDS time).
+template <int CA>
 __device__ __forceinline__ int swz_a(int row) {
-    if constexpr (AMODE == 1) return CA == 4 ? (row >> 2) & 3 : (row >> 1) & 7;
     return CA == 4 ? ((row >> 1) ^ (row >> 3)) & 3 : (row ^ (row >> 3)) & 7;
 }
 
@@ -265,9 +257,9 @@ struct Bf16DmaCfg {
 //             (no wave reads it any more); the copy of stage kt+STAGES into
 //             that slot and the first fragment reads of stage kt+1 are
 //             issued before the last step's MFMAs.
-// SCHED = 1 adds scheduling-group barriers that interleave one or two LDS
-// reads with each MFMA.
-template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES, int AMODE, int SCHED>
+// Scheduling-group barriers interleave the LDS reads of the next k-step
+// with the MFMAs of the current one.
+template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES>
 __global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
 gemm_bf16_dma_kernel(GemmArgs p) {
     typedef Bf16DmaCfg<BM, BN, BK, WM, WN, MI, STAGES> G;
@@ -297,7 +289,7 @@ gemm_bf16_dma_kernel(GemmArgs p) {
         const int blk = wave * G::A_PER_WAVE + q;
         const int row = blk * (1024 / G::RA) + lane / G::CA;
         a_row[q] = row;
-        a_col[q] = 8 * ((lane % G::CA) ^ swz_a<G::CA, AMODE>(row));
+        a_col[q] = 8 * ((lane % G::CA) ^ swz_a<G::CA>(row));
     }
     int b_row[G::B_PER_WAVE], b_col[G::B_PER_WAVE];
 #pragma unroll
@@ -338,15 +330,12 @@ gemm_bf16_dma_kernel(GemmArgs p) {
     };
 
     // Fragment addressing inside one stage (byte offsets).
-    int a_off[G::TM], a_swz[G::TM], a_first[G::TM];
+    int a_off[G::TM], a_swz[G::TM];
 #pragma unroll
     for (int i = 0; i < G::TM; ++i) {
         const int row = wm * WM + i * MI + lrow;
         a_off[i] = row * G::RA;
-        a_swz[i] = swz_a<G::CA, AMODE>(row);
-        // AMODE 1: 8-byte half read first (row bit 4 for 32-row instruction
-        // tiles; for 16-row tiles the k-groups sharing a cycle differ in lgrp)
-        a_first[i] = MI == 32 ? (row >> 4) & 1 : (lgrp & 1);
+        a_swz[i] = swz_a<G::CA>(row);
     }
     const int rsub = (lane & 15) >> 2;  // transpose-read row inside the group of four
     const int bsw = swz_b(rsub);        // the rows this lane reads are all == rsub (mod 4)
@@ -373,22 +362,7 @@ gemm_bf16_dma_kernel(GemmArgs p) {
 #pragma unroll
         for (int i = 0; i < G::TM; ++i) {
             const int slot = ((kk >> 3) + lgrp) ^ a_swz[i];
-            if constexpr (AMODE == 1) {
-                // The offsets go through an empty asm so that the compiler
-                // cannot see that reads of neighbouring fragments are a
-                // constant distance apart: it would fuse them into
-                // ds_read2st64_b64, which costs as much LDS time as b128.
-                int o1 = a_off[i] + slot * 16 + 8 * a_first[i];
-                int o2 = a_off[i] + slot * 16 + 8 - 8 * a_first[i];
-                asm volatile("" : "+v"(o1), "+v"(o2));
-                const u16x4 first = *reinterpret_cast<const u16x4 *>(As + o1);
-                const u16x4 second = *reinterpret_cast<const u16x4 *>(As + o2);
-                const u16x4 lo = a_first[i] ? second : first;
-                const u16x4 hi = a_first[i] ? first : second;
-                af[buf][i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-            } else {
-                af[buf][i] = *reinterpret_cast<const u16x8 *>(As + a_off[i] + slot * 16);
-            }
+            af[buf][i] = *reinterpret_cast<const u16x8 *>(As + a_off[i] + slot * 16);
         }
 #pragma unroll
         for (int j = 0; j < G::TN; ++j) {
@@ -436,15 +410,13 @@ gemm_bf16_dma_kernel(GemmArgs p) {
 
     // One MFMA followed by its share of the next step's LDS reads.
     auto interleave = [&]() {
-        if constexpr (SCHED == 1) {
-            constexpr int NM = G::TM * G::TN;
-            constexpr int ND = (AMODE == 1 ? 2 : 1) * G::TM + 2 * G::TN;
-            constexpr int PER = (ND + NM - 1) / NM;
+        constexpr int NM = G::TM * G::TN;
+        constexpr int ND = G::TM + 2 * G::TN;
+        constexpr int PER = (ND + NM - 1) / NM;
 #pragma unroll
-            for (int m = 0; m < NM; ++m) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-                if (m * PER < ND) __builtin_amdgcn_sched_group_barrier(0x100, PER, 0);  // DS read
-            }
+        for (int m = 0; m < NM; ++m) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            if (m * PER < ND) __builtin_amdgcn_sched_group_barrier(0x100, PER, 0);  // DS read
         }
     };
 
@@ -503,7 +475,7 @@ gemm_bf16_dma_kernel(GemmArgs p) {
         }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES, int AMODE, int SCHED>
+template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES>
 hipError_t launch_bf16_dma(const GemmArgs &a, hipStream_t s) {
     typedef Bf16DmaCfg<BM, BN, BK, WM, WN, MI, STAGES> G;
     const unsigned tiles = (unsigned)(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
@@ -511,7 +483,7 @@ hipError_t launch_bf16_dma(const GemmArgs &a, hipStream_t s) {
     void *kargs[] = {&args};
     return hipLaunchKernel(
         reinterpret_cast<const void *>(
-            &gemm_bf16_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES, AMODE, SCHED>),
+            &gemm_bf16_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES>),
         dim3(tiles), dim3(G::NT), kargs, 0, s);
 }
 
@@ -542,9 +514,9 @@ hipError_t launch_bf16(const GemmArgs &a, hipStream_t s) {
 #define XTC_BF16_DMA_INSTANCE(BM, BN, BK, WM, WN, MI, STAGES)                                 \
     GemmInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), STAGES, -1, 0),           \
-            &launch_bf16_dma<BM, BN, BK, WM, WN, MI, STAGES, 0, 1>,                           \
+            &launch_bf16_dma<BM, BN, BK, WM, WN, MI, STAGES>,                                 \
             &launch_bf16<BM, BN, BK, WM, WN, MI, 8, false>, kWholeChunks,                     \
-            &occupancy_of<&gemm_bf16_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES, 0, 1>,        \
+            &occupancy_of<&gemm_bf16_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES>,              \
                           (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
