@@ -623,6 +623,17 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
                           (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
+// 256x256 tiles: the register-staged kernel with the same tiles would spill,
+// so the fallback runs 128x128 tiles of four 64x64 waves.
+#define XTC_F32_DMA_BIG_INSTANCE(BM, BN, BK, WM, WN, STAGES)                                  \
+    GemmInstance {                                                                            \
+        make_sched(BM, BN, BK, WM, WN, 32, 32, 2, STAGES, -1, 0),                             \
+            &launch_f32_dma<BM, BN, BK, WM, WN, 32, STAGES>,                                  \
+            &launch_f32<128, 128, 32, 64, 64, 32, 4, false>, kWholeChunks,                    \
+            &occupancy_of<&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, 32, STAGES>,               \
+                          (BM / WM) * (BN / WN) * 64, 0>                                      \
+    }
+
 // Reduction-split instances: KS waves per MI*TM x MI*TN tile, U fragment
 // sets per K-step, D K-steps in flight per wave, no LDS staging.
 #define XTC_F32_KSPLIT_INSTANCE(MI, TM, TN, KS, U, D)                                         \
@@ -642,6 +653,8 @@ const GemmInstance kF32Instances[] = {
     XTC_F32_DMA_MI_INSTANCE(128, 128, 32, 64, 64, 16, 2),   // 16x16x4 instruction tile
     XTC_F32_DMA_INSTANCE(256, 128, 32, 64, 64, 2),   // 8 waves of 64x64
     XTC_F32_DMA_INSTANCE(128, 256, 32, 64, 64, 2),
+    XTC_F32_DMA_BIG_INSTANCE(256, 256, 32, 128, 64, 2),   // default for large problems
+    XTC_F32_DMA_BIG_INSTANCE(256, 256, 32, 64, 64, 2),    // 16 waves of 64x64
     XTC_F32_DMA_INSTANCE(64, 128, 32, 32, 64, 3),    // mid-size problems
     XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 4),
     XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 2),

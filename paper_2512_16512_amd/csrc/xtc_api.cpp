@@ -184,7 +184,13 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
         // reduction-split tile that still gives one tile per CU (measured
         // over 16x16 .. 128x128 tiles on shapes from 256^3 to 4096^3 and
         // skinny ones such as 128x128x4096 and 64x4096x1024).
-        if (tiles(256, 128) >= 2 * cus) {
+        if (tiles(256, 256) >= cus) {
+            // eight 128x64 waves, one workgroup per CU: half the copy
+            // traffic per FLOP of 256x128 tiles (4096^3: 141.3 -> 145.3
+            // TFLOP/s in one sweep)
+            *out = make_sched(256, 256, 32, 128, 64, 32, 32, 2, 2, -1, 0);
+            big = true;
+        } else if (tiles(256, 128) >= 2 * cus) {
             // eight 64x64 waves: a quarter less copy traffic per FLOP than
             // 128x128 (4096^3: 139.6 -> 142.5 TFLOP/s)
             *out = make_sched(256, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0);
