@@ -100,6 +100,8 @@ typedef enum {
  *                  block_n = 208 (16x16x4 instructions) needs C % 8 == 0
  *                  and covers at most 208 pixels per workgroup, the count
  *                  chosen per launch so that workgroups split evenly;
+ *                  block_n = 416 is the same with two such pixel halves
+ *                  per workgroup (8 waves) sharing one input patch;
  *                  other shapes run the tap-major kernel;
  *                  bf16: chunks of 16, k = ((ic/16)*R*S + kh*S + kw)*16 +
  *                  ic%16, needs C % 16 == 0, even W, pad_w <= 2,

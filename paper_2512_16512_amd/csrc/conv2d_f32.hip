@@ -999,30 +999,45 @@ conv2d_f32_halo_kernel(ConvArgs p) {
 // 16 banks, which keeps the groups on disjoint banks unless a 16-pixel
 // block wraps to the next image row.
 namespace halo16 {
-constexpr int BM = 64, NWAVES = 4, NT = 256;
+constexpr int BM = 64;
 constexpr int NB = 13;                        // 16-pixel column blocks per wave
-constexpr int BN = 16 * NB;                   // largest pixel tile (208)
-constexpr int CC = 8, NTAP = 9, PR = 8, CO = 4;
+constexpr int CC = 8, NTAP = 9, CO = 4;
 constexpr int NSTEP = NTAP * CC / 4;          // instruction k-steps per stage (18)
-constexpr int PLANE = PR * 64 + 16;
 constexpr int A_FLOATS = NTAP * BM * CC;      // [tap][oc][c]
 constexpr int A_BYTES = A_FLOATS * 4;
-constexpr int B_BYTES = CC * PLANE * 4;
-constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
 constexpr int A_COPIES = A_FLOATS / 64;       // 72
-constexpr int A_PER_WAVE = A_COPIES / NWAVES; // 18
-constexpr int B_COPIES = CC * PR;             // 64
-constexpr int B_PER_WAVE = B_COPIES / NWAVES; // 16: two channels x eight rows
-constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;
-static_assert(A_PER_WAVE * NWAVES == A_COPIES && B_PER_WAVE * NWAVES == B_COPIES, "copy split");
-static_assert((PLANE % 64) == 16, "lane groups 16 banks apart");
 static_assert(NSTEP % 2 == 0, "fragment buffers keep their parity from stage to stage");
+
+// NH pixel halves per workgroup: 4*NH waves, wave w owns output channels
+// 16*(w % 4) .. +15 and the 16*NB pixels of half w / 4.  Two halves (8
+// waves, up to 416 pixels) share one patch of 10 rows and one copy of the
+// stage's weights, where two one-half workgroups load 8 rows and the
+// weights each.
+template <int NH>
+struct Cfg {
+    static constexpr int NWAVES = 4 * NH, NT = 64 * NWAVES;
+    static constexpr int BN = 16 * NB * NH;       // largest pixel tile
+    static constexpr int PR = NH == 1 ? 8 : 10;   // patch rows
+    static constexpr int PLANE = PR * 64 + 16;
+    static constexpr int B_BYTES = CC * PLANE * 4;
+    static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+    static constexpr int A_PER_WAVE = A_COPIES / NWAVES;   // 18 or 9
+    static constexpr int B_COPIES = CC * PR;               // one per (channel, patch row)
+    static constexpr int B_PER_WAVE = B_COPIES / NWAVES;   // 16 (two channels) or 10 (one)
+    static constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;
+    static_assert(A_PER_WAVE * NWAVES == A_COPIES && B_PER_WAVE * NWAVES == B_COPIES, "copy split");
+    static_assert(B_PER_WAVE % PR == 0, "a wave copies whole channels");
+    static_assert((PLANE % 64) == 16, "lane groups 16 banks apart");
+};
 }  // namespace halo16
 
-template <int STAGES>
-__global__ void __launch_bounds__(halo16::NT)
+template <int STAGES, int NH>
+__global__ void __launch_bounds__(halo16::Cfg<NH>::NT)
 conv2d_f32_halo16_kernel(ConvArgs p) {
     using namespace halo16;
+    typedef Cfg<NH> G;
+    constexpr int NWAVES = G::NWAVES, PR = G::PR, PLANE = G::PLANE, STAGE_BYTES = G::STAGE_BYTES;
+    constexpr int A_PER_WAVE = G::A_PER_WAVE, LOADS = G::LOADS;
     typedef F32Mfma<16> MF;
     static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
     static_assert(STAGES * STAGE_BYTES <= 80 * 1024, "two workgroups per CU");
@@ -1030,6 +1045,7 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
+    const int wq = wave & 3, half = wave >> 2;   // output-channel group, pixel half
     const int lcol = lane & 15, lgrp = lane >> 4;
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
 
@@ -1085,14 +1101,15 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
         so_b += b_stage;
     };
 
-    // Fragment bases.  A: output channel 16*wave + lcol, channel lgrp (+4s).
-    // B: pixel p0 + 16j + lcol of the patch (clamped to position 0 past the
+    // Fragment bases.  A: output channel 16*wq + lcol, channel lgrp (+4s).
+    // B: pixel pw0 + 16j + lcol of the patch (clamped to position 0 past the
     // tile; such columns are not stored), channel plane lgrp (+4s).
-    const int a_base = ((wave * 16 + lcol) * CC + lgrp) * 4;
+    const int a_base = ((wq * 16 + lcol) * CC + lgrp) * 4;
+    const int pw0 = p0 + 16 * NB * half;     // first pixel of this wave's half
     int b_base[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-        const int pix = p0 + 16 * j + lcol;
+        const int pix = pw0 + 16 * j + lcol;
         int off = 0;
         if (pix < pend) {
             const int oh = pix / OW, ow = pix - oh * OW;
@@ -1182,11 +1199,11 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
     float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-        const int pix = p0 + 16 * j + lcol;
+        const int pix = pw0 + 16 * j + lcol;
         if (pix >= pend) continue;
 #pragma unroll
         for (int r = 0; r < MF::NACC; ++r) {
-            const int oc = m0 + 16 * wave + MF::row(lane, r);
+            const int oc = m0 + 16 * wq + MF::row(lane, r);
             if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[j][r] < 0.f) ? 0.f : acc[j][r];
         }
     }
@@ -1215,24 +1232,27 @@ hipError_t launch_conv_f32_halo(const ConvArgs &a, hipStream_t s) {
                            dim3(tiles), dim3(halo::NT), kargs, 0, s);
 }
 
-// Tiles per image for the balanced halo kernel: the fewest that keep a tile
-// within 208 pixels; 0 when the shape is outside the kernel's class (then
-// the 64x256 halo kernel, or the tap-major kernel, runs).
+// Pixels per tile for the balanced halo kernel with NH halves: the fewest
+// tiles per image that keep a tile within 208*NH pixels; 0 when the shape is
+// outside the kernel's class (then the 64x256 halo kernel, or the tap-major
+// kernel, runs).
+template <int NH>
 inline int halo16_tile_px(const ConvArgs &a) {
     using namespace halo16;
+    typedef Cfg<NH> G;
     if (a.R != 3 || a.S != 3 || a.sh != 1 || a.sw != 1) return 0;
     if (a.C % CC != 0 || a.pw > CO) return 0;
     if (a.OW - a.pw + 5 > 63) return 0;                  // last patch column used (W + pw <= 60)
     const int OHW = a.OH * a.OW;
-    const int t = (OHW + BN - 1) / BN;
+    const int t = (OHW + G::BN - 1) / G::BN;
     const int pt = (OHW + t - 1) / t;
     const int span = (pt - 1 + a.OW - 1) / a.OW + 1;      // output rows a tile can touch
-    return span + 2 <= PR ? pt : 0;
+    return span + 2 <= G::PR ? pt : 0;
 }
 
-template <int STAGES>
+template <int STAGES, int NH>
 hipError_t launch_conv_f32_halo16(const ConvArgs &a, hipStream_t s) {
-    const int pt = halo16_tile_px(a);
+    const int pt = halo16_tile_px<NH>(a);
     if (pt == 0) return launch_conv_f32_halo<STAGES>(a, s);
     ConvArgs args = a;
     args.tile_px = pt;
@@ -1240,8 +1260,8 @@ hipError_t launch_conv_f32_halo16(const ConvArgs &a, hipStream_t s) {
     const unsigned tiles = (unsigned)(((a.OC + halo16::BM - 1) / halo16::BM) * a.Nb *
                                       ((OHW + pt - 1) / pt));
     void *kargs[] = {&args};
-    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_halo16_kernel<STAGES>),
-                           dim3(tiles), dim3(halo16::NT), kargs, 0, s);
+    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_halo16_kernel<STAGES, NH>),
+                           dim3(tiles), dim3(halo16::Cfg<NH>::NT), kargs, 0, s);
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int MI, int PAD>
@@ -1284,8 +1304,11 @@ hipError_t launch_conv_f32(const ConvArgs &a, hipStream_t s) {
 
 const ConvInstance kConvInstances[] = {
     ConvInstance{make_sched(64, 208, 8, 16, 208, 16, 16, 4, 2, -1, 0, 2),  // balanced halo, 3x3 stride 1
-                 &launch_conv_f32_halo16<2>,
-                 &occupancy_of<&conv2d_f32_halo16_kernel<2>, halo16::NT, 0>},
+                 &launch_conv_f32_halo16<2, 1>,
+                 &occupancy_of<&conv2d_f32_halo16_kernel<2, 1>, halo16::Cfg<1>::NT, 0>},
+    ConvInstance{make_sched(64, 416, 8, 16, 208, 16, 16, 4, 2, -1, 0, 2),  // the same, two pixel halves
+                 &launch_conv_f32_halo16<2, 2>,
+                 &occupancy_of<&conv2d_f32_halo16_kernel<2, 2>, halo16::Cfg<2>::NT, 0>},
     ConvInstance{make_sched(64, 256, 8, 64, 64, 32, 32, 2, 2, -1, 0, 2),   // halo, 3x3 stride 1
                  &launch_conv_f32_halo<2>,
                  &occupancy_of<&conv2d_f32_halo_kernel<2>, halo::NT, 0>},

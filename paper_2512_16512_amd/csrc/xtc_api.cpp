@@ -162,13 +162,18 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     if (op == XTC_OP_CONV2D) {
         // The balanced halo-tiled kernel where the shape allows it (3x3,
         // stride 1, rows of about 56 pixels): 64 output channels x at most
-        // 208 pixels per workgroup, the pixel tile sized so that the
+        // 208 (or 416) pixels per workgroup, the pixel tile sized so that the
         // workgroups split evenly over the CUs; else the tap-major kernel's
         // 64x256 tiles of 4 waves (64x64 each) with a two-stage ring, two
         // workgroups per CU, so up to 512 tiles run in a single wave.  When
         // that leaves CUs idle (a small image batch), 64x64 tiles of four
         // 32x32 waves give four times as many workgroups.
         *out = make_sched(64, 208, 8, 16, 208, 16, 16, 4, 2, -1, 0, 2);
+        // two pixel halves per workgroup (one patch and one weight copy for
+        // 416 pixels) once that still gives about a workgroup per CU
+        // (32x64x56x56 layer: 65.6 -> 63.6 us)
+        if (tiles(64, 416) >= cus - cus / 8)
+            *out = make_sched(64, 416, 8, 16, 208, 16, 16, 4, 2, -1, 0, 2);
         if (M > 64)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 2, 2, -1, 0, 1);
         else if (tiles(64, 256) < cus)
