@@ -337,7 +337,7 @@ def cpu_baseline_leg(results, budget_s: float):
     out["parity"] = parity
     # the oracle on one thread for the two small configs (full products)
     single = {}
-    for cfg in xi.CONFIGS[:2]:
+    for cfg in (xi.MATMUL_F32_256, xi.MATMUL_F32_1000):
         A, B = xi.matmul_inputs(cfg)
         _, dt = oracle.timed(oracle.matmul, A, B, nthreads=1)
         single["matmul_f32_%dx%dx%d" % (cfg["M"], cfg["N"], cfg["K"])] = {
@@ -379,10 +379,10 @@ def _cpu_model():
 def head_shape(kind: str) -> dict:
     """Shape and layout keys of a headline workload for the JSON config."""
     if kind in ("fp32", "bf16"):
-        cfg = xi.CONFIGS[2 if kind == "fp32" else 3]
+        cfg = (xi.MATMUL_F32_4096 if kind == "fp32" else xi.MATMUL_BF16_8192)
         return {"M": cfg["M"], "N": cfg["N"], "K": cfg["K"],
                 "layout": "row-major A[M,K], B[K,N], C[M,N]"}
-    cfg = xi.CONFIGS[4]
+    cfg = xi.CONV_F32_56
     return {k: cfg[k] for k in ("N", "C", "H", "W", "OC", "R", "S", "stride", "pad")} | {
         "layout": "X NCHW, W OIHW, Y NCHW"}
 
@@ -427,22 +427,22 @@ def main():
     kinds = [k.strip() for k in args.only.split(",") if k.strip()]
     results, summaries = {}, {}
     if "fp32" in kinds:
-        cfg = xi.CONFIGS[2]
+        cfg = xi.MATMUL_F32_4096
         results["fp32"] = run_matmul(cfg, args.steps, args.warmup)
         summaries["fp32"] = summary("f32", cfg, results["fp32"], "matmul_f32_4096x4096x4096")
         print("# fp32 4096^3: %.4f ms/launch" % results["fp32"]["ms"], file=sys.stderr, flush=True)
     if "bf16" in kinds:
-        cfg = xi.CONFIGS[3]
+        cfg = xi.MATMUL_BF16_8192
         results["bf16"] = run_matmul(cfg, args.steps, args.warmup)
         summaries["bf16"] = summary("bf16", cfg, results["bf16"], "matmul_bf16_8192x8192x8192")
         print("# bf16 8192^3: %.4f ms/launch" % results["bf16"]["ms"], file=sys.stderr, flush=True)
     if "conv" in kinds:
-        cfg = xi.CONFIGS[4]
+        cfg = xi.CONV_F32_56
         results["conv"] = run_conv(cfg, args.steps, args.warmup)
         summaries["conv"] = summary("conv", cfg, results["conv"], "conv2d_f32_n32c64h56w56_oc64_r3s3")
         print("# conv: %.4f ms/launch" % results["conv"]["ms"], file=sys.stderr, flush=True)
     if "conv_bf16" in kinds:
-        cfg = xi.CONFIGS[4]
+        cfg = xi.CONV_F32_56
         results["conv_bf16"] = run_conv(cfg, args.steps, args.warmup, dtype="bf16")
         summaries["conv_bf16"] = summary("conv_bf16", cfg, results["conv_bf16"],
                                          "conv2d_bf16_n32c64h56w56_oc64_r3s3")
@@ -517,7 +517,7 @@ def vendor_line(steps: int, warmup: int, ours: dict):
     torch.backends.cuda.matmul.allow_tf32 = False
     torch.backends.cudnn.allow_tf32 = False
     out = {"vendor": "torch %s, HIP %s" % (torch.__version__, torch.version.hip)}
-    for kind, cfg in (("fp32", xi.CONFIGS[2]), ("bf16", xi.CONFIGS[3])):
+    for kind, cfg in (("fp32", xi.MATMUL_F32_4096), ("bf16", xi.MATMUL_BF16_8192)):
         A, B = xi.matmul_inputs(cfg)
         a, b = to_dev(A), to_dev(B)
         c = torch.empty((cfg["M"], cfg["N"]), dtype=a.dtype, device="cuda")
@@ -539,7 +539,7 @@ def vendor_line(steps: int, warmup: int, ours: dict):
                 out["bf16_f32_out"] = {"error": str(e)[:200]}
             del c32
         del a, b, c
-    cfg = xi.CONFIGS[4]
+    cfg = xi.CONV_F32_56
     X, W = xi.conv_inputs(cfg)
     xd, wd = to_dev(X), to_dev(W)
     f = lambda: torch.nn.functional.conv2d(xd, wd, stride=cfg["stride"], padding=cfg["pad"])

@@ -44,14 +44,14 @@ def _run_mm(x, A, B, sched=None):
     return to_host(c)
 
 
-# ------------------------------------------------------------ full configs
+# ---------------------------------------------------------- full workloads
 
 
 @pytest.mark.parametrize("ci", [0, 1, 2, 3])
-def test_matmul_config_parity(x, ci):
+def test_matmul_workload_parity(x, ci):
     import torch
-    cfg = xi.CONFIGS[ci]
-    say("matmul config", ci, cfg["name"])
+    cfg = xi.WORKLOADS[ci]
+    say("matmul workload", ci, cfg["name"])
     A, B = xi.matmul_inputs(cfg)
     a, b = to_dev(A), to_dev(B)
     c = x.matmul(a, b)
@@ -95,7 +95,7 @@ def test_conv_bf16_small_int_exact_every_instance(x, shape):
 def test_conv_bf16_config_shape_parity(x):
     # the 32x64x56x56 -> 64 layer with bf16 inputs, checked on sampled outputs
     import torch
-    cfg = xi.CONFIGS[4]
+    cfg = xi.CONV_F32_56
     X, W = xi.conv_inputs(cfg)
     Xb, Wb = xi.f32_to_bf16_bits(X), xi.f32_to_bf16_bits(W)
     say("conv bf16 config shape")
@@ -109,7 +109,7 @@ def test_conv_bf16_config_shape_parity(x):
 
 def test_conv_config_parity(x):
     import torch
-    cfg = xi.CONFIGS[4]
+    cfg = xi.CONV_F32_56
     say("conv config", cfg["name"])
     X, W = xi.conv_inputs(cfg)
     y = x.conv2d_nchw(to_dev(X), to_dev(W), stride=cfg["stride"], pad=cfg["pad"])

@@ -80,9 +80,11 @@ def test_sample_indices():
     assert f.min() >= 0 and f.max() < 32 * 64 * 56 * 56
 
 
-def test_config_shapes():
-    c = xi.CONFIGS
+def test_workload_shapes():
+    c = xi.WORKLOADS
     assert [x["index"] for x in c] == [0, 1, 2, 3, 4]
+    assert (xi.MATMUL_F32_256, xi.MATMUL_F32_1000, xi.MATMUL_F32_4096, xi.MATMUL_BF16_8192,
+            xi.CONV_F32_56) == tuple(c)
     assert (c[3]["M"], c[3]["dtype"]) == (8192, "bf16")
     oh, ow = xi.conv_out_hw(56, 56, 3, 3, 1, 1, 1, 1)
     assert (oh, ow) == (56, 56)
@@ -98,4 +100,4 @@ def test_paper_workload_shapes():
     oh, ow = xi.conv_out_hw(c["H"], c["W"], c["R"], c["S"], c["stride"], c["stride"], c["pad"],
                             c["pad"])
     assert (oh, ow, c["OC"], c["C"]) == (112, 112, 16, 3)     # [112,112,16] x [7,7,3]
-    assert not set(w) & {x["index"] for x in xi.CONFIGS}        # distinct seeds
+    assert not set(w) & {x["index"] for x in xi.WORKLOADS}        # distinct seeds

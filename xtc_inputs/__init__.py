@@ -16,7 +16,7 @@ a 2**-23 grid, exactly representable in fp32.
 bf16 values are the round-to-nearest-even of those fp32 values on the bit
 pattern (finite inputs only, no NaN case).
 
-Seeds follow ``1000 * config_index + stream`` with stream 1 = A (or X), 2 = B
+Seeds follow ``1000 * index + stream`` (the workload's index) with stream 1 = A (or X), 2 = B
 (or W), 3 = sample indices.
 """
 
@@ -144,14 +144,16 @@ def sample_indices_flat(seed: int, total: int, count: int = 4096) -> np.ndarray:
     return (z % np.uint64(total)).astype(np.int64)
 
 
-def seed(config_index: int, stream: int) -> int:
-    """Seed of a stream: 1 = A/X, 2 = B/W, 3 = sample indices."""
-    return 1000 * config_index + stream
+def seed(index: int, stream: int) -> int:
+    """Seed of stream `stream` of workload `index`: 1 = A/X, 2 = B/W,
+    3 = sample indices."""
+    return 1000 * index + stream
 
 
 # The five synthetic workloads.  "check" is "full" when every output is
-# compared, else the number of seeded sampled outputs.
-CONFIGS = [
+# compared, else the number of seeded sampled outputs; "index" numbers the
+# workload for its seeds.
+WORKLOADS = [
     dict(index=0, op="matmul", dtype="f32", M=256, N=256, K=256, check="full",
          name="matmul fp32 256x256x256"),
     dict(index=1, op="matmul", dtype="f32", M=1000, N=1000, K=1000, check="full",
@@ -164,6 +166,7 @@ CONFIGS = [
          stride=1, pad=1, check=4096,
          name="conv2d NCHW fp32 32x64x56x56 -> 64, 3x3, stride 1, pad 1"),
 ]
+MATMUL_F32_256, MATMUL_F32_1000, MATMUL_F32_4096, MATMUL_BF16_8192, CONV_F32_56 = WORKLOADS
 
 
 # The other workloads the paper runs, as extra parity and measurement cases.
