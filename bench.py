@@ -7,8 +7,10 @@ the HIP-event time of exactly ``--steps`` launches, after ``--warmup``
 untimed ones).  The same line also reports, timed the same way, the bf16
 matmul 8192^3 (fp32 accumulate and output) and the fp32 conv2d 32x64x56x56
 -> 64, 3x3, stride 1, pad 1 as an implicit GEMM (also with bf16 inputs), each
-with its fraction of the MI355X matrix-core peak; the paper's other, smaller
-workloads (matmuls
+with its roofline (the matrix-core peak, or HBM bandwidth for workloads below
+the ridge point, such as the bf16 conv and the tall-skinny fp32 matmul
+32768x16x4096 that measures the HBM streaming rate); the paper's other,
+smaller workloads (matmuls
 1024^3, [512,128]x[128,1024], matmul+relu [256,128]x[128,1024], 256x258x512,
 and the 7x7 stride-2 conv2d 3 -> 16 channels at 224x224), timed as replays of
 a HIP graph of launches; and the fp64 CPU oracle timed on the host cores on a
@@ -17,7 +19,7 @@ sampled outputs of every timed launch (every output of the small workloads)
 against the oracle.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--only fp32,bf16,conv,conv_bf16,paper] [--no-cpu-baseline]
+                       [--only fp32,bf16,conv,conv_bf16,skinny,paper] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -328,7 +330,7 @@ def cpu_baseline_leg(results, budget_s: float):
             tol = 1e-5 if kind == "conv" else 1e-2
         else:
             ref = oracle.matmul_sampled(r["A"], r["B"], r["I"], r["J"])
-            tol = 1e-5 if kind == "fp32" else 1e-2
+            tol = 1e-2 if kind == "bf16" else 1e-5
         dt = time.perf_counter() - t0
         err = oracle.rel_fro(r["sampled"], ref)
         parity[kind] = {"rel_fro": float("%.3e" % err), "tol": tol, "samples": int(len(ref)),
@@ -392,7 +394,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--only", default="fp32,bf16,conv,conv_bf16,paper")
+    ap.add_argument("--only", default="fp32,bf16,conv,conv_bf16,skinny,paper")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--vendor", action="store_true",
@@ -447,6 +449,13 @@ def main():
         summaries["conv_bf16"] = summary("conv_bf16", cfg, results["conv_bf16"],
                                          "conv2d_bf16_n32c64h56w56_oc64_r3s3")
         print("# conv bf16: %.4f ms/launch" % results["conv_bf16"]["ms"], file=sys.stderr,
+              flush=True)
+
+    if "skinny" in kinds:
+        cfg = xi.MATMUL_F32_SKINNY
+        results["skinny"] = run_matmul(cfg, args.steps, args.warmup)
+        summaries["skinny"] = summary("f32", cfg, results["skinny"], "matmul_f32_32768x16x4096")
+        print("# skinny fp32: %.4f ms/launch" % results["skinny"]["ms"], file=sys.stderr,
               flush=True)
 
     paper = {}

@@ -669,6 +669,7 @@ const GemmInstance kF32Instances[] = {
     XTC_F32_KSPLIT_INSTANCE(32, 2, 2, 4, 2, 3),      // 64x64 tiles
     XTC_F32_KSPLIT_INSTANCE(16, 1, 1, 4, 2, 4),      // 16x16 tiles, 16x16x4 instruction
     XTC_F32_KSPLIT_INSTANCE(16, 1, 1, 8, 2, 4),      // 16x16 tiles, 8 waves
+    XTC_F32_KSPLIT_INSTANCE(16, 2, 1, 8, 2, 4),      // 32x16 tiles: tall-skinny products
 };
 
 }  // namespace

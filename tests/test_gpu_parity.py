@@ -47,10 +47,10 @@ def _run_mm(x, A, B, sched=None):
 # ---------------------------------------------------------- full workloads
 
 
-@pytest.mark.parametrize("ci", [0, 1, 2, 3])
+@pytest.mark.parametrize("ci", [0, 1, 2, 3, 10])
 def test_matmul_workload_parity(x, ci):
     import torch
-    cfg = xi.WORKLOADS[ci]
+    cfg = xi.MATMUL_F32_SKINNY if ci == 10 else xi.WORKLOADS[ci]
     say("matmul workload", ci, cfg["name"])
     A, B = xi.matmul_inputs(cfg)
     a, b = to_dev(A), to_dev(B)

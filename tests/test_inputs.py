@@ -88,6 +88,12 @@ def test_workload_shapes():
     assert (c[3]["M"], c[3]["dtype"]) == (8192, "bf16")
     oh, ow = xi.conv_out_hw(56, 56, 3, 3, 1, 1, 1, 1)
     assert (oh, ow) == (56, 56)
+    sk = xi.MATMUL_F32_SKINNY
+    assert sk["index"] not in {x["index"] for x in c + xi.PAPER_WORKLOADS}   # distinct seeds
+    # below the fp32 ridge point (157.3 TFLOP/s over 8 TB/s = 19.7 FLOP per byte)
+    fl = 2.0 * sk["M"] * sk["N"] * sk["K"]
+    by = 4 * (sk["M"] * sk["K"] + sk["K"] * sk["N"] + sk["M"] * sk["N"])
+    assert fl / by < 19.7
 
 
 def test_paper_workload_shapes():

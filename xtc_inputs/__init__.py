@@ -168,6 +168,11 @@ WORKLOADS = [
 ]
 MATMUL_F32_256, MATMUL_F32_1000, MATMUL_F32_4096, MATMUL_BF16_8192, CONV_F32_56 = WORKLOADS
 
+# A tall-skinny product (16 output columns): 8 FLOP per algorithmic byte, far
+# below the fp32 ridge point, so it measures the path's HBM streaming rate.
+MATMUL_F32_SKINNY = dict(index=10, op="matmul", dtype="f32", M=32768, N=16, K=4096, check=4096,
+                         name="matmul fp32 32768x16x4096 (tall-skinny)")
+
 
 # The other workloads the paper runs, as extra parity and measurement cases.
 # Same generators; seeds follow the index.  "matmul_relu" is the matmul with
