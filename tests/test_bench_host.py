@@ -23,7 +23,8 @@ def test_traffic_only_for_the_measured_kernel_source(monkeypatch):
     rec = json.load(open(path))
     for workload, kind in (("matmul_f32_4096x4096x4096", "f32"),
                            ("matmul_bf16_8192x8192x8192", "bf16"),
-                           ("conv2d_f32_n32c64h56w56_oc64_r3s3", "conv")):
+                           ("conv2d_f32_n32c64h56w56_oc64_r3s3", "conv"),
+                           ("matmul_f32_32768x16x4096", "f32")):
         assert workload in rec
         monkeypatch.setattr(bench, "kernel_hash", lambda k: rec[workload]["kernel_hash"])
         assert bench.measured_traffic(kind, workload) == rec[workload]["hbm_bytes_per_launch"]
