@@ -526,13 +526,14 @@ def vendor_line(steps: int, warmup: int, ours: dict):
     torch.backends.cuda.matmul.allow_tf32 = False
     torch.backends.cudnn.allow_tf32 = False
     out = {"vendor": "torch %s, HIP %s" % (torch.__version__, torch.version.hip)}
-    for kind, cfg in (("fp32", xi.MATMUL_F32_4096), ("bf16", xi.MATMUL_BF16_8192)):
+    for kind, cfg in (("fp32", xi.MATMUL_F32_4096), ("bf16", xi.MATMUL_BF16_8192),
+                      ("skinny", xi.MATMUL_F32_SKINNY)):
         A, B = xi.matmul_inputs(cfg)
         a, b = to_dev(A), to_dev(B)
         c = torch.empty((cfg["M"], cfg["N"]), dtype=a.dtype, device="cuda")
         ms = time_launches(lambda: torch.matmul(a, b, out=c), steps, warmup)
         tf = 2.0 * cfg["M"] * cfg["N"] * cfg["K"] / (ms * 1e-3) / 1e12
-        mine = ours["value"] if kind == "fp32" else ours["also"].get("bf16", {}).get("value")
+        mine = ours["value"] if kind == "fp32" else ours["also"].get(kind, {}).get("value")
         out[kind] = {"workload": cfg["name"], "ms_per_launch": round(ms, 4), "TFLOP/s": round(tf, 2),
                      "ours_TFLOP/s": mine, "output_dtype": str(c.dtype).replace("torch.", "")}
         if kind == "bf16":
