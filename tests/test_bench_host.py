@@ -24,7 +24,8 @@ def test_traffic_only_for_the_measured_kernel_source(monkeypatch):
     for workload, kind in (("matmul_f32_4096x4096x4096", "f32"),
                            ("matmul_bf16_8192x8192x8192", "bf16"),
                            ("conv2d_f32_n32c64h56w56_oc64_r3s3", "conv"),
-                           ("matmul_f32_32768x16x4096", "f32")):
+                           ("matmul_f32_32768x16x4096", "f32"),
+                           ("conv2d_bf16_n32c64h56w56_oc64_r3s3", "conv_bf16")):
         assert workload in rec
         monkeypatch.setattr(bench, "kernel_hash", lambda k: rec[workload]["kernel_hash"])
         assert bench.measured_traffic(kind, workload) == rec[workload]["hbm_bytes_per_launch"]
@@ -37,10 +38,14 @@ def test_traffic_only_for_the_measured_kernel_source(monkeypatch):
 
 
 def test_kernel_hash_covers_every_source_of_the_kernel():
+    import re
+    csrc = os.path.join(ROOT, "paper_2512_16512_amd", "csrc")
     for kind, files in bench.KERNEL_SOURCES.items():
-        assert "tile_map.h" in files and "lds_dma.h" in files
         for f in files:
-            assert os.path.exists(os.path.join(ROOT, "paper_2512_16512_amd", "csrc", f))
+            assert os.path.exists(os.path.join(csrc, f))
+        # every kernel header the kernel's source includes is hashed too
+        inc = set(re.findall(r'#include "([a-z_0-9]+\.h)"', open(os.path.join(csrc, files[0])).read()))
+        assert inc - {"xtc_internal.h"} <= set(files), (kind, inc - set(files))
         assert bench.kernel_hash(kind) == bench.kernel_hash(kind)
 
 
