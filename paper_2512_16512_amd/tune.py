@@ -21,7 +21,7 @@ the replays divided by the launches they contain.
 
 Usage::
 
-    python -m paper_2512_16512_amd.tune matmul f32 1024 1024 1024 [--samples 40]
+    python -m paper_2512_16512_amd.tune matmul f32 1024 1024 1024 [--samples 40] [--journal f.jsonl]
     python -m paper_2512_16512_amd.tune conv2d f32 1 3 224 224 16 7 7 2 3
 """
 from __future__ import annotations
@@ -190,10 +190,39 @@ def warm_up(problem: Problem, sched, ms: float = 100.0) -> None:
         torch.cuda.synchronize()
 
 
-def explore(problem: Problem, n: int | None = None, seed: int = 0, space=None, log=None):
+def _key(sched) -> str:
+    return json.dumps(sched.as_dict(), sort_keys=True)
+
+
+def read_journal(path: str, problem_key: str) -> dict:
+    """Results already recorded in the JSON-lines journal ``path`` for the
+    problem ``problem_key``, by schedule (an incomplete last line, left by an
+    interrupted run, is ignored)."""
+    done = {}
+    try:
+        lines = open(path).read().splitlines()
+    except FileNotFoundError:
+        return done
+    for line in lines:
+        try:
+            rec = json.loads(line)
+        except ValueError:
+            continue
+        if rec.get("problem") == problem_key:
+            done[json.dumps(rec["sched"], sort_keys=True)] = rec
+    return done
+
+
+def explore(problem: Problem, n: int | None = None, seed: int = 0, space=None, log=None,
+            journal: str | None = None):
     """Evaluate ``n`` sampled schedules (the whole design space when None),
     plus the default schedule, against the default schedule's output.
-    Returns (default result, results sorted fastest first)."""
+    Returns (default result, results sorted fastest first).
+
+    With ``journal`` (a JSON-lines file), every evaluated point is appended
+    to it as soon as it is measured, and points the journal already holds for
+    this problem are taken from it instead of being run again: an
+    interrupted sweep resumes where it stopped."""
     if space is None:
         space = design_space(problem.op_code, problem.code)
     pts = space if n is None else sample(space, n, seed)
@@ -202,14 +231,24 @@ def explore(problem: Problem, n: int | None = None, seed: int = 0, space=None, l
     base = evaluate(problem, dflt)
     reference = problem.out.clone()
     base["sched"] = dflt
+    pkey = repr(problem)
+    done = read_journal(journal, pkey) if journal else {}
     results = []
     for s in pts:
-        r = evaluate(problem, s, reference)
+        rec = done.get(_key(s))
+        if rec is not None:
+            r = {k: v for k, v in rec.items() if k not in ("problem", "sched")}
+        else:
+            r = evaluate(problem, s, reference)
+            if journal:
+                with open(journal, "a") as f:
+                    f.write(json.dumps(dict({"problem": pkey, "sched": s.as_dict()}, **r)) + "\n")
         r["sched"] = s
         results.append(r)
         if log:
-            log("%-100r %9.2f us %8.2f TF err %.1e%s" % (s, r["us"], r["tflops"], r["err"],
-                                                          "" if r["valid"] else "  INVALID"))
+            log("%-100r %9.2f us %8.2f TF err %.1e%s%s" % (
+                s, r["us"], r["tflops"], r["err"], "" if r["valid"] else "  INVALID",
+                "  (journal)" if rec is not None else ""))
     results.sort(key=lambda r: (not r["valid"], r["us"]))
     return base, results
 
@@ -228,11 +267,14 @@ def main(argv=None):
     ap.add_argument("--samples", type=int, default=None, help="sampled points (default: all)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--json", default=None, help="write every result to this file")
+    ap.add_argument("--journal", default=None,
+                    help="JSON-lines file: append each point as it is measured and skip points "
+                         "already recorded for this problem (resumes an interrupted sweep)")
     ap.add_argument("--quiet", action="store_true")
     a = ap.parse_args(argv)
     p = Problem(a.op, a.dtype, a.dims)
     log = None if a.quiet else (lambda s: print(s, flush=True))
-    base, res = explore(p, a.samples, a.seed, log=log)
+    base, res = explore(p, a.samples, a.seed, log=log, journal=a.journal)
     best = res[0]
     print("problem  %r" % p)
     print("default  %r  %.2f us  %.2f TFLOP/s" % (base["sched"], base["us"], base["tflops"]))

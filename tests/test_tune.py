@@ -36,6 +36,59 @@ def test_sample_is_seeded_and_distinct(t):
     assert len(t.sample(space, 10 ** 6)) == len(space)
 
 
+def test_journal_resumes_an_interrupted_sweep(t, tmp_path, monkeypatch):
+    """Host logic of the sweep journal, with the measurement replaced by a
+    deterministic stand-in: points are appended as they are measured, a
+    second run over the same journal measures nothing, a run cut short
+    resumes with only the missing points, and an incomplete last line or
+    another problem's lines are not taken as results."""
+    import json
+
+    import paper_2512_16512_amd as x
+    space = t.design_space(x.XTC_OP_MATMUL, x.XTC_F32)[:9]
+    calls = []
+
+    def fake_evaluate(problem, sched, reference=None, **kw):
+        calls.append(t._key(sched))
+        us = 1.0 + sched.block_m / 64.0 + sched.raster + 0.5 * sched.xcd_remap
+        return {"us": us, "tflops": 1.0 / us, "err": 0.0, "valid": True, "per_graph": 1}
+
+    class FakeOut:
+        def clone(self):
+            return self
+
+    class FakeProblem:
+        op_code, code, out = x.XTC_OP_MATMUL, x.XTC_F32, FakeOut()
+
+        def __init__(self, name):
+            self.name = name
+
+        def default_schedule(self):
+            return space[0]
+
+        def __repr__(self):
+            return self.name
+
+    monkeypatch.setattr(t, "evaluate", fake_evaluate)
+    monkeypatch.setattr(t, "warm_up", lambda p, s, ms=0: None)
+    j = str(tmp_path / "sweep.jsonl")
+    _, full = t.explore(FakeProblem("p"), space=space, journal=j)
+    assert len(calls) == 1 + 9 and len(open(j).read().splitlines()) == 9
+    calls.clear()
+    _, again = t.explore(FakeProblem("p"), space=space, journal=j)
+    assert len(calls) == 1                       # only the default's reference run
+    assert [r["us"] for r in again] == [r["us"] for r in full]
+    # cut short after 4 points, with a torn fifth line and another problem's line
+    lines = open(j).read().splitlines()
+    other = json.loads(lines[5])
+    other["problem"] = "q"
+    open(j, "w").write("\n".join(lines[:4] + [json.dumps(other), lines[4][:20]]))
+    calls.clear()
+    _, resumed = t.explore(FakeProblem("p"), space=space, journal=j)
+    assert sorted(calls[1:]) == sorted(t._key(s) for s in space[4:])
+    assert [r["us"] for r in resumed] == [r["us"] for r in full]
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("op,dtype,dims", [
     ("matmul", "f32", (200, 300, 96)),
