@@ -5,6 +5,8 @@
   small-integer inputs make every correct result bit-exact.
 - Random 3x3 stride-1 layers in and around the class of the patch-staging
   conv kernels, through every such instance and the default schedule.
+- A wider seeded sweep over every kind of instance (matmul and conv, both
+  dtypes, narrow and long-reduction shapes, misaligned bf16 operands).
 - Several host threads, each on its own stream, launching different
   contractions at once: the library keeps no state shared between calls, so
   every result must equal its single-threaded one.
@@ -145,6 +147,92 @@ def test_bf16_rows_at_any_two_byte_boundary(x):
                               torch.cuda.current_stream().cuda_stream)
             assert st == 0, x.xtc_status_str(st)
             assert np.array_equal(to_host(Cd), ref), ((M, N, K), (lda, ldb), (oa, ob), s)
+
+
+def test_random_sweep_every_instance_kind(x):
+    """A wider seeded sweep: 240 matmuls (fp32 and bf16, M, N, K up to 700,
+    every eighth with at most 32 columns, every eleventh with K up to 3000),
+    each through a random compiled instance or the default schedule with a
+    random raster order, XCD remap and relu flag, padded leading dimensions,
+    NaN around the operands and, for bf16, a base pointer 0-7 elements past a
+    16-byte boundary; and 60 convolutions (3x3 stride-1 layers of about 56
+    pixels every third case, else small random 1x1/3x3/5x5 layers with
+    stride 1 or 2), each through a random instance.  Small-integer inputs:
+    every result is bit-exact."""
+    import torch
+    rng = np.random.default_rng(424242)
+    for case in range(240):
+        dt = ("f32", "bf16")[case % 2]
+        code = x.XTC_F32 if dt == "f32" else x.XTC_BF16
+        scheds = x.xtc_sched_list(x.XTC_OP_MATMUL, code) + [None]
+        M, N, K = (int(v) for v in rng.integers(1, 700, size=3))
+        if case % 8 == 0:
+            N = int(rng.integers(1, 33))
+        if case % 11 == 0:
+            K = int(rng.integers(1, 3000))
+        s = scheds[int(rng.integers(len(scheds)))]
+        if s is not None:
+            s.raster = int(rng.choice([0, 1, 4, 8, 16]))
+            s.xcd_remap = int(rng.integers(2))
+        pa, pb, pc = (int(v) for v in rng.integers(0, 9, size=3))
+        off = int(rng.integers(0, 8)) if dt == "bf16" else 0
+        relu = bool(rng.integers(2))
+        A = xi.small_int_f32(10000 + case, (M, K))
+        B = xi.small_int_f32(20000 + case, (K, N))
+        if dt == "bf16":
+            A, B = xi.f32_to_bf16_bits(A), xi.f32_to_bf16_bits(B)
+        ref = oracle.matmul(A, B)
+        if relu:
+            ref = oracle.relu(ref)
+        lda, ldb, ldc = K + pa, N + pb, N + pc
+
+        def place(arr, ld, o):
+            fill = 0x7FC0 if arr.dtype == np.uint16 else np.nan
+            flat = np.full(o + arr.shape[0] * ld + 16, fill, dtype=arr.dtype)
+            flat[o:o + arr.shape[0] * ld] = _strided(arr, ld).ravel()
+            return to_dev(flat)
+
+        Ad, Bd = place(A, lda, off), place(B, ldb, 0)
+        Cd = torch.full((M, ldc), 7.0, dtype=torch.float32, device="cuda")
+        fn = x.xtc_matmul_relu if relu else x.xtc_matmul
+        say("sweep mm", dt, case, (M, N, K), (lda, ldb, ldc), off, relu, s)
+        st = fn(M, N, K, Ad.data_ptr() + 2 * off, lda, Bd.data_ptr(), ldb, Cd.data_ptr(), ldc,
+                code, s, torch.cuda.current_stream().cuda_stream)
+        assert st == 0, x.xtc_status_str(st)
+        got = to_host(Cd)
+        assert np.array_equal(got[:, :N], ref), (dt, case, (M, N, K), off, relu, s)
+        assert np.all(got[:, N:] == 7.0), "columns past N were written"
+    for case in range(60):
+        dt = ("f32", "bf16")[case % 2]
+        code = x.XTC_F32 if dt == "f32" else x.XTC_BF16
+        scheds = x.xtc_sched_list(x.XTC_OP_CONV2D, code) + [None]
+        n = int(rng.integers(1, 4))
+        C = int(rng.choice([3, 8, 16, 24, 32, 48, 64]))
+        if case % 3 == 0:
+            H, W = (int(v) for v in rng.integers(48, 62, size=2))
+            R, stride = 3, 1
+        else:
+            H, W = (int(v) for v in rng.integers(5, 40, size=2))
+            R, stride = int(rng.choice([1, 3, 5])), int(rng.integers(1, 3))
+        pad = int(rng.integers(0, 3))
+        OC = int(rng.integers(1, 140))
+        if H + 2 * pad < R or W + 2 * pad < R:
+            continue
+        s = scheds[int(rng.integers(len(scheds)))]
+        if s is not None:
+            s.raster = int(rng.choice([0, 1, 8]))
+            s.xcd_remap = int(rng.integers(2))
+        relu = bool(rng.integers(2))
+        X = xi.small_int_f32(30000 + case, (n, C, H, W))
+        Wt = xi.small_int_f32(40000 + case, (OC, C, R, R))
+        if dt == "bf16":
+            X, Wt = xi.f32_to_bf16_bits(X), xi.f32_to_bf16_bits(Wt)
+        ref = oracle.conv2d(X, Wt, stride=stride, pad=pad)
+        if relu:
+            ref = oracle.relu(ref)
+        say("sweep conv", dt, case, (n, C, H, W, OC, R, stride, pad), relu, s)
+        got = to_host(x.conv2d_nchw(to_dev(X), to_dev(Wt), stride=stride, pad=pad, sched=s, relu=relu))
+        assert np.array_equal(got, ref), (dt, case, (n, C, H, W, OC, R, stride, pad), relu, s)
 
 
 def test_concurrent_host_threads_on_separate_streams(x):
