@@ -183,12 +183,14 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     }
     bool mid = false, big = false;
     if (dt == XTC_F32) {
-        // 256x128 tiles, then 128x128, once they give two tiles per CU; 64x64 tiles of the
-        // same direct-to-LDS kernel down to half a tile per CU (these won
-        // from 512x1024x128 to 2048^3); below that, the largest
-        // reduction-split tile that still gives one tile per CU (measured
-        // over 16x16 .. 128x128 tiles on shapes from 256^3 to 4096^3 and
-        // skinny ones such as 128x128x4096 and 64x4096x1024).
+        // Direct-to-LDS tiles from 256x256 (a tile per CU) through 256x128
+        // and 128x128 (two tiles per CU); the reduction-split kernels for
+        // long reductions with a narrow operand; 64x64 direct-to-LDS tiles
+        // down to half a tile per CU (these won from 512x1024x128 to
+        // 2048^3); below that, the largest reduction-split tile that still
+        // gives one tile per CU (measured over 16x16 .. 128x128 tiles on
+        // shapes from 256^3 to 4096^3 and skinny ones such as 128x128x4096
+        // and 64x4096x1024).
         if (tiles(256, 256) >= cus) {
             // eight 128x64 waves, one workgroup per CU: half the copy
             // traffic per FLOP of 256x128 tiles (4096^3: 141.3 -> 145.3
