@@ -1101,112 +1101,124 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
         so_b += b_stage;
     };
 
-    // Fragment bases.  A: output channel 16*wq + lcol, channel lgrp (+4s).
-    // B: pixel pw0 + 16j + lcol of the patch (clamped to position 0 past the
-    // tile; such columns are not stored), channel plane lgrp (+4s).
-    const int a_base = ((wq * 16 + lcol) * CC + lgrp) * 4;
-    const int pw0 = p0 + 16 * NB * half;     // first pixel of this wave's half
-    int b_base[NB];
+    // The waves of the second half run NB - 1 column blocks when the tile's
+    // second half fits in them (PT <= 16 * (2 * NB - 1) pixels, 392 for
+    // 56 x 56 images): on each SIMD, which holds one wave of each half, that
+    // is 25 instead of 26 blocks of MFMAs.  Each instance runs the same copy
+    // and barrier sequence.
+    auto body = [&](auto nbc) __attribute__((always_inline)) {
+        constexpr int NBW = decltype(nbc)::value;
+        // Fragment bases.  A: output channel 16*wq + lcol, channel lgrp (+4s).
+        // B: pixel pw0 + 16j + lcol of the patch (clamped to position 0 past the
+        // tile; such columns are not stored), channel plane lgrp (+4s).
+        const int a_base = ((wq * 16 + lcol) * CC + lgrp) * 4;
+        const int pw0 = p0 + 16 * NB * half;     // first pixel of this wave's half
+        int b_base[NBW];
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-        const int pix = pw0 + 16 * j + lcol;
-        int off = 0;
-        if (pix < pend) {
-            const int oh = pix / OW, ow = pix - oh * OW;
-            off = (oh - oh0) * 64 + ow - p.pw + CO;
+        for (int j = 0; j < NBW; ++j) {
+            const int pix = pw0 + 16 * j + lcol;
+            int off = 0;
+            if (pix < pend) {
+                const int oh = pix / OW, ow = pix - oh * OW;
+                off = (oh - oh0) * 64 + ow - p.pw + CO;
+            }
+            b_base[j] = (lgrp * PLANE + off) * 4;
         }
-        b_base[j] = (lgrp * PLANE + off) * 4;
-    }
 
-    typename MF::acc_t acc[NB];
+        typename MF::acc_t acc[NBW];
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
+        for (int j = 0; j < NBW; ++j)
 #pragma unroll
-        for (int r = 0; r < MF::NACC; ++r) acc[j][r] = 0.f;
+            for (int r = 0; r < MF::NACC; ++r) acc[j][r] = 0.f;
 
-    float af[2], bfr[2][NB];
-    // k-step t of a stage: tap t / 2, channels 4 * (t % 2) .. + 3
-    auto load_frags = [&](int st, int t, int buf) __attribute__((always_inline)) {
-        const unsigned char *As = smem + st * STAGE_BYTES;
-        const unsigned char *Bs = As + A_BYTES;
-        const int tap = t >> 1, s = t & 1;
-        const int kh = tap / 3, kw = tap - 3 * kh;
-        af[buf] = *reinterpret_cast<const float *>(As + a_base + (tap * BM * CC + 4 * s) * 4);
+        float af[2], bfr[2][NBW];
+        // k-step t of a stage: tap t / 2, channels 4 * (t % 2) .. + 3
+        auto load_frags = [&](int st, int t, int buf) __attribute__((always_inline)) {
+            const unsigned char *As = smem + st * STAGE_BYTES;
+            const unsigned char *Bs = As + A_BYTES;
+            const int tap = t >> 1, s = t & 1;
+            const int kh = tap / 3, kw = tap - 3 * kh;
+            af[buf] = *reinterpret_cast<const float *>(As + a_base + (tap * BM * CC + 4 * s) * 4);
 #pragma unroll
-        for (int j = 0; j < NB; ++j)
-            bfr[buf][j] = *reinterpret_cast<const float *>(Bs + b_base[j] + (4 * s * PLANE + kh * 64 + kw) * 4);
-    };
-    auto mfmas = [&](int buf) __attribute__((always_inline)) {
+            for (int j = 0; j < NBW; ++j)
+                bfr[buf][j] = *reinterpret_cast<const float *>(Bs + b_base[j] + (4 * s * PLANE + kh * 64 + kw) * 4);
+        };
+        auto mfmas = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < NB; ++j) acc[j] = MF::mma(af[buf], bfr[buf][j], acc[j]);
-    };
-    // K-step t of the stage in slot st, one MFMA at a time, each followed by
-    // one fragment read of k-step t + 1 and its share of the copies of the
-    // next stage into slot nx.  A stage's copies are spread over its first
-    // CSTEPS k-steps: issued together, the copies of all waves would queue at
-    // the texture unit and stall the issuing waves.  The fences keep the
-    // order (and keep the compiler from hoisting the reads).
-    static_assert(STAGES == 2, "the next stage is copied into the other slot of a two-slot ring");
-    constexpr int CSTEPS = 12;
-    auto step = [&](int st, auto tc, int nx) __attribute__((always_inline)) {
-        constexpr int t = decltype(tc)::value;   // a constant: the copy split is fixed per k-step
-        const int cur = t & 1, nxt = (t + 1) & 1;
-        const unsigned char *As = smem + st * STAGE_BYTES;
-        const unsigned char *Bs = As + A_BYTES;
-        const int tap = (t + 1) >> 1, s = (t + 1) & 1;
-        const int kh = tap / 3, kw = tap - 3 * kh;
-        constexpr int q0 = t < CSTEPS ? t * LOADS / CSTEPS : LOADS;
-        constexpr int q1 = t < CSTEPS ? (t + 1) * LOADS / CSTEPS : LOADS;
+            for (int j = 0; j < NBW; ++j) acc[j] = MF::mma(af[buf], bfr[buf][j], acc[j]);
+        };
+        // K-step t of the stage in slot st, one MFMA at a time, each followed by
+        // one fragment read of k-step t + 1 and its share of the copies of the
+        // next stage into slot nx.  A stage's copies are spread over its first
+        // CSTEPS k-steps: issued together, the copies of all waves would queue at
+        // the texture unit and stall the issuing waves.  The fences keep the
+        // order (and keep the compiler from hoisting the reads).
+        static_assert(STAGES == 2, "the next stage is copied into the other slot of a two-slot ring");
+        constexpr int CSTEPS = 12;
+        auto step = [&](int st, auto tc, int nx) __attribute__((always_inline)) {
+            constexpr int t = decltype(tc)::value;   // a constant: the copy split is fixed per k-step
+            const int cur = t & 1, nxt = (t + 1) & 1;
+            const unsigned char *As = smem + st * STAGE_BYTES;
+            const unsigned char *Bs = As + A_BYTES;
+            const int tap = (t + 1) >> 1, s = (t + 1) & 1;
+            const int kh = tap / 3, kw = tap - 3 * kh;
+            constexpr int q0 = t < CSTEPS ? t * LOADS / CSTEPS : LOADS;
+            constexpr int q1 = t < CSTEPS ? (t + 1) * LOADS / CSTEPS : LOADS;
 #pragma unroll
-        for (int m = 0; m < NB; ++m) {
-            acc[m] = MF::mma(af[cur], bfr[cur][m], acc[m]);
-            if (m == 0)
-                af[nxt] = *reinterpret_cast<const float *>(As + a_base + (tap * BM * CC + 4 * s) * 4);
-            bfr[nxt][m] =
-                *reinterpret_cast<const float *>(Bs + b_base[m] + (4 * s * PLANE + kh * 64 + kw) * 4);
+            for (int m = 0; m < NBW; ++m) {
+                acc[m] = MF::mma(af[cur], bfr[cur][m], acc[m]);
+                if (m == 0)
+                    af[nxt] = *reinterpret_cast<const float *>(As + a_base + (tap * BM * CC + 4 * s) * 4);
+                bfr[nxt][m] =
+                    *reinterpret_cast<const float *>(Bs + b_base[m] + (4 * s * PLANE + kh * 64 + kw) * 4);
 #pragma unroll
-            for (int q = q0 + m * (q1 - q0) / NB; q < q0 + (m + 1) * (q1 - q0) / NB; ++q) copy(nx, q);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
+                for (int q = q0 + m * (q1 - q0) / NBW; q < q0 + (m + 1) * (q1 - q0) / NBW; ++q) copy(nx, q);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
 
-    // Stage 0 into slot 0; then every iteration computes stage kt from slot
-    // kt % 2 while copying stage kt + 1 into the other slot (stages past the
-    // end read in range or zero and are never used).
+        // Stage 0 into slot 0; then every iteration computes stage kt from slot
+        // kt % 2 while copying stage kt + 1 into the other slot (stages past the
+        // end read in range or zero and are never used).
 #pragma unroll
-    for (int q = 0; q < LOADS; ++q) copy(0, q);
-    advance();
-    wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    load_frags(0, 0, 0);
-    for (int kt = 0; kt < KT; ++kt) {
-        const int st = kt & 1, nx = st ^ 1;
-        each_index([&](auto tc) __attribute__((always_inline)) { step(st, tc, nx); },
-                   std::make_integer_sequence<int, NSTEP - 1>());
+        for (int q = 0; q < LOADS; ++q) copy(0, q);
         advance();
-        // this wave's copies of stage kt + 1 have landed, then everyone's; every
-        // wave has also issued its last read of slot st (k-step NSTEP - 1's
-        // fragments, now in registers)
-        wait_vmcnt_and_lds<0>();
+        wait_vmcnt<0>();
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        load_frags(nx, 0, 0);
-        mfmas((NSTEP - 1) & 1);
-    }
-    wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
-
-    float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-        const int pix = pw0 + 16 * j + lcol;
-        if (pix >= pend) continue;
-#pragma unroll
-        for (int r = 0; r < MF::NACC; ++r) {
-            const int oc = m0 + 16 * wq + MF::row(lane, r);
-            if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[j][r] < 0.f) ? 0.f : acc[j][r];
+        load_frags(0, 0, 0);
+        for (int kt = 0; kt < KT; ++kt) {
+            const int st = kt & 1, nx = st ^ 1;
+            each_index([&](auto tc) __attribute__((always_inline)) { step(st, tc, nx); },
+                       std::make_integer_sequence<int, NSTEP - 1>());
+            advance();
+            // this wave's copies of stage kt + 1 have landed, then everyone's; every
+            // wave has also issued its last read of slot st (k-step NSTEP - 1's
+            // fragments, now in registers)
+            wait_vmcnt_and_lds<0>();
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            load_frags(nx, 0, 0);
+            mfmas((NSTEP - 1) & 1);
         }
-    }
+        wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
+
+        float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
+#pragma unroll
+        for (int j = 0; j < NBW; ++j) {
+            const int pix = pw0 + 16 * j + lcol;
+            if (pix >= pend) continue;
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) {
+                const int oc = m0 + 16 * wq + MF::row(lane, r);
+                if (oc < OC) Y[oc * OHW + pix] = (p.relu && acc[j][r] < 0.f) ? 0.f : acc[j][r];
+            }
+        }
+    };
+    if (NH == 2 && half == 1 && PT <= 16 * (2 * NB - 1))
+        body(std::integral_constant<int, NB - 1>());
+    else
+        body(std::integral_constant<int, NB>());
 }
 
 // Shapes the halo kernel covers; anything else runs the tap-major kernel

@@ -151,6 +151,9 @@ def test_small_int_exact_every_instance(x, dtype, M, N, K):
     (1, 16, 57, 55, 20, 3, 3, 1, 0),    # halo: no padding (53 x 55 output)
     (1, 48, 56, 56, 16, 3, 3, 1, 2),    # halo: pad 2 (58-wide output rows), six stages
     (1, 24, 56, 56, 64, 3, 3, 1, 1),    # balanced halo: 8-channel stages, odd stage count
+    (1, 8, 61, 59, 64, 3, 3, 1, 1),     # balanced halo: 400-pixel tiles, second half 12 blocks
+    (1, 8, 69, 58, 64, 3, 3, 1, 1),     # balanced halo: 401-pixel tiles, second half 13 blocks
+    (2, 8, 7, 57, 48, 3, 3, 1, 1),      # balanced halo: 399-pixel tiles, one tile per image
 ])
 def test_conv_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape
