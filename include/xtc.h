@@ -28,8 +28,11 @@
  *   synchronisation on that stream, not in the return value.
  * - The return value is the only error channel.
  * - Element offsets are 32-bit inside the kernels: every operand's span
- *   (bytes from its first to its last addressed element) must be < 2^31,
- *   else XTC_ERR_TOO_LARGE.
+ *   (bytes from its first to its last addressed element) must be at most
+ *   0x7FFFFFD0 bytes (2^31 - 48), else XTC_ERR_TOO_LARGE.  Elements
+ *   outside an operand (ragged edges, zero padding) are read through a
+ *   buffer offset of 0x7FFFFFF0, which this limit keeps past every operand,
+ *   so they read as zero.
  */
 #ifndef XTC_H
 #define XTC_H
@@ -54,7 +57,9 @@ typedef enum {
     XTC_ERR_BAD_DTYPE = 4,            /* unknown dtype, or not supported here */
     XTC_ERR_BAD_SCHEDULE = 5,         /* illegal field values / combination   */
     XTC_ERR_UNSUPPORTED_SCHEDULE = 6, /* legal but not among compiled ones    */
-    XTC_ERR_TOO_LARGE = 7,            /* an operand span is >= 2^31 bytes     */
+    XTC_ERR_TOO_LARGE = 7,            /* an operand span above 0x7FFFFFD0     */
+                                      /* bytes, or a conv stride/pad/extent   */
+                                      /* above 2^30                           */
     XTC_ERR_HIP = 8,                  /* a HIP call failed (see below)        */
     XTC_ERR_MISALIGNED = 9            /* a tensor pointer is not aligned to   */
                                       /* its element size                     */
@@ -76,14 +81,16 @@ typedef enum {
  *                (block_m/wave_m)*(block_n/wave_n) waves.
  *  mfma_m/n/k    matrix-core instruction tile (the vectorize primitive):
  *                fp32: 32x32x2 or 16x16x4; bf16: 32x32x16 or 16x16x32.
- *  lds_stages    LDS buffers per operand (pack + software pipelining), 1-4;
+ *  lds_stages    LDS buffers per operand (pack + software pipelining), 1-5;
  *                0 = no LDS staging (the k_split kernels).
  *  lds_pad       LDS row padding in elements (pack with padding against bank
  *                conflicts); -1 selects an XOR-swizzled layout instead.
  *  unroll_k      MFMA k-steps unrolled per LDS stage (0 = the whole stage).
  *  raster        order of the parallel tile loops (interchange): 0 row-major
- *                (N fastest), 1 column-major (M fastest), g >= 2 grouped:
- *                bands of g tile-rows, walked column by column.
+ *                (N fastest), 1 column-major (M fastest), 2 <= g <= 64
+ *                grouped: bands of g tile-rows, walked column by column (a
+ *                band taller than the tile grid is the whole grid).  Values
+ *                outside 0..64 are XTC_ERR_BAD_SCHEDULE.
  *  xcd_remap     1: renumber workgroups so that each of the 8 XCDs (which
  *                receive workgroups round-robin and each own an L2) works on
  *                one contiguous band of the tile order; 0: hardware order.
@@ -185,6 +192,9 @@ xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K,
  *  X, Wt and Y are aligned to their element size (else XTC_ERR_MISALIGNED).
  *  N, C, H, W, OC, R, S >= 1 except that N == 0 or OC == 0 is a no-op;
  *  stride >= 1, pad >= 0, OH >= 1 and OW >= 1, else XTC_ERR_BAD_SHAPE.
+ *  stride_h, stride_w, pad_h, pad_w, H, W, H + 2*pad_h and W + 2*pad_w are
+ *  at most 2^30 (input coordinates stay in 32-bit arithmetic), else
+ *  XTC_ERR_TOO_LARGE.
  *  dtype XTC_F32 or XTC_BF16 (else XTC_ERR_BAD_DTYPE); the bf16 kernels
  *  reduce in OIHW order (k_order 0).
  *  sched NULL selects the default conv schedule.
@@ -234,21 +244,33 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dtype,
 /*
  * xtc_sched_check -- XTC_OK if `s` can run op/dtype: its fields are legal
  * (XTC_ERR_BAD_SCHEDULE otherwise) and they name a compiled instance
- * (XTC_ERR_UNSUPPORTED_SCHEDULE otherwise).  Pure host function.
+ * (XTC_ERR_UNSUPPORTED_SCHEDULE otherwise).  This is the membership test of
+ * the design space a scheduling strategy samples from (Sec. 5.2: a strategy
+ * defines a design space over a scheduling template and turns a sample into
+ * a schedule); the fields are the primitives of Table 1 (Sec. 3.2).
+ * Pure host function; `s` is only read.  Errors: XTC_ERR_NULL_POINTER (s
+ * NULL), XTC_ERR_BAD_DTYPE, XTC_ERR_BAD_SCHEDULE (also an unknown op),
+ * XTC_ERR_UNSUPPORTED_SCHEDULE.
  */
 xtc_status xtc_sched_check(xtc_op op, xtc_dtype dtype, const xtc_sched *s);
 
 /*
- * xtc_sched_list -- writes up to `cap` compiled schedules for op/dtype into
- * `out` (raster = 0, xcd_remap = 1) and returns how many exist in total
- * (call with cap = 0 to size the array).  Returns -1 for an unknown
- * op/dtype.  Pure host function.
+ * xtc_sched_list -- the compiled part of the design space (Sec. 5.2: the
+ * grid a strategy samples from): writes up to `cap` compiled schedules for
+ * op/dtype into the caller-owned array `out` (may be NULL when cap is 0;
+ * each entry has raster = 0, xcd_remap = 1) and returns how many exist in
+ * total (call with cap = 0 to size the array).  Combined with every raster
+ * and xcd_remap value they span the schedules an exploration can sample.
+ * Returns -1 for an unknown op/dtype.  Pure host function.
  */
 int32_t xtc_sched_list(xtc_op op, xtc_dtype dtype, xtc_sched *out, int32_t cap);
 
 /*
  * xtc_sched_occupancy -- how many workgroups of the kernel instance `s`
- * names one CU holds at once (the hardware limit set by the kernel's
+ * names one CU holds at once (an input of the per-schedule traffic model
+ * evaluated against hardware counters, the GPU form of the cache-model
+ * study of Sec. 6.3: the tiles resident together decide what the caches
+ * share) (the hardware limit set by the kernel's
  * registers, LDS and threads), for reduction length K (matmul: K; conv2d:
  * C*R*S, which sizes the conv kernels' LDS k-offset table).  For a conv
  * tap-major instance the figure is that of the tap-major kernel itself, not
@@ -261,17 +283,35 @@ int32_t xtc_sched_list(xtc_op op, xtc_dtype dtype, xtc_sched *out, int32_t cap);
 xtc_status xtc_sched_occupancy(xtc_op op, xtc_dtype dtype, int64_t K,
                                const xtc_sched *s, int32_t *wg_per_cu);
 
-/* Static description of a status code. */
+/*
+ * xtc_status_str -- static, NUL-terminated description of a status code, for
+ * the harness that reports why a generated operator could not run (Sec. 4.2:
+ * the Executor validates results, the Evaluator runs the code and collects
+ * metrics).  Never NULL ("unknown status" for a value outside the enum); the
+ * string is owned by the library and must not be freed.
+ */
 const char *xtc_status_str(xtc_status s);
 
-/* hipError_t value of the last failed HIP call made by this thread inside
- * the library (0 if none). */
+/*
+ * xtc_last_hip_error -- hipError_t value of the last failed HIP call made by
+ * this thread inside the library, 0 if none (the detail behind XTC_ERR_HIP,
+ * for the harness of Sec. 4.2).  Thread-local; not reset by later
+ * successful calls.
+ */
 int32_t xtc_last_hip_error(void);
 
-/* Largest C*R*S accepted by xtc_conv2d_nchw. */
+/*
+ * xtc_conv_max_k -- largest reduction length C*R*S that xtc_conv2d_nchw
+ * accepts (the capacity of the conv kernels' k-offset table; the conv2d
+ * operator of Sec. 3.1 lowered to an implicit GEMM).  Pure host function.
+ */
 int64_t xtc_conv_max_k(void);
 
-/* Library version: major*10000 + minor*100 + patch. */
+/*
+ * xtc_version -- library version, major*10000 + minor*100 + patch, so that a
+ * caller loading the module (Sec. 4.1, "Module": a shared library loaded at
+ * run time) can check the ABI it binds to.  Pure host function.
+ */
 int32_t xtc_version(void);
 
 #ifdef __cplusplus

@@ -39,34 +39,10 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-PROBES = os.path.join(HERE, "probes")
-
-
-def build_probes(verbose: bool = False) -> list:
-    """Standalone measurement programs next to their sources (not part of the
-    library): probes/mfma_ceiling, the matrix cores' sustained rate with no
-    memory traffic."""
-    out = []
-    for src in sorted(os.listdir(PROBES)):
-        if not src.endswith(".hip"):
-            continue
-        exe = os.path.join(PROBES, os.path.splitext(src)[0])
-        cmd = [HIPCC] + FLAGS + [os.path.join(PROBES, src), "-o", exe]
-        if verbose:
-            print(" ".join(cmd), flush=True)
-        r = subprocess.run(cmd, capture_output=True, text=True)
-        if r.returncode != 0:
-            raise RuntimeError("hipcc failed for %s:\n%s%s" % (src, r.stdout, r.stderr))
-        out.append(exe)
-    return out
-
-
 def build(verbose: bool = False) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
-    with ThreadPoolExecutor(min(len(SOURCES) + 1, os.cpu_count() or 1)) as ex:
-        probes = ex.submit(build_probes, verbose)
+    with ThreadPoolExecutor(min(len(SOURCES), os.cpu_count() or 1)) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-        probes.result()
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:

@@ -28,11 +28,14 @@ __device__ __forceinline__ void tile_coords(int bid, int G, int tiles_m, int til
         tm = bid % tiles_m;
         tn = bid / tiles_m;
     } else if (raster >= 2) {
-        const int per = raster * tiles_n;
+        // a group taller than the grid is the whole grid (also keeps
+        // raster * tiles_n within the tile count)
+        const int rg = raster < tiles_m ? raster : tiles_m;
+        const int per = rg * tiles_n;
         const int grp = bid / per;
-        const int first = grp * raster;
+        const int first = grp * rg;
         const int left = tiles_m - first;
-        const int gsz = left < raster ? left : raster;
+        const int gsz = left < rg ? left : rg;
         const int r = bid - grp * per;
         tm = first + r % gsz;
         tn = r / gsz;

@@ -11,7 +11,17 @@ using namespace xtc;
 
 thread_local int32_t g_last_hip_error = 0;
 
-constexpr int64_t kMaxSpan = (int64_t(1) << 31) - 1;  // bytes; kernels use 32-bit offsets
+// Largest operand span in bytes.  Kernels use 32-bit buffer offsets, and
+// an element outside an operand is read through the offset kOOB
+// (0x7FFFFFF0): the span stays 32 bytes below it, so that offset (plus a
+// 16-byte chunk, plus the 16-byte alignment slack of the shifted bf16 loads)
+// always lies past the operand's buffer range and reads zero.
+constexpr int64_t kMaxSpan = 0x7FFFFFF0 - 32;
+// Largest raster group; the kernels also clamp it to the tile rows.
+constexpr int kMaxRaster = 64;
+// Largest stride or padding, and padded extent, of a convolution: keeps
+// every input coordinate oh*stride - pad + kh within 32-bit arithmetic.
+constexpr int64_t kMaxConvExtent = int64_t(1) << 30;
 constexpr int kLdsBytes = 160 * 1024;                  // LDS per CU on gfx950
 
 // Bytes from the first to one past the last addressed element of a
@@ -67,10 +77,11 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     const int kchunk = (op == XTC_OP_CONV2D && s.k_order == 2) ? s.mfma_k
                        : dt == XTC_F32 ? 4 * (64 / s.mfma_m) : s.mfma_k;
     if (s.block_k % kchunk) return XTC_ERR_BAD_SCHEDULE;
-    if (s.lds_stages < (s.k_split > 1 ? 0 : 1) || s.lds_stages > 4) return XTC_ERR_BAD_SCHEDULE;
+    if (s.lds_stages < (s.k_split > 1 ? 0 : 1) || s.lds_stages > 5) return XTC_ERR_BAD_SCHEDULE;
     if (s.lds_pad < -1 || s.lds_pad > 64) return XTC_ERR_BAD_SCHEDULE;
     if (s.unroll_k < 0) return XTC_ERR_BAD_SCHEDULE;
-    if (s.raster < 0 || s.xcd_remap < 0 || s.xcd_remap > 1) return XTC_ERR_BAD_SCHEDULE;
+    if (s.raster < 0 || s.raster > kMaxRaster || s.xcd_remap < 0 || s.xcd_remap > 1)
+        return XTC_ERR_BAD_SCHEDULE;
     if (s.k_order < 0 || s.k_order > 2 || (op == XTC_OP_MATMUL && s.k_order != 0))
         return XTC_ERR_BAD_SCHEDULE;
     // LDS budget of the staged tiles
@@ -359,6 +370,10 @@ xtc_status conv_impl(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int
     if (N < 0 || OC < 0 || C < 1 || H < 1 || W < 1 || R < 1 || S < 1 || stride_h < 1 ||
         stride_w < 1 || pad_h < 0 || pad_w < 0)
         return XTC_ERR_BAD_SHAPE;
+    if (stride_h > kMaxConvExtent || stride_w > kMaxConvExtent || pad_h > kMaxConvExtent ||
+        pad_w > kMaxConvExtent || H > kMaxConvExtent || W > kMaxConvExtent ||
+        H + 2 * pad_h > kMaxConvExtent || W + 2 * pad_w > kMaxConvExtent)
+        return XTC_ERR_TOO_LARGE;
     if (H + 2 * pad_h < R || W + 2 * pad_w < S) return XTC_ERR_BAD_SHAPE;
     const int64_t OH = (H + 2 * pad_h - R) / stride_h + 1;
     const int64_t OW = (W + 2 * pad_w - S) / stride_w + 1;

@@ -68,6 +68,7 @@ BAD = 0x10  # a dummy non-NULL pointer: dereferencing it would fault
     ((4, 4, 4, BAD, 4, BAD, 4, 0, 4, 0), 1),             # C NULL
     ((1 << 16, 1 << 15, 1 << 15, BAD, 1 << 15, BAD, 1 << 15, BAD, 1 << 15, 0), 7),  # span >= 2^31
     ((3, 3, 1 << 30, BAD, 1 << 30, BAD, 3, BAD, 3, 1), 7),
+    ((1, 1, 0x1FFFFFF5, BAD, 0x1FFFFFF5, BAD, 1, BAD, 1, 0), 7),  # span 0x7FFFFFD4 > 0x7FFFFFD0
     ((4, 4, 4, BAD + 2, 4, BAD, 4, BAD, 4, 0), 9),       # fp32 A on a 2-byte boundary
     ((4, 4, 4, BAD, 4, BAD + 1, 4, BAD, 4, 1), 9),       # bf16 B on an odd byte
     ((4, 4, 4, BAD, 4, BAD, 4, BAD + 2, 4, 1), 9),       # C (fp32) on a 2-byte boundary
@@ -99,6 +100,13 @@ def test_matmul_empty_is_noop(x):
     ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD + 2, BAD, BAD, 0), 9),  # fp32 X on a 2-byte boundary
     ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD + 1, BAD, 1), 9),  # bf16 W on an odd byte
     ((1, 3, 8, 8, 4, 3, 3, 1, 1, 1, 1, BAD, BAD, BAD + 2, 1), 9),  # Y on a 2-byte boundary
+    # strides, pads and padded extents above 2^30 (coordinates must stay in
+    # 32-bit arithmetic): a stride of 2^34 and a pad of 2^32 on a 3x3 input
+    # would give OH = 1 and pass every other check
+    ((1, 1, 3, 3, 1, 3, 3, 1 << 34, 1, 1 << 32, 0, BAD, BAD, BAD, 0), 7),
+    ((1, 1, 3, 3, 1, 3, 3, 1, 1 << 31, 0, 0, BAD, BAD, BAD, 0), 7),
+    ((1, 1, 3, 3, 1, 3, 3, 1, 1, 0, (1 << 30) + 1, BAD, BAD, BAD, 0), 7),
+    ((1, 1, 3, 3, 1, 3, 3, 1, 1, 1 << 29, 0, BAD, BAD, BAD, 0), 7),   # H + 2*pad_h > 2^30
 ])
 def test_conv_validation(x, args, expected):
     assert x.xtc_conv2d_nchw(*args) == expected
@@ -131,6 +139,7 @@ def _base(x, dt=0):
 @pytest.mark.parametrize("field,value", [
     ("block_m", 96), ("block_n", 0), ("wave_m", 512), ("mfma_m", 8), ("mfma_k", 16),
     ("lds_stages", 0), ("lds_pad", -2), ("raster", -1), ("xcd_remap", 2), ("block_k", 4),
+    ("raster", 65), ("raster", 1 << 28), ("raster", 2**31 - 1),
     ("size", 12), ("k_order", 1), ("k_order", -1), ("k_split", 0), ("k_split", 3),
     ("k_split", 16),
 ])

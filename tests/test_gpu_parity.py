@@ -137,6 +137,57 @@ def test_small_int_exact_every_instance(x, dtype, M, N, K):
             assert np.array_equal(got, ref), "%s %s: not bit-exact" % (dtype, s)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_large_tiles_exact_at_scale(x, dtype):
+    """Every instance with 128- or 256-wide tiles on 2048 x 2048 x 4096 small
+    integers (exact in fp32 for any summation order): many full interior
+    tiles, every CU busy, and 64 to 128 turns of the LDS ring, compared with
+    the oracle element by element."""
+    M, N, K = 2048, 2048, 4096
+    A, B = _prep(xi.small_int_f32(31, (M, K)), xi.small_int_f32(32, (K, N)), dtype)
+    ref = oracle.matmul(A, B)
+    code = x.XTC_F32 if dtype == "f32" else x.XTC_BF16
+    n = 0
+    for s in x.xtc_sched_list(x.XTC_OP_MATMUL, code):
+        if s.block_m < 128 or s.block_n < 128:
+            continue
+        for raster, xcd in ((1, 0), (4, 1)):
+            s.raster, s.xcd_remap = raster, xcd
+            say(dtype, (M, N, K), s)
+            got = _run_mm(x, A, B, sched=s)
+            bad = np.argwhere(got != ref)
+            assert bad.size == 0, "%s %s: %d outputs differ, first at %s" % (
+                dtype, s, len(bad), tuple(bad[0]))
+        n += 1
+    assert n >= 3
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [
+    # N, C, H, W, OC, R, S, (stride_h, stride_w), (pad_h, pad_w)
+    (2, 16, 13, 17, 20, 3, 3, (1, 1), (1, 2)),      # pad_h != pad_w
+    (2, 8, 15, 16, 24, 3, 3, (1, 2), (1, 1)),       # stride_h != stride_w
+    (1, 12, 14, 13, 17, 3, 5, (1, 1), (1, 2)),      # R != S
+    (1, 32, 11, 12, 40, 5, 3, (2, 1), (2, 0)),      # R != S, both asymmetric, tap-major fp32
+    (1, 16, 20, 57, 64, 3, 3, (1, 1), (1, 3)),      # halo kernels: pad_w 3, W + pad_w = 60
+    (1, 16, 19, 56, 64, 3, 3, (1, 1), (2, 4)),      # halo kernels: pad_w 4, W + pad_w = 60
+    (1, 32, 18, 56, 64, 3, 3, (1, 1), (0, 2)),      # halo: pad_h 0, pad_w 2
+])
+def test_conv_asymmetric_exact_every_instance(x, dtype, shape):
+    N, C, H, W_, OC, R, S, stride, pad = shape
+    X = xi.small_int_f32(41, (N, C, H, W_))
+    W = xi.small_int_f32(42, (OC, C, R, S))
+    if dtype == "bf16":
+        X, W = _bits(X), _bits(W)
+    ref = oracle.conv2d(X, W, stride=stride, pad=pad)
+    code = x.XTC_F32 if dtype == "f32" else x.XTC_BF16
+    for s in x.xtc_sched_list(x.XTC_OP_CONV2D, code) + [None]:
+        say("conv asym", dtype, shape, s)
+        got = to_host(x.conv2d_nchw(to_dev(X), to_dev(W), stride=stride, pad=pad, sched=s))
+        assert got.shape == ref.shape
+        assert np.array_equal(got, ref), "conv %s %s %s: not bit-exact" % (dtype, shape, s)
+
+
 @pytest.mark.parametrize("shape", [
     (3, 5, 13, 11, 7, 3, 3, 1, 1),      # C*R*S = 45: not a multiple of 4 (register-staged path)
     (2, 8, 17, 19, 70, 3, 3, 1, 1),     # C*R*S = 72, OC = 70: ragged weight rows, pixel tail

@@ -178,6 +178,11 @@ def test_conv_hand_worked(name):
     (2, 2, 11, 10, 5, 5, 3, 1, 2),
     (1, 3, 16, 16, 4, 7, 7, 2, 3),   # the paper's 7x7 stride-2 shape, scaled down
     (3, 4, 5, 6, 2, 1, 1, 1, 0),
+    # separate vertical/horizontal strides and pads, R != S: a swap of
+    # (stride_h, stride_w), (pad_h, pad_w) or (R, S) changes every output
+    (1, 3, 9, 11, 4, 3, 5, (1, 2), (2, 1)),
+    (2, 2, 10, 7, 3, 5, 3, (2, 1), (0, 2)),
+    (1, 4, 8, 12, 2, 1, 3, (3, 1), (1, 0)),
 ])
 def test_conv_vs_torch_float64(N, C, H, W, OC, R, S, stride, pad):
     X = xi.uniform_f32(91, (N, C, H, W))
