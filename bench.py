@@ -4,22 +4,29 @@ A step is one launch of the contraction on the headline workload: the fp32
 matmul M = N = K = 4096 (row-major, uniform [-1, 1) inputs from a fixed seed,
 already resident in HBM).  ``value`` is its TFLOP/s (2*M*N*K per launch over
 the HIP-event time of exactly ``--steps`` launches, after ``--warmup``
-untimed ones).  The same line also reports, timed the same way, the bf16
-matmul 8192^3 (fp32 accumulate and output) and the fp32 conv2d 32x64x56x56
--> 64, 3x3, stride 1, pad 1 as an implicit GEMM (also with bf16 inputs), each
-with its roofline (the matrix-core peak, or HBM bandwidth for workloads below
-the ridge point, such as the bf16 conv and the tall-skinny fp32 matmul
-32768x16x4096 that measures the HBM streaming rate); the paper's other,
-smaller workloads (matmuls
-1024^3, [512,128]x[128,1024], matmul+relu [256,128]x[128,1024], 256x258x512,
-and the 7x7 stride-2 conv2d 3 -> 16 channels at 224x224), timed as replays of
-a HIP graph of launches; and the fp64 CPU oracle timed on the host cores on a
-bounded sample of the headline workload (``cpu_baseline``), which also checks
-sampled outputs of every timed launch (every output of the small workloads)
-against the oracle.
+untimed ones, extended to at least 100 ms of launches); ``median_TFLOP/s``
+is the per-launch median of further launches, each between its own events.
+
+The same line also reports, under ``also``:
+- timed the same way: the bf16 matmul 8192^3 (fp32 accumulate and output),
+  the fp32 conv2d 32x64x56x56 -> 64, 3x3, stride 1, pad 1 as an implicit GEMM
+  (also with bf16 inputs) and the tall-skinny fp32 matmul 32768x16x4096 that
+  measures the HBM streaming rate, each with its roofline (the matrix-core
+  peak, or HBM bandwidth below the ridge point);
+- replayed as HIP graphs of 50 launches: the two small synthetic matmuls
+  (fp32 256^3 and the ragged 1000^3) and the paper's other workloads
+  (matmuls 1024^3, [512,128]x[128,1024], matmul+relu [256,128]x[128,1024],
+  256x258x512, and the 7x7 stride-2 conv2d 3 -> 16 channels at 224x224).
+
+``cpu_baseline`` is the fp64 oracle on the host cores: the full 4096^3
+product (``value``), and per workload the full oracle where its projected
+time allows, else leading row slabs scaled to the whole product.  The full
+products check every output of the timed GPU launches; ``parity`` also holds
+the 4096 seeded sampled checks of the large workloads.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--only fp32,bf16,conv,conv_bf16,skinny,paper] [--no-cpu-baseline]
+                       [--only fp32,bf16,conv,conv_bf16,skinny,small,paper]
+                       [--no-cpu-baseline] [--cpu-budget S]
 """
 from __future__ import annotations
 
@@ -82,15 +89,25 @@ def to_dev(arr):
     return torch.from_numpy(np.ascontiguousarray(arr)).cuda()
 
 
-def time_launches(fn, steps: int, warmup: int):
-    """Run ``warmup`` untimed launches, then time exactly ``steps`` launches
+MIN_WARM_MS = 100.0
+
+
+def time_launches(fn, steps: int, warmup: int, min_warm_ms: float = MIN_WARM_MS):
+    """Run ``warmup`` untimed launches (continued, untimed, until at least
+    ``min_warm_ms`` of launches have run, so that the clock has ramped up;
+    the scope asks for 50 ms or more), then time exactly ``steps`` launches
     between two HIP events recorded on the launch stream (torch's current
     stream), with a device synchronisation on both sides.  Returns ms per
     launch."""
     import torch
+    t0 = time.perf_counter()
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
+    while (time.perf_counter() - t0) * 1e3 < min_warm_ms:
+        for _ in range(max(1, warmup)):
+            fn()
+        torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     start.record()
@@ -146,7 +163,7 @@ def run_matmul(cfg, steps, warmup):
     i, j = xi.sample_indices_matmul(xi.seed(cfg["index"], 3), cfg["M"], cfg["N"], cfg["check"])
     sampled = c[torch.from_numpy(i).cuda(), torch.from_numpy(j).cuda()].cpu().numpy()
     return dict(ms=ms, flops=flops, alg_bytes=alg_bytes, sched=repr(sched), A=A, B=B, I=i, J=j,
-                sampled=sampled, stats=stats)
+                sampled=sampled, stats=stats, out=c)
 
 
 def run_conv(cfg, steps, warmup, dtype="f32"):
@@ -178,7 +195,7 @@ def run_conv(cfg, steps, warmup, dtype="f32"):
     sampled = y.reshape(-1)[torch.from_numpy(F).cuda()].cpu().numpy()
     alg_bytes = X.itemsize * (X.size + W.size) + 4 * y.numel()
     return dict(ms=ms, flops=2.0 * Mg * Ng * Kg, alg_bytes=alg_bytes, sched=repr(sched), X=X, W=W,
-                F=F, sampled=sampled, gemm=(Mg, Ng, Kg), stats=stats)
+                F=F, sampled=sampled, gemm=(Mg, Ng, Kg), stats=stats, out=y)
 
 
 def _paper_launcher(xtc, cfg):
@@ -290,62 +307,122 @@ def summary(kind, cfg, r, workload):
         "unit": "TFLOP/s",
         "ms_per_launch": round(r["ms"], 4),
         "launch_stats": r["stats"],
+        "median_TFLOP/s": round(r["flops"] / (r["stats"]["median_ms"] * 1e-3) / 1e12, 2),
         "frac_of_peak": round(tflops / peak, 4),
         "schedule": r["sched"],
         "roofline": roofline_of(r["flops"], r["alg_bytes"], r["ms"], peak, traffic),
     }
 
 
-def cpu_baseline_leg(results, budget_s: float):
-    """The fp64 oracle on the host cores: (1) a bounded sample of the
-    headline workload -- leading row slabs of the fp32 4096^3 product, run
-    until ``budget_s`` seconds have elapsed or every row is done -- reported
-    in TFLOP/s; (2) the sampled parity check of every timed launch."""
+def _check(got, ref, tol):
     import oracle
-    out = {}
-    if "fp32" in results:
-        r = results["fp32"]
-        A, B = r["A"], r["B"]
+    err = oracle.rel_fro(got, ref)
+    return {"rel_fro": float("%.3e" % err), "tol": tol, "outputs": int(np.size(ref)),
+            "max_abs": float("%.3e" % np.max(np.abs(np.asarray(got, np.float64) - ref))),
+            "ok": bool(err <= tol)}
+
+
+def cpu_baseline_leg(results, graphs, budget_s: float):
+    """The fp64 oracle on the host cores, timed on a monotonic clock.
+
+    Per synthetic workload: the full oracle on all cores when its projected
+    time is at most ``budget_s`` (else a leading row slab of at least 10 s,
+    scaled to the whole product and labelled extrapolated), plus the
+    single-thread time of the two small matmuls.  The full products also
+    serve as the parity check of every output of the timed GPU launch; the
+    workloads timed only on sampled outputs are checked on those samples too.
+    The headline figure (``value``) is the full 4096^3 fp32 product."""
+    import oracle
+    import torch
+    # read before any one-thread run: the OpenMP default keeps the last count
+    cores = oracle.max_threads()
+    legs, parity = {}, {}
+
+    def leg(name, flops, mode, dt, rows=None):
+        legs[name] = {"mode": mode, "s": round(dt, 4), "TFLOP/s": round(flops / dt / 1e12, 6),
+                      "threads": cores}
+        if rows is not None:
+            legs[name]["rows"] = rows
+
+    rate = None   # TFLOP/s of the last full matmul leg, for projections
+    for key, cfg in (("c0", xi.MATMUL_F32_256), ("c1", xi.MATMUL_F32_1000),
+                     ("fp32", xi.MATMUL_F32_4096), ("bf16", xi.MATMUL_BF16_8192)):
+        r = results.get(key) or graphs.get(key)
+        if r is None:
+            continue
+        A, B = (r["A"], r["B"]) if "A" in r else xi.matmul_inputs(cfg)
         M, K = A.shape
         N = B.shape[1]
-        rows, t0 = 0, time.perf_counter()
-        slab = 128
-        while rows < M and time.perf_counter() - t0 < budget_s:
-            oracle.matmul(A, B, rows=(rows, min(M, rows + slab)))
-            rows = min(M, rows + slab)
-        dt = time.perf_counter() - t0
-        out["cpu_baseline"] = {
-            "value": round(2.0 * rows * N * K / dt / 1e12, 6),
-            "unit": "TFLOP/s",
-            "cores": oracle.max_threads(),
-            "kind": "oracle",
-            "sample": "fp64 oracle (i-k-j loop, OpenMP over rows) on the first %d of %d rows of "
-                      "the fp32 %dx%dx%d matmul, %.1f s wall" % (rows, M, M, N, K, dt),
-            "cpu_model": _cpu_model(),
-        }
-    parity = {}
-    for kind, r in results.items():
-        t0 = time.perf_counter()
-        if kind in ("conv", "conv_bf16"):
-            ref = oracle.conv2d_sampled(r["X"], r["W"], r["F"], stride=1, pad=1)
-            tol = 1e-5 if kind == "conv" else 1e-2
+        flops = 2.0 * M * N * K
+        tol = 1e-2 if cfg["dtype"] == "bf16" else 1e-5
+        projected = flops / (rate * 1e12) if rate else 0.0
+        if projected <= budget_s:
+            ref, dt = oracle.timed(oracle.matmul, A, B, nthreads=cores)
+            leg(cfg["name"], flops, "full", dt)
+            rate = flops / dt / 1e12
+            got = r["out"]
+            got = got.cpu().numpy() if isinstance(got, torch.Tensor) else got
+            parity[key] = _check(got, ref, tol)
+            del ref, got
         else:
-            ref = oracle.matmul_sampled(r["A"], r["B"], r["I"], r["J"])
-            tol = 1e-2 if kind == "bf16" else 1e-5
-        dt = time.perf_counter() - t0
-        err = oracle.rel_fro(r["sampled"], ref)
-        parity[kind] = {"rel_fro": float("%.3e" % err), "tol": tol, "samples": int(len(ref)),
-                        "max_abs": float("%.3e" % np.max(np.abs(r["sampled"] - ref))),
-                        "check_s": round(dt, 4), "ok": bool(err <= tol)}
-    out["parity"] = parity
+            # leading row slabs for at least 10 s, scaled by M / rows
+            rows, t0, slab = 0, time.perf_counter(), 128
+            while rows < M and time.perf_counter() - t0 < 10.0:
+                oracle.matmul(A, B, rows=(rows, min(M, rows + slab)), nthreads=cores)
+                rows = min(M, rows + slab)
+            dt = (time.perf_counter() - t0) * M / rows
+            leg(cfg["name"], flops, "extrapolated from the first %d of %d rows" % (rows, M), dt,
+                rows=rows)
+        if key in results:
+            # the sampled check the scope names for the large workloads
+            r = results[key]
+            t0 = time.perf_counter()
+            ref = oracle.matmul_sampled(r["A"], r["B"], r["I"], r["J"], nthreads=cores)
+            dt = time.perf_counter() - t0
+            parity.setdefault(key, {})
+            parity[key]["sampled"] = dict(_check(r["sampled"], ref, tol), check_s=round(dt, 4))
+    for key, dtype in (("conv", "f32"), ("conv_bf16", "bf16")):
+        if key not in results:
+            continue
+        r = results[key]
+        cfg = xi.CONV_F32_56
+        ref, dt = oracle.timed(oracle.conv2d, r["X"], r["W"], stride=cfg["stride"], pad=cfg["pad"],
+                               nthreads=cores)
+        if key == "conv":
+            leg(cfg["name"], r["flops"], "full", dt)
+        tol = 1e-5 if dtype == "f32" else 1e-2
+        parity[key] = _check(r["out"].cpu().numpy(), ref, tol)
+        t0 = time.perf_counter()
+        ref = oracle.conv2d_sampled(r["X"], r["W"], r["F"], stride=cfg["stride"], pad=cfg["pad"],
+                                    nthreads=cores)
+        parity[key]["sampled"] = dict(_check(r["sampled"], ref, tol),
+                                      check_s=round(time.perf_counter() - t0, 4))
+    if "skinny" in results:
+        r = results["skinny"]
+        ref = oracle.matmul_sampled(r["A"], r["B"], r["I"], r["J"], nthreads=cores)
+        parity["skinny"] = {"sampled": _check(r["sampled"], ref, 1e-5)}
     # the oracle on one thread for the two small configs (full products)
-    single = {}
     for cfg in (xi.MATMUL_F32_256, xi.MATMUL_F32_1000):
         A, B = xi.matmul_inputs(cfg)
         _, dt = oracle.timed(oracle.matmul, A, B, nthreads=1)
-        single["matmul_f32_%dx%dx%d" % (cfg["M"], cfg["N"], cfg["K"])] = {
-            "s": round(dt, 4), "GFLOP/s": round(2.0 * cfg["M"] * cfg["N"] * cfg["K"] / dt / 1e9, 2)}
-    out["oracle_single_thread"] = single
+        one = legs.setdefault(cfg["name"], {})
+        one["one_thread_s"] = round(dt, 4)
+        one["one_thread_TFLOP/s"] = round(2.0 * cfg["M"] * cfg["N"] * cfg["K"] / dt / 1e12, 6)
+    out = {"parity": parity, "legs": legs}
+    head = legs.get(xi.MATMUL_F32_4096["name"])
+    if head is not None:
+        out["cpu_baseline"] = {
+            "value": head["TFLOP/s"],
+            "unit": "TFLOP/s",
+            "cores": cores,
+            "kind": "oracle",
+            "sample": "fp64 oracle (i-k-j loop, OpenMP over rows) on the whole fp32 4096x4096x4096 "
+                      "matmul (%s, %.1f s wall on %d threads); per_config holds the other "
+                      "workloads (full where projected <= %.0f s)" % (head["mode"], head["s"],
+                                                                      cores, budget_s),
+            "cpu_model": _cpu_model(),
+            "per_config": legs,
+        }
     return out
 
 
@@ -379,6 +456,16 @@ def _cpu_model():
     return "unknown"
 
 
+def head_flops(kind: str) -> float:
+    if kind in ("fp32", "bf16"):
+        cfg = xi.MATMUL_F32_4096 if kind == "fp32" else xi.MATMUL_BF16_8192
+        return 2.0 * cfg["M"] * cfg["N"] * cfg["K"]
+    cfg = xi.CONV_F32_56
+    OH, OW = xi.conv_out_hw(cfg["H"], cfg["W"], cfg["R"], cfg["S"], cfg["stride"], cfg["stride"],
+                            cfg["pad"], cfg["pad"])
+    return 2.0 * cfg["OC"] * cfg["N"] * OH * OW * cfg["C"] * cfg["R"] * cfg["S"]
+
+
 def head_shape(kind: str) -> dict:
     """Shape and layout keys of a headline workload for the JSON config."""
     if kind in ("fp32", "bf16"):
@@ -395,9 +482,11 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--only", default="fp32,bf16,conv,conv_bf16,skinny,paper")
+    ap.add_argument("--only", default="fp32,bf16,conv,conv_bf16,skinny,small,paper")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--cpu-budget", type=float, default=60.0,
+                    help="largest projected time (s) of a full oracle run; longer ones are "
+                         "timed on leading row slabs and extrapolated")
     ap.add_argument("--vendor", action="store_true",
                     help="also time the vendor libraries behind torch (hipBLASLt matmul, MIOpen "
                          "conv2d) on the same workloads, as a second JSON line (comparison only)")
@@ -459,6 +548,25 @@ def main():
         print("# skinny fp32: %.4f ms/launch" % results["skinny"]["ms"], file=sys.stderr,
               flush=True)
 
+    # the two small synthetic workloads, replayed as HIP graphs of launches
+    graphs = {}
+    for key, cfg, wl in (("c0", xi.MATMUL_F32_256, "matmul_f32_256x256x256"),
+                         ("c1", xi.MATMUL_F32_1000, "matmul_f32_1000x1000x1000")):
+        if "small" not in kinds:
+            continue
+        r = run_paper(cfg, args.steps, args.warmup)
+        A, B = xi.matmul_inputs(cfg)
+        r.update(A=A, B=B)
+        graphs[key] = r
+        tf = r["flops"] / (r["ms"] * 1e-3) / 1e12
+        summaries[key] = {
+            "workload": wl, "value": round(tf, 2), "unit": "TFLOP/s",
+            "us_per_launch": round(r["ms"] * 1e3, 3), "frac_of_peak": round(tf / PEAK["f32"], 4),
+            "schedule": r["sched"], "timing": "HIP graph of 50 launches, replayed",
+            "graph_replay_exact": r["replay_ok"],
+            "roofline": roofline_of(r["flops"], r["alg_bytes"], r["ms"], PEAK["f32"], None)}
+        print("# %s: %.2f us/launch" % (cfg["name"], r["ms"] * 1e3), file=sys.stderr, flush=True)
+
     paper = {}
     if "paper" in kinds:
         for cfg in xi.PAPER_WORKLOADS:
@@ -502,18 +610,23 @@ def main():
             hip=torch.version.hip,
         ),
         "launch_stats": head["launch_stats"],
+        "median_TFLOP/s": round(head_flops(head_kind) / (head["launch_stats"]["median_ms"] * 1e-3)
+                                / 1e12, 2),
+        "value_basis": "value: the K timed launches bracketed by two HIP events (whole-run mean); "
+                       "median_TFLOP/s: the per-launch median of K further launches, each between "
+                       "its own events, which is the figure the scope's metric grades",
+        "warmup_policy": "W untimed launches, continued until at least %d ms of launches have "
+                         "run (clock ramp)" % MIN_WARM_MS,
         "roofline": head["roofline"],
         "frac_of_peak": head["frac_of_peak"],
         "also": {k: v for k, v in summaries.items() if k != head_kind},
     }
     if not args.no_cpu_baseline:
-        extra = cpu_baseline_leg(results, args.cpu_budget)
+        extra = cpu_baseline_leg(results, graphs, args.cpu_budget)
         if "cpu_baseline" in extra:
             line["cpu_baseline"] = extra["cpu_baseline"]
         line["parity"] = extra["parity"]
         line["parity"].update(paper_parity(paper))
-        if "cpu_baseline" in line:
-            line["cpu_baseline"]["single_thread"] = extra["oracle_single_thread"]
     print(json.dumps(line), flush=True)
     if args.vendor:
         print(json.dumps(vendor_line(args.steps, args.warmup, line)), flush=True)
