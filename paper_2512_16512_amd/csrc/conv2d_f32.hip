@@ -995,9 +995,18 @@ conv2d_f32_halo_kernel(ConvArgs p) {
 // past the tile are computed and not stored.  For the 16x16x4 instruction a
 // lane holds the weight of (channel 4s + lane/16, output channel lane%16)
 // and the input value of (channel 4s + lane/16, pixel lane%16), so the four
-// lane groups read four channel planes; planes are 8*64 + 16 floats apart,
-// 16 banks, which keeps the groups on disjoint banks unless a 16-pixel
-// block wraps to the next image row.
+// lane groups read four channel planes.  gfx950 serves a ds_read_b32 in two
+// phases of 32 lanes (two lane groups each), and within a phase two lanes
+// conflict when their dword addresses are equal modulo 32 (measured):
+//  - patch planes are PR*64 + 16 floats apart, so the two groups of a phase
+//    sit 16 banks apart and a 16-pixel block within one image row reads 32
+//    distinct banks.  A block that wraps to the next image row still
+//    collides with the other group; avoiding that needs patch rows of 72
+//    floats, which does not fit two workgroups per CU;
+//  - the weights of a stage are [tap][oc][8 channels]; a phase reads two
+//    channels of 16 output channels, and with plain rows output channels
+//    oc, oc + 4, oc + 8, oc + 12 share banks, so output channel oc holds its
+//    channel c at slot c ^ (2 * ((oc >> 2) & 3)).
 namespace halo16 {
 constexpr int BM = 64;
 constexpr int NB = 13;                        // 16-pixel column blocks per wave
@@ -1027,7 +1036,7 @@ struct Cfg {
     static constexpr int LOADS = A_PER_WAVE + B_PER_WAVE;
     static_assert(A_PER_WAVE * NWAVES == A_COPIES && B_PER_WAVE * NWAVES == B_COPIES, "copy split");
     static_assert(B_PER_WAVE % PR == 0, "a wave copies whole channels");
-    static_assert((PLANE % 64) == 16, "lane groups 16 banks apart");
+    static_assert((PLANE % 32) == 16, "the two lane groups of a phase 16 of 32 banks apart");
 };
 }  // namespace halo16
 
@@ -1071,7 +1080,12 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
     // plus a scalar offset that moves by a constant per stage; padding and
     // rows outside the image are out-of-range offsets that read zero, and
     // stages past the end read in range or zero and are never used.
-    const int voffA = ((lane >> 3) * C * NTAP + (lane & 7) * NTAP) * 4;
+    // A copy fills 8 output channels x 8 channel slots of one tap: lane l
+    // writes slot l % 8 of output channel 8 * block + l / 8, which holds
+    // channel (l % 8) ^ (2 * ((oc >> 2) & 3)) (the weight swizzle); the XOR
+    // is 2 * (l >> 5) for even blocks and 2 * (2 + (l >> 5)) for odd ones.
+    const int voffA0 = ((lane >> 3) * C * NTAP + ((lane & 7) ^ ((lane >> 5) << 1)) * NTAP) * 4;
+    const int voffA1 = ((lane >> 3) * C * NTAP + ((lane & 7) ^ ((2 | (lane >> 5)) << 1)) * NTAP) * 4;
     const int iwl = lane - CO;
     const int voffB = (iwl >= 0 && iwl < Wd) ? iwl * 4 : kOOB;
     int voffR[PR];
@@ -1087,7 +1101,7 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
         if (q < A_PER_WAVE) {
             const int cq = wave_u * A_PER_WAVE + q;          // copy index: tap-major
             const int tap = cq / 8, ocb = cq % 8;
-            dma4_so(rw, base + (tap * BM * CC + ocb * 64) * 4, voffA,
+            dma4_so(rw, base + (tap * BM * CC + ocb * 64) * 4, (ocb & 1) ? voffA1 : voffA0,
                     so_a + (ocb * 8 * C * NTAP + tap) * 4);
         } else {
             const int cl = (q - A_PER_WAVE) / PR, row = (q - A_PER_WAVE) % PR;
@@ -1108,10 +1122,13 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
     // and barrier sequence.
     auto body = [&](auto nbc) __attribute__((always_inline)) {
         constexpr int NBW = decltype(nbc)::value;
-        // Fragment bases.  A: output channel 16*wq + lcol, channel lgrp (+4s).
+        // Fragment bases.  A: output channel 16*wq + lcol, channel lgrp + 4s
+        // (one base per s: the swizzle may flip bit 2 of the slot).
         // B: pixel pw0 + 16j + lcol of the patch (clamped to position 0 past the
         // tile; such columns are not stored), channel plane lgrp (+4s).
-        const int a_base = ((wq * 16 + lcol) * CC + lgrp) * 4;
+        const int a_sw = ((lcol >> 2) & 3) << 1;
+        const int a_base[2] = {((wq * 16 + lcol) * CC + (lgrp ^ a_sw)) * 4,
+                               ((wq * 16 + lcol) * CC + ((lgrp + 4) ^ a_sw)) * 4};
         const int pw0 = p0 + 16 * NB * half;     // first pixel of this wave's half
         int b_base[NBW];
 #pragma unroll
@@ -1138,7 +1155,7 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
             const unsigned char *Bs = As + A_BYTES;
             const int tap = t >> 1, s = t & 1;
             const int kh = tap / 3, kw = tap - 3 * kh;
-            af[buf] = *reinterpret_cast<const float *>(As + a_base + (tap * BM * CC + 4 * s) * 4);
+            af[buf] = *reinterpret_cast<const float *>(As + a_base[s] + tap * BM * CC * 4);
 #pragma unroll
             for (int j = 0; j < NBW; ++j)
                 bfr[buf][j] = *reinterpret_cast<const float *>(Bs + b_base[j] + (4 * s * PLANE + kh * 64 + kw) * 4);
@@ -1168,7 +1185,7 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
             for (int m = 0; m < NBW; ++m) {
                 acc[m] = MF::mma(af[cur], bfr[cur][m], acc[m]);
                 if (m == 0)
-                    af[nxt] = *reinterpret_cast<const float *>(As + a_base + (tap * BM * CC + 4 * s) * 4);
+                    af[nxt] = *reinterpret_cast<const float *>(As + a_base[s] + tap * BM * CC * 4);
                 bfr[nxt][m] =
                     *reinterpret_cast<const float *>(Bs + b_base[m] + (4 * s * PLANE + kh * 64 + kw) * 4);
 #pragma unroll
@@ -1219,6 +1236,403 @@ conv2d_f32_halo16_kernel(ConvArgs p) {
         body(std::integral_constant<int, NB - 1>());
     else
         body(std::integral_constant<int, NB>());
+}
+
+// ---------------------------------------------------------------------------
+// Few output channels (block_m = 16, lds_stages = 0): layers such as the
+// paper's 7x7 stride-2 conv of 3 input channels into 16 (K = 147), where
+// 64-row tiles leave three quarters of the matrix cores idle and the
+// reduction is too short to amortise LDS staging.  A workgroup covers 16
+// output channels x 16*NB*4 pixels with four waves; each wave owns NB blocks
+// of 16 pixels and runs 16x16x4 instructions.  Both operands go straight
+// from memory into the instruction's registers: a lane holds, per k-step
+// s, the weight W[oc0 + lane % 16][4s + lane / 16] and the input value of
+// its pixel at that k, gathered through the LDS k-offset table.  Elements
+// outside the image, past K or past the output channels are buffer loads
+// at an out-of-range offset, which read zero, so there are no predicated
+// loads and K needs no particular multiple.  The k-steps are processed in
+// chunks of KC, the loads of chunk c + 1 in flight while chunk c's MFMAs
+// run (two register sets: for K up to 8 * KC every load is issued before
+// the first MFMA waits); MFMAs of k-steps past K are skipped, and even and
+// odd k-steps accumulate into two chains, added at the end, which halves
+// the dependent MFMA chain.
+namespace smallm {
+constexpr int WAVES = 4, NT = 64 * WAVES;
+}
+
+template <int NB, int KC>
+__global__ void __launch_bounds__(smallm::NT)
+conv2d_f32_smallm_kernel(ConvArgs p) {
+    typedef F32Mfma<16> MF;
+    constexpr int KCH = 4 * KC;                  // k per chunk
+    constexpr int BN = 16 * NB * smallm::WAVES;
+    extern __shared__ int2 ktab[];  // [KP]: {ic*H*W + kh*W + kw, kh | kw << 16}
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, g = lane >> 4;
+
+    const int C = p.C, H = p.H, Wd = p.W, R = p.R, S = p.S;
+    const int OC = p.OC, OHW = p.OH * p.OW;
+    const int N = p.Nb * OHW, K = C * R * S;
+    const int HW = H * Wd, RS = R * S;
+    const int NC = (K + KCH - 1) / KCH;          // chunks
+    const int KP = NC * KCH;                     // table entries
+
+    const int tiles_m = (OC + 15) / 16, tiles_n = (N + BN - 1) / BN;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * 16, n0 = tn * BN + wave * 16 * NB;
+
+    for (int k = tid; k < KP; k += smallm::NT) {
+        int2 e = make_int2(0, 0);
+        if (k < K) {
+            const int ic = k / RS, rem = k - ic * RS;
+            const int kh = rem / S, kw = rem - kh * S;
+            e = make_int2(ic * HW + kh * Wd + kw, kh | (kw << 16));
+        }
+        ktab[k] = e;
+    }
+
+    const __amdgpu_buffer_rsrc_t rw =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p.Wt), 0, OC * K * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rx =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p.X), 0, p.Nb * C * HW * 4, 0x00020000);
+    const int oc = m0 + l16;
+    const int woff = oc < OC ? oc * K : 0;
+
+    // this lane's pixel of each of its blocks
+    int xb[NB], ih0[NB], iw0[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int q = n0 + 16 * j + l16;
+        xb[j] = 0;
+        ih0[j] = -(1 << 30);    // a pixel past the end: every tap out of range
+        iw0[j] = 0;
+        if (q < N) {
+            const int img = q / OHW, pix = q - img * OHW;
+            const int oh = pix / p.OW, ow = pix - oh * p.OW;
+            ih0[j] = oh * p.sh - p.ph;
+            iw0[j] = ow * p.sw - p.pw;
+            xb[j] = img * C * HW + ih0[j] * Wd + iw0[j];
+        }
+    }
+
+    float a[2][KC], b[2][NB][KC];
+    auto load = [&](int buf, int k0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int s = 0; s < KC; ++s) {
+            const int k = k0 + 4 * s + g;
+            const bool kok = k < K;
+            a[buf][s] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rw, (kok && oc < OC) ? (woff + k) * 4 : kOOB, 0, 0));
+            const int2 t = ktab[k];
+            const int kh = t.y & 0xffff, kw = t.y >> 16;
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                const bool in = kok && (unsigned)(ih0[j] + kh) < (unsigned)H &&
+                                (unsigned)(iw0[j] + kw) < (unsigned)Wd;
+                b[buf][j][s] = __builtin_bit_cast(
+                    float, __builtin_amdgcn_raw_buffer_load_b32(rx, in ? (xb[j] + t.x) * 4 : kOOB, 0, 0));
+            }
+        }
+    };
+
+    typename MF::acc_t acc[2][NB];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[h][j][r] = 0.f;
+    auto mfmas = [&](int buf, int k0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int s = 0; s < KC; ++s)
+            if (k0 + 4 * s < K)   // uniform
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+                    acc[s & 1][j] = MF::mma(a[buf][s], b[buf][j][s], acc[s & 1][j]);
+    };
+
+    __syncthreads();  // k-offset table ready
+    // Ring of two register sets over the NC chunks (a uniform trip count);
+    // k-steps past K in the last chunk load zeros and add nothing.
+    load(0, 0);
+    for (int c = 0; c < NC; c += 2) {
+        if (c + 1 < NC) load(1, (c + 1) * KCH);
+        mfmas(0, c * KCH);
+        if (c + 1 >= NC) break;
+        if (c + 2 < NC) load(0, (c + 2) * KCH);
+        mfmas(1, (c + 1) * KCH);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) acc[0][j] += acc[1][j];
+
+    float *__restrict__ Y = p.Y;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int q = n0 + 16 * j + l16;
+        if (q >= N) continue;
+        const int img = q / OHW, pix = q - img * OHW;
+#pragma unroll
+        for (int r = 0; r < MF::NACC; ++r) {
+            const int o = m0 + MF::row(lane, r);
+            if (o < OC) Y[((size_t)img * OC + o) * OHW + pix] = (p.relu && acc[0][j][r] < 0.f) ? 0.f : acc[0][j][r];
+        }
+    }
+}
+
+// Patch-staged variant of the few-output-channel kernel, for layers whose
+// input patch fits in LDS (at most 48 KiB with the weights, 256 padded
+// columns and 256 k) (the paper's 7x7 stride-2 layer: 3 channels x 9
+// rows x 229 columns, 24.7 KB).  A workgroup covers 64 consecutive output
+// pixels of one image (one or two output rows).  It stages, with coalesced
+// loads in one round trip to memory:
+//  - its input patch: every channel, the input rows those output rows reach
+//    (rows outside the image as zeros) and every padded column, so that
+//    patch[c][r][col] holds X[c][ih_lo + r][col - pad_w] or zero;
+//  - the weights of its 16 output channels, [oc][K] (zero past OC);
+//  - the k-offset table relative to the patch, k -> c*PR*WP + kh*WP + kw.
+// An output pixel's B value at k is then patch[pix_base + ktab[k]] with
+// pix_base = (oh*stride_h - pad_h - ih_lo)*WP + ow*stride_w: no bounds
+// checks in the K loop, which reads only LDS.
+namespace smallm {
+constexpr int PATCH_MAX_BYTES = 48 * 1024;
+
+// Geometry of the patch-staged kernel for a launch: rows PR and padded
+// width WP of the patch, or PR = 0 when the patch does not fit.
+struct PatchGeom {
+    int PR, WP, bytes;
+};
+__host__ __device__ inline PatchGeom patch_geom(const ConvArgs &a, int bn) {
+    const int span = (bn - 1 + a.OW - 1) / a.OW + 1;   // output rows a tile can touch
+    PatchGeom g;
+    g.PR = (span - 1) * a.sh + a.R;
+    g.WP = (a.OW - 1) * a.sw + a.S;
+    const long long K = (long long)a.C * a.R * a.S;
+    const long long kp = (K + 31) / 32 * 32;
+    const long long bytes = 4LL * ((long long)a.C * g.PR * g.WP + 16 * (kp + 2)) + 4 * kp;
+    // the staging loops cover up to 256 padded columns and 256 k
+    g.bytes = (bytes <= PATCH_MAX_BYTES && g.WP <= 256 && kp <= 256) ? (int)bytes : 0;
+    if (g.bytes == 0) g.PR = 0;
+    return g;
+}
+}  // namespace smallm
+
+template <int NB>
+__global__ void __launch_bounds__(smallm::NT)
+conv2d_f32_smallm_patch_kernel(ConvArgs p) {
+    typedef F32Mfma<16> MF;
+    constexpr int BN = 16 * NB * smallm::WAVES;
+    extern __shared__ float sm[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, g = lane >> 4;
+
+    const int C = p.C, H = p.H, Wd = p.W, R = p.R, S = p.S;
+    const int OC = p.OC, OW = p.OW, OHW = p.OH * OW;
+    const int K = C * R * S, KP = (K + 31) / 32 * 32;
+    const int RS = R * S;
+    const smallm::PatchGeom geo = smallm::patch_geom(p, BN);
+    const int PR = geo.PR, WP = geo.WP, PLANE = PR * WP;
+
+    const int chunks = (OHW + BN - 1) / BN;   // tiles per image
+    const int tiles_m = (OC + 15) / 16, tiles_n = p.Nb * chunks;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * 16;
+    const int img = tn / chunks, p0 = (tn - img * chunks) * BN;
+    const int ih_lo = (p0 / OW) * p.sh - p.ph;
+
+    // weight rows are KP + 2 floats apart: a phase of a ds_read_b32 (16
+    // output channels x 2 lane groups) then covers 32 distinct banks (KP is
+    // a multiple of 32, so rows KP apart would all share one bank)
+    const int WS = KP + 2;
+    float *patch = sm;                                  // [C][PR][WP]
+    float *wl = sm + C * PLANE;                         // [16][WS]
+    int *ktab = reinterpret_cast<int *>(wl + 16 * WS);  // [KP]
+
+    const __amdgpu_buffer_rsrc_t rw =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p.Wt), 0, OC * K * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rx =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p.X), 0, p.Nb * C * H * Wd * 4, 0x00020000);
+
+    // Stage the patch, the weights and the table (zeros where out of range).
+    // Wave w takes patch rows w, w + 4, ...; lane l takes columns l + 64q
+    // (WP <= 256); every load of a batch is issued before its LDS stores.
+    const int xb = img * C * H * Wd;
+    const int nrows = C * PR;
+    constexpr int RPW = 8;   // rows per wave per batch
+    // Weights first (wave w takes output channels w, w + 4, w + 8, w + 12),
+    // so that their loads and the patch's are in flight together: one round
+    // trip to memory for the whole staging.
+    float wv[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int o = wave + smallm::WAVES * i;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = lane + 64 * q;
+            const bool in = m0 + o < OC && k < K;
+            wv[i][q] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rw, in ? ((m0 + o) * K + k) * 4 : kOOB, 0, 0));
+        }
+    }
+    // this thread's table entry (KP <= 256 threads), computed while the
+    // loads are in flight; k >= K: any in-range entry (its weight is zero)
+    int tk = 0;
+    if (tid < K) {
+        const int ic = tid / RS, rem = tid - ic * RS;
+        const int kh = rem / S, kw = rem - kh * S;
+        tk = ic * PLANE + kh * WP + kw;
+    }
+    // (channel, patch row) of row `wave`, stepped by 4 rows without division
+    int c_next = wave / PR, r_next = wave - c_next * PR;
+    for (int rb = wave; rb < nrows; rb += smallm::WAVES * RPW) {
+        float v[RPW][4];
+        int c = c_next, r = r_next;
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int row = rb + smallm::WAVES * i;
+            if (i > 0) {
+                r += smallm::WAVES;
+                while (r >= PR) {   // uniform
+                    r -= PR;
+                    ++c;
+                }
+            }
+            const int ih = ih_lo + r;
+            const bool rok = row < nrows && (unsigned)ih < (unsigned)H;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int iw = lane + 64 * q - p.pw;
+                const bool in = rok && lane + 64 * q < WP && (unsigned)iw < (unsigned)Wd;
+                v[i][q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                        rx, in ? (xb + (c * H + ih) * Wd + iw) * 4 : kOOB, 0, 0));
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int row = rb + smallm::WAVES * i;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (row < nrows && lane + 64 * q < WP) patch[row * WP + lane + 64 * q] = v[i][q];
+        }
+        r += smallm::WAVES;   // the next batch's first row
+        while (r >= PR) {
+            r -= PR;
+            ++c;
+        }
+        c_next = c;
+        r_next = r;
+    }
+    // the weights' stores, after the patch: their loads were issued first
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (lane + 64 * q < KP) wl[(wave + smallm::WAVES * i) * WS + lane + 64 * q] = wv[i][q];
+    if (tid < KP) ktab[tid] = tk;
+
+    // this lane's pixel of each of its blocks (position 0 past the image)
+    const int n0 = p0 + wave * 16 * NB;
+    int pb[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int pix = n0 + 16 * j + l16;
+        pb[j] = 0;
+        if (pix < OHW) {
+            const int oh = pix / OW, ow = pix - oh * OW;
+            pb[j] = (oh * p.sh - p.ph - ih_lo) * WP + ow * p.sw;
+        }
+    }
+
+    typename MF::acc_t acc[2][NB];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[h][j][r] = 0.f;
+    __syncthreads();
+
+    // k-step s: lane group g takes k = 4s + g.  Steps run in chunks of 8
+    // (KP is a multiple of 32: padded steps have zero weights), through two
+    // register sets: the table entries and weights of chunk c + 1 are read
+    // while chunk c's MFMAs run, and its input values right after them, so
+    // the dependent LDS reads of a step are not waited for one at a time.
+    // Even and odd steps accumulate into two chains.
+    const float *wrow = wl + l16 * WS + g;
+    const int NCH = KP / 32;
+    int tv[2][8];
+    float av[2][8], bv[2][NB][8];
+    auto rd_ta = [&](int buf, int c) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            tv[buf][i] = ktab[32 * c + 4 * i + g];
+            av[buf][i] = wrow[32 * c + 4 * i];
+        }
+    };
+    auto rd_b = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < NB; ++j) bv[buf][j][i] = patch[pb[j] + tv[buf][i]];
+    };
+    auto mm = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int j = 0; j < NB; ++j) acc[i & 1][j] = MF::mma(av[buf][i], bv[buf][j][i], acc[i & 1][j]);
+    };
+    rd_ta(0, 0);
+    rd_b(0);
+    for (int c = 0; c < NCH; c += 2) {
+        const bool n1 = c + 1 < NCH, n2 = c + 2 < NCH;   // uniform
+        if (n1) rd_ta(1, c + 1);
+        mm(0);
+        if (!n1) break;
+        rd_b(1);
+        if (n2) rd_ta(0, c + 2);
+        mm(1);
+        if (n2) rd_b(0);
+    }
+
+    float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int pix = n0 + 16 * j + l16;
+        if (pix >= OHW) continue;
+#pragma unroll
+        for (int r = 0; r < MF::NACC; ++r) {
+            const int o = m0 + MF::row(lane, r);
+            const float v = acc[0][j][r] + acc[1][j][r];
+            if (o < OC) Y[(size_t)o * OHW + pix] = (p.relu && v < 0.f) ? 0.f : v;
+        }
+    }
+}
+
+template <int NB, int KC>
+hipError_t launch_conv_f32_smallm(const ConvArgs &a, hipStream_t s) {
+    constexpr int BN = 16 * NB * smallm::WAVES, KCH = 4 * KC;
+    const smallm::PatchGeom geo = smallm::patch_geom(a, BN);
+    if (geo.PR > 0) {
+        const int OHW = a.OH * a.OW;
+        const unsigned tiles =
+            (unsigned)(((a.OC + 15) / 16) * a.Nb * ((OHW + BN - 1) / BN));
+        ConvArgs args = a;
+        void *kargs[] = {&args};
+        return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB>),
+                               dim3(tiles), dim3(smallm::NT), kargs, (size_t)geo.bytes, s);
+    }
+    const int N = a.Nb * a.OH * a.OW, K = a.C * a.R * a.S;
+    const unsigned tiles = (unsigned)(((a.OC + 15) / 16) * ((N + BN - 1) / BN));
+    const size_t dyn = (size_t)(((K + KCH - 1) / KCH) * KCH) * sizeof(int2);
+    ConvArgs args = a;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_smallm_kernel<NB, KC>),
+                           dim3(tiles), dim3(smallm::NT), kargs, dyn, s);
 }
 
 // Shapes the halo kernel covers; anything else runs the tap-major kernel
@@ -1335,6 +1749,10 @@ const ConvInstance kConvInstances[] = {
     XTC_CONV_INSTANCE(64, 64, 32, 32, 32, 32, 4),
     XTC_CONV_INSTANCE(128, 128, 32, 64, 64, 32, 4),
     XTC_CONV_INSTANCE(64, 128, 32, 32, 64, 16, 4),
+    // few output channels: 16 x 64 tiles, operands straight to registers
+    ConvInstance{make_sched(16, 64, 128, 16, 16, 16, 16, 4, 0, 0, 0, 0),
+                 &launch_conv_f32_smallm<1, 32>,
+                 &occupancy_of<&conv2d_f32_smallm_kernel<1, 32>, smallm::NT, (int)sizeof(int2)>},
 };
 
 }  // namespace

@@ -77,7 +77,10 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     const int kchunk = (op == XTC_OP_CONV2D && s.k_order == 2) ? s.mfma_k
                        : dt == XTC_F32 ? 4 * (64 / s.mfma_m) : s.mfma_k;
     if (s.block_k % kchunk) return XTC_ERR_BAD_SCHEDULE;
-    if (s.lds_stages < (s.k_split > 1 ? 0 : 1) || s.lds_stages > 5) return XTC_ERR_BAD_SCHEDULE;
+    // lds_stages 0: operands straight to registers (the k_split matmul
+    // kernels and the few-output-channel conv kernel)
+    const bool regs_ok = s.k_split > 1 || (op == XTC_OP_CONV2D && s.block_m == s.wave_m);
+    if (s.lds_stages < (regs_ok ? 0 : 1) || s.lds_stages > 5) return XTC_ERR_BAD_SCHEDULE;
     if (s.lds_pad < -1 || s.lds_pad > 64) return XTC_ERR_BAD_SCHEDULE;
     if (s.unroll_k < 0) return XTC_ERR_BAD_SCHEDULE;
     if (s.raster < 0 || s.raster > kMaxRaster || s.xcd_remap < 0 || s.xcd_remap > 1)
@@ -179,6 +182,13 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
         // workgroups per CU, so up to 512 tiles run in a single wave.  When
         // that leaves CUs idle (a small image batch), 64x64 tiles of four
         // 32x32 waves give four times as many workgroups.
+        if (M <= 16) {
+            // few output channels (the paper's 7x7 stride-2 layer into 16
+            // channels: 11.9 us with 64x64 tiles)
+            *out = make_sched(16, 64, 128, 16, 16, 16, 16, 4, 0, 0, 0, 0);
+            out->raster = 0;
+            return XTC_OK;
+        }
         *out = make_sched(64, 208, 8, 16, 208, 16, 16, 4, 2, -1, 0, 2);
         // two pixel halves per workgroup (one patch and one weight copy for
         // 416 pixels) once that still gives about a workgroup per CU

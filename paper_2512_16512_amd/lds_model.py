@@ -1,0 +1,324 @@
+"""LDS bank-conflict model of the kernels' LDS instructions.
+
+The GPU analogue of the paper's cache-model study (Sec. 6.3: a model of one
+memory level, evaluated per schedule against hardware counters), for the
+level the kernels stage their operands in: LDS.  It predicts, per kernel
+launch, the LDS cycles of every fragment read and staging write and how
+many of them are bank-conflict cycles, the quantities rocprofv3 counts as
+``SQ_LDS_IDX_ACTIVE`` and ``SQ_LDS_BANK_CONFLICT``.
+
+Hardware model (gfx950, measured with an in-bounds per-lane-pair probe: for
+each pair of lanes only those two were active, on the same banks at
+different addresses, and ``SQ_LDS_BANK_CONFLICT`` showed whether the pair
+shares a phase):
+
+- banks of 4 bytes; within a phase, dword address ``a`` uses bank
+  ``a % P``, where P (measured by scanning the address distance between two
+  lanes of one phase) is 64 for ds_read_b128/b64/b64_tr_b16 and 32 for
+  ds_read_b32 and every write form;
+- an instruction is served in phases of lanes; a phase takes as many cycles
+  as the largest number of distinct dwords any one bank must deliver (lanes
+  reading the same dword share it);
+- phases per instruction:
+    ds_read_b128          4 phases of 16 lanes: {0-3, 12-15, 20-23, 24-27},
+                          {4-11, 16-19, 28-31} and the same sets + 32;
+    ds_read_b64, ds_read_b64_tr_b16, ds_read_b32
+                          2 phases of 32 lanes (0-31, 32-63);
+    ds_write_b128         8 phases of 8 consecutive lanes;
+    ds_write_b64          4 phases of 16 consecutive lanes.
+  Copies written into LDS by buffer loads (``... lds``) are not counted:
+  they do not show in those counters (the bf16 GEMM's measured LDS-active
+  cycles equal its predicted fragment-read cycles within 0.2%).
+
+Each ``*_launch`` function below mirrors the addressing of one kernel family
+in ``csrc/`` and returns a :class:`LdsCost` for one launch.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+BANKS = 64
+
+_B128 = [[0, 1, 2, 3, 12, 13, 14, 15, 20, 21, 22, 23, 24, 25, 26, 27],
+         [4, 5, 6, 7, 8, 9, 10, 11, 16, 17, 18, 19, 28, 29, 30, 31]]
+PHASES = {
+    "ds_read_b128": _B128 + [[l + 32 for l in p] for p in _B128],
+    "ds_read_b64": [list(range(32)), list(range(32, 64))],
+    "ds_read_b64_tr_b16": [list(range(32)), list(range(32, 64))],
+    "ds_read_b32": [list(range(32)), list(range(32, 64))],
+    "ds_write_b128": [list(range(8 * i, 8 * i + 8)) for i in range(8)],
+    "ds_write_b64": [list(range(16 * i, 16 * i + 16)) for i in range(4)],
+    "ds_write_b32": [list(range(32)), list(range(32, 64))],
+}
+WIDTH = {"ds_read_b128": 16, "ds_read_b64": 8, "ds_read_b64_tr_b16": 8, "ds_read_b32": 4,
+         "ds_write_b128": 16, "ds_write_b64": 8, "ds_write_b32": 4}
+# Banks a phase of the instruction sees: two lanes of one phase conflict when
+# their dword addresses differ by a multiple of this (measured by scanning
+# the address distance of two lanes of one phase).
+PERIOD = {"ds_read_b128": 64, "ds_read_b64": 64, "ds_read_b64_tr_b16": 64, "ds_read_b32": 32,
+          "ds_write_b128": 32, "ds_write_b64": 32, "ds_write_b32": 32}
+
+
+def cycles(op: str, addrs) -> int:
+    """LDS cycles of one wave instruction: ``addrs`` holds each lane's byte
+    address (None for an inactive lane)."""
+    words = WIDTH[op] // 4
+    nbanks = PERIOD.get(op, BANKS)
+    total = 0
+    for phase in PHASES[op]:
+        banks = {}
+        for lane in phase:
+            a = addrs[lane]
+            if a is None:
+                continue
+            w0 = a // 4
+            for d in range(words):
+                banks.setdefault((w0 + d) % nbanks, set()).add(w0 + d)
+        total += max((len(s) for s in banks.values()), default=0)
+    return total
+
+
+def ideal(op: str) -> int:
+    """Conflict-free cycles of one wave instruction (one per phase)."""
+    return len(PHASES[op])
+
+
+@dataclass
+class LdsCost:
+    """LDS cycles of one launch: ``active`` (every cycle an LDS instruction
+    occupies, the counterpart of SQ_LDS_IDX_ACTIVE), ``conflict`` (the
+    cycles beyond one per phase, SQ_LDS_BANK_CONFLICT), ``read_bytes`` and
+    ``write_bytes`` (bytes the instructions move)."""
+    active: int = 0
+    conflict: int = 0
+    read_bytes: int = 0
+    write_bytes: int = 0
+
+    def add(self, op: str, addrs, times: int = 1):
+        c = cycles(op, addrs)
+        self.active += c * times
+        self.conflict += (c - ideal(op)) * times
+        nb = WIDTH[op] * sum(a is not None for a in addrs) * times
+        if op.startswith("ds_write"):
+            self.write_bytes += nb
+        else:
+            self.read_bytes += nb
+
+    def scaled(self, k: int) -> "LdsCost":
+        return LdsCost(self.active * k, self.conflict * k, self.read_bytes * k, self.write_bytes * k)
+
+    def __iadd__(self, o: "LdsCost"):
+        self.active += o.active
+        self.conflict += o.conflict
+        self.read_bytes += o.read_bytes
+        self.write_bytes += o.write_bytes
+        return self
+
+    @property
+    def ratio(self) -> float:
+        return self.conflict / self.active if self.active else 0.0
+
+
+def _cdiv(a, b):
+    return (a + b - 1) // b
+
+
+# ---------------------------------------------------------------- bf16 GEMM
+
+def swz_a_bf16(ca: int, row: int) -> int:
+    """A-row chunk swizzle of the bf16 direct-to-LDS GEMM (csrc/gemm_bf16.hip)."""
+    return (row >> 2) & 3 if ca == 4 else (row >> 1) & 7
+
+
+def swz_b_bf16(k: int) -> int:
+    return ((k & 1) * 6) ^ ((k & 2) * 5)
+
+
+def gemm_bf16_dma_stage(BM, BN, BK, WM, WN, MI, swz_a=swz_a_bf16) -> LdsCost:
+    """LDS cost of one LDS stage of one workgroup (all its waves) of the
+    bf16 direct-to-LDS GEMM: per MFMA k-step, TM ds_read_b128 A fragments and
+    2*TN ds_read_b64_tr_b16 B fragment halves per wave."""
+    NWN = BN // WN
+    TM, TN = WM // MI, WN // MI
+    KCH = 16 if MI == 32 else 32
+    RA, CA, RB = BK * 2, BK // 8, BN * 2
+    cost = LdsCost()
+    for wave in range((BM // WM) * NWN):
+        wm, wn = wave // NWN, wave % NWN
+        for kk in range(0, BK, KCH):
+            for i in range(TM):
+                addrs = []
+                for lane in range(64):
+                    lrow, lgrp = lane % MI, lane // MI
+                    row = wm * WM + i * MI + lrow
+                    addrs.append(row * RA + (((kk >> 3) + lgrp) ^ swz_a(CA, row)) * 16)
+                cost.add("ds_read_b128", addrs)
+            for j in range(TN):
+                for half in (0, 4):
+                    addrs = []
+                    for lane in range(64):
+                        lrow, lgrp = lane % MI, lane // MI
+                        rsub = (lane & 15) >> 2
+                        chunk = (((wn * WN + j * MI + (lrow & ~15) + 4 * (lane & 3)) >> 3)
+                                 ^ swz_b_bf16(rsub)) * 16 + 8 * (lane & 1)
+                        addrs.append((kk + 8 * lgrp + rsub + half) * RB + chunk)
+                    cost.add("ds_read_b64_tr_b16", addrs)
+    return cost
+
+
+def gemm_bf16_dma_launch(sched, M, N, K, swz_a=swz_a_bf16) -> LdsCost:
+    """One launch of the bf16 direct-to-LDS GEMM: every stage of every tile
+    (the stage's slot base is a multiple of 256 bytes, so every stage has the
+    same bank pattern), plus the one fragment set read past the last stage."""
+    s = sched
+    stage = gemm_bf16_dma_stage(s["block_m"], s["block_n"], s["block_k"], s["wave_m"],
+                                s["wave_n"], s["mfma_m"], swz_a)
+    tiles = _cdiv(M, s["block_m"]) * _cdiv(N, s["block_n"])
+    kt = _cdiv(K, s["block_k"])
+    steps = s["block_k"] // (16 if s["mfma_m"] == 32 else 32)
+    total = stage.scaled(kt * steps)
+    # the per-stage cost is per step-set times steps; add one extra set
+    per_set = LdsCost(stage.active // steps, stage.conflict // steps,
+                      stage.read_bytes // steps, stage.write_bytes // steps)
+    total += per_set
+    return LdsCost(total.active * tiles // steps, total.conflict * tiles // steps,
+                   total.read_bytes * tiles // steps, total.write_bytes * tiles // steps)
+
+
+# ------------------------------------------------- fp32 balanced halo conv
+
+def conv_f32_halo16_launch(N, C, H, W, OC, pad_h, pad_w, nh=2, plane_pad=16,
+                           a_swizzle=False, tile_px=None) -> LdsCost:
+    """One launch of the balanced halo-tiled fp32 conv (3x3, stride 1,
+    csrc/conv2d_f32.hip): per instruction k-step (tap, 4-channel group) one
+    ds_read_b32 A value and one ds_read_b32 B value per 16-pixel column
+    block.  ``plane_pad``: floats between patch planes beyond the patch rows;
+    ``a_swizzle``: output channel oc holds its channel c at slot
+    c ^ (2 * ((oc >> 2) & 3))."""
+    BM, NB, CC, CO = 64, 13, 8, 4
+    PR = 8 if nh == 1 else 10
+    PLANE = PR * 64 + plane_pad
+    OH, OW = H + 2 * pad_h - 2, W + 2 * pad_w - 2
+    OHW = OH * OW
+    BNmax = 16 * NB * nh
+    if tile_px is None:
+        t = _cdiv(OHW, BNmax)
+        tile_px = _cdiv(OHW, t)
+    chunks = _cdiv(OHW, tile_px)
+    per_image = LdsCost()
+    for ch in range(chunks):
+        p0 = ch * tile_px
+        pend = min(p0 + tile_px, OHW)
+        oh0 = p0 // OW
+        for wave in range(4 * nh):
+            wq, half = wave & 3, wave >> 2
+            nbw = NB - 1 if (nh == 2 and half == 1 and tile_px <= 16 * (2 * NB - 1)) else NB
+            pw0 = p0 + 16 * NB * half
+            offs = []
+            for j in range(nbw):
+                row = []
+                for lane in range(64):
+                    pix = pw0 + 16 * j + (lane & 15)
+                    off = 0
+                    if pix < pend:
+                        oh, ow = divmod(pix, OW)
+                        off = (oh - oh0) * 64 + ow - pad_w + CO
+                    row.append(off)
+                offs.append(row)
+            for t in range(18):
+                tap, s = t >> 1, t & 1
+                kh, kw = divmod(tap, 3)
+                a = []
+                for lane in range(64):
+                    lcol, lgrp = lane & 15, lane >> 4
+                    c = lgrp + 4 * s
+                    slot = c ^ (((lcol >> 2) & 3) << 1) if a_swizzle else c
+                    a.append(4 * (tap * BM * CC + (wq * 16 + lcol) * CC + slot))
+                per_image.add("ds_read_b32", a)
+                for j in range(nbw):
+                    b = [4 * ((lane >> 4) * PLANE + offs[j][lane] + 4 * s * PLANE + kh * 64 + kw)
+                         for lane in range(64)]
+                    per_image.add("ds_read_b32", b)
+    # tiles per output-channel block; stages C / 8; images N
+    return per_image.scaled(_cdiv(OC, BM) * (C // CC) * N)
+
+
+# --------------------------------------------------- bf16 halo-tiled conv
+
+def conv_bf16_halo_launch(N, C, H, W, OC, pad_h, pad_w, a_swizzle=False, rotate=False,
+                          store_order=False) -> LdsCost:
+    """One launch of the bf16 halo-tiled conv (3x3, stride 1,
+    csrc/conv2d_bf16.hip): per stage and wave, the register-staged patch and
+    weight stores (ds_write_b128) and, per tap, TM ds_read_b128 A fragments
+    and TN ds_read_b128 B fragments (one 16-byte cell of 8 channels).
+    ``a_swizzle``: output channels with bit 3 set hold their two 8-channel
+    halves swapped; ``rotate``: patch row r is stored rotated by
+    (r * OW) mod 16 cells in rows of 80 cells (else unrotated rows of 64);
+    ``store_order``: a thread writes its two patch cells in the order bit 2
+    of its column pair selects (else even cells first)."""
+    BM, BN, WM, WN, MI = 64, 256, 64, 64, 32
+    TM, TN, CC, PR, CO = WM // MI, WN // MI, 16, 8, 2
+    PC = 80 if rotate else 64
+    HALF = PR * PC * 16
+    P_BYTES = 2 * HALF
+    OH, OW = H + 2 * pad_h - 2, W + 2 * pad_w - 2
+    OHW = OH * OW
+    chunks = _cdiv(OHW, BN)
+
+    def rot(r):
+        return (r * OW) % 16 if rotate else 0
+
+    stage_w = LdsCost()
+    # patch stores: thread tid -> patch row tid >> 5, column pair tid & 31
+    for wave in range(4):
+        for h in range(2):
+            for second in range(2):
+                addrs = []
+                for lane in range(64):
+                    tid = wave * 64 + lane
+                    pr, cp = tid >> 5, tid & 31
+                    first = ((cp >> 2) & 1) if store_order else 0
+                    addrs.append(h * HALF + (pr * PC + 2 * cp + (second ^ first) + rot(pr)) * 16)
+                stage_w.add("ds_write_b128", addrs)
+        if wave < 2:   # weight slabs: threads 0 .. 127
+            for t in range(9):
+                addrs = []
+                for lane in range(64):
+                    tid = wave * 64 + lane
+                    woc, wh = tid >> 1, tid & 1
+                    slot = wh ^ ((woc >> 3) & 1) if a_swizzle else wh
+                    addrs.append(P_BYTES + ((t * BM + woc) * CC + 8 * slot) * 2)
+                stage_w.add("ds_write_b128", addrs)
+    per_image = LdsCost()
+    for ch in range(chunks):
+        p0 = ch * BN
+        oh0 = p0 // OW
+        for wave in range(4):
+            cells = []
+            for j in range(TN):
+                row = []
+                for lane in range(64):
+                    pix = p0 + wave * WN + j * MI + lane % MI
+                    if pix < OHW:
+                        oh, ow = divmod(pix, OW)
+                        row.append((oh - oh0, ow - pad_w + CO))
+                    else:
+                        row.append((0, 0))
+                cells.append(row)
+            for t in range(9):
+                kh, kw = divmod(t, 3)
+                for i in range(TM):
+                    addrs = []
+                    for lane in range(64):
+                        lrow, lgrp = lane % MI, lane // MI
+                        slot = lgrp ^ ((lrow >> 3) & 1) if a_swizzle else lgrp
+                        addrs.append(P_BYTES + ((t * BM + i * MI + lrow) * CC + 8 * slot) * 2)
+                    per_image.add("ds_read_b128", addrs)
+                for j in range(TN):
+                    addrs = []
+                    for lane in range(64):
+                        r, c = cells[j][lane]
+                        addrs.append((lane // MI) * HALF + ((r + kh) * PC + c + kw + rot(r + kh)) * 16)
+                    per_image.add("ds_read_b128", addrs)
+        per_image += stage_w
+    return per_image.scaled(_cdiv(OC, BM) * (C // CC) * N)
