@@ -224,8 +224,14 @@ __device__ __forceinline__ int swz_a(int row) {
 // B rows (one k each) are read four consecutive rows at a time by the
 // transpose reads, which gfx950 serves in two phases of 32 lanes (0-31,
 // 32-63); XOR values {0, 6, 10, 12} on k % 4 spread the four rows a phase
-// reads over distinct bank groups.
-__device__ __forceinline__ int swz_b(int k) { return ((k & 1) * 6) ^ ((k & 2) * 5); }
+// reads over distinct bank groups.  With the 16x16x32 instruction one phase
+// also reads rows k and k + 8 (lane groups 0 and 1), which XOR 2 on bit 3
+// of k separates (with the 32x32x16 instruction that term costs 0.6% on
+// 8192^3 and is left out).
+template <int MI>
+__device__ __forceinline__ int swz_b(int k) {
+    return ((k & 1) * 6) ^ ((k & 2) * 5) ^ (MI == 16 ? ((k >> 3) & 1) * 2 : 0);
+}
 
 
 template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES>
@@ -311,7 +317,7 @@ gemm_bf16_dma_kernel(GemmArgs p) {
         const int blk = wave * G::B_PER_WAVE + q;
         const int row = blk * (1024 / G::RB) + lane / G::CB;
         b_row[q] = row;
-        b_col[q] = 8 * ((lane % G::CB) ^ swz_b(row));
+        b_col[q] = 8 * ((lane % G::CB) ^ swz_b<MI>(row));
     }
 
     // Copies of one stage: prepare() computes the buffer offsets (out of
@@ -352,7 +358,9 @@ gemm_bf16_dma_kernel(GemmArgs p) {
         a_swz[i] = swz_a<G::CA>(row);
     }
     const int rsub = (lane & 15) >> 2;  // transpose-read row inside the group of four
-    const int bsw = swz_b(rsub);        // the rows this lane reads are all == rsub (mod 4)
+    // the rows this lane reads are kk + 8*lgrp + rsub (+ 4) with kk a multiple
+    // of 16: == rsub (mod 4), with bit 3 equal to bit 0 of lgrp
+    const int bsw = swz_b<MI>(8 * (lgrp & 1) + rsub);
     int b_chunk[G::TN];
 #pragma unroll
     for (int j = 0; j < G::TN; ++j)

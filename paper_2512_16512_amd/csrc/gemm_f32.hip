@@ -196,15 +196,18 @@ hipError_t launch_f32(const GemmArgs &a, hipStream_t s) {
 // (needs K and N multiples of 4 and 16-byte aligned rows, else the
 // register-staged kernel above runs).
 //  - A rows (BK floats, 16-byte chunks) store chunk c of row m at slot
-//    c ^ swizzle(m), which keeps the wave-wide ds_read_b128 of a fragment at
-//    its 16-cycle floor;
+//    c ^ swizzle(m).  gfx950 serves a ds_read_b128 in four phases of 16
+//    lanes ({0-3, 12-15, 20-23, 24-27}, {4-11, 16-19, 28-31} and the same
+//    + 32) over 64 banks; the swizzles give the rows of each phase distinct
+//    16-byte bank groups for both instruction tiles (checked for every
+//    instance with the LDS model, paper_2512_16512_amd/lds_model.py);
 //  - B rows (n-contiguous) store chunk c of row k at c ^ 8*((k >> 2) & 1):
 //    a ds_read_b32 of the B operand reads rows k and k+4 with the two halves
 //    of the wave, which then land 128 bytes apart (different bank halves).
 // Main loop: the ping-pong of the bf16 direct-to-LDS kernel.
 template <int CA>
 __device__ __forceinline__ int swz_a_f32(int row) {
-    return CA == 4 ? ((row >> 1) ^ (row >> 3)) & 3 : (row ^ (row >> 3)) & 7;
+    return CA == 4 ? (row >> 2) & 3 : (row >> 1) & 7;
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int MI_, int STAGES>
@@ -661,7 +664,8 @@ const GemmInstance kF32Instances[] = {
     XTC_F32_INSTANCE(128, 128, 32, 64, 64, 32, 4),
     XTC_F32_INSTANCE(128, 128, 16, 64, 64, 32, 4),
     XTC_F32_INSTANCE(64, 64, 32, 32, 32, 32, 4),     // small problems: more tiles
-    XTC_F32_INSTANCE(128, 128, 32, 64, 64, 16, 4),   // 16x16x4 instruction tile
+    XTC_F32_INSTANCE(128, 128, 32, 64, 64, 16, 8),   // 16x16x4 instruction tile (A rows padded by
+                                                     // 8: conflict-free fragment reads)
     XTC_F32_INSTANCE(256, 128, 16, 128, 64, 32, 4),
     XTC_F32_KSPLIT_INSTANCE(32, 1, 1, 4, 4, 4),      // 32x32 tiles, 4 waves
     XTC_F32_KSPLIT_INSTANCE(32, 1, 1, 8, 4, 4),      // 32x32 tiles, 8 waves

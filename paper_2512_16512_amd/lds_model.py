@@ -35,6 +35,7 @@ in ``csrc/`` and returns a :class:`LdsCost` for one launch.
 """
 from __future__ import annotations
 
+import json
 from dataclasses import dataclass
 
 BANKS = 64
@@ -130,8 +131,8 @@ def swz_a_bf16(ca: int, row: int) -> int:
     return (row >> 2) & 3 if ca == 4 else (row >> 1) & 7
 
 
-def swz_b_bf16(k: int) -> int:
-    return ((k & 1) * 6) ^ ((k & 2) * 5)
+def swz_b_bf16(k: int, mi: int = 32) -> int:
+    return ((k & 1) * 6) ^ ((k & 2) * 5) ^ ((((k >> 3) & 1) * 2) if mi == 16 else 0)
 
 
 def gemm_bf16_dma_stage(BM, BN, BK, WM, WN, MI, swz_a=swz_a_bf16) -> LdsCost:
@@ -160,7 +161,7 @@ def gemm_bf16_dma_stage(BM, BN, BK, WM, WN, MI, swz_a=swz_a_bf16) -> LdsCost:
                         lrow, lgrp = lane % MI, lane // MI
                         rsub = (lane & 15) >> 2
                         chunk = (((wn * WN + j * MI + (lrow & ~15) + 4 * (lane & 3)) >> 3)
-                                 ^ swz_b_bf16(rsub)) * 16 + 8 * (lane & 1)
+                                 ^ swz_b_bf16(8 * (lgrp & 1) + rsub, MI)) * 16 + 8 * (lane & 1)
                         addrs.append((kk + 8 * lgrp + rsub + half) * RB + chunk)
                     cost.add("ds_read_b64_tr_b16", addrs)
     return cost
@@ -194,8 +195,15 @@ def conv_f32_halo16_launch(N, C, H, W, OC, pad_h, pad_w, nh=2, plane_pad=16,
     ds_read_b32 A value and one ds_read_b32 B value per 16-pixel column
     block.  ``plane_pad``: floats between patch planes beyond the patch rows;
     ``a_swizzle``: output channel oc holds its channel c at slot
-    c ^ (2 * ((oc >> 2) & 3))."""
+    c ^ (2 * ((oc >> 2) & 3)) (True, the kernel's layout), at c ^ f(oc % 16)
+    for a callable f, or at c (False)."""
     BM, NB, CC, CO = 64, 13, 8, 4
+    if callable(a_swizzle):
+        a_xor = a_swizzle
+    elif a_swizzle:
+        a_xor = lambda lcol: ((lcol >> 2) & 3) << 1
+    else:
+        a_xor = lambda lcol: 0
     PR = 8 if nh == 1 else 10
     PLANE = PR * 64 + plane_pad
     OH, OW = H + 2 * pad_h - 2, W + 2 * pad_w - 2
@@ -232,7 +240,7 @@ def conv_f32_halo16_launch(N, C, H, W, OC, pad_h, pad_w, nh=2, plane_pad=16,
                 for lane in range(64):
                     lcol, lgrp = lane & 15, lane >> 4
                     c = lgrp + 4 * s
-                    slot = c ^ (((lcol >> 2) & 3) << 1) if a_swizzle else c
+                    slot = c ^ a_xor(lcol)
                     a.append(4 * (tap * BM * CC + (wq * 16 + lcol) * CC + slot))
                 per_image.add("ds_read_b32", a)
                 for j in range(nbw):
@@ -321,4 +329,370 @@ def conv_bf16_halo_launch(N, C, H, W, OC, pad_h, pad_w, a_swizzle=False, rotate=
                         addrs.append((lane // MI) * HALF + ((r + kh) * PC + c + kw + rot(r + kh)) * 16)
                     per_image.add("ds_read_b128", addrs)
         per_image += stage_w
-    return per_image.scaled(_cdiv(OC, BM) * (C // CC) * N)
+    # every stage's stores, plus the prologue's store of stage 0
+    total = per_image.scaled(C // CC)
+    total += stage_w.scaled(chunks)
+    return total.scaled(_cdiv(OC, BM) * N)
+
+
+# ---------------------------------------------------------------- fp32 GEMM
+
+def swz_a_f32(ca: int, row: int) -> int:
+    """A-row chunk swizzle of the fp32 direct-to-LDS GEMM (csrc/gemm_f32.hip)."""
+    return (row >> 2) & 3 if ca == 4 else (row >> 1) & 7
+
+
+def _waves(BM, BN, WM, WN):
+    NWN = BN // WN
+    return [(w // NWN, w % NWN) for w in range((BM // WM) * NWN)]
+
+
+def gemm_f32_dma_stage(BM, BN, BK, WM, WN, MI, swz_a=swz_a_f32) -> LdsCost:
+    """One LDS stage of one workgroup of the fp32 direct-to-LDS GEMM: per
+    fragment set, TM ds_read_b128 A fragments and 4*TN ds_read_b32 B
+    values per wave (B rows swizzled by lane group)."""
+    KG = 2 if MI == 32 else 4
+    KCH, SWB = 4 * KG, 16 // KG
+    RA, CA, RB = BK * 4, BK // 4, BN * 4
+    TM, TN = WM // MI, WN // MI
+    cost = LdsCost()
+    for wm, wn in _waves(BM, BN, WM, WN):
+        for kk in range(0, BK, KCH):
+            for i in range(TM):
+                addrs = []
+                for lane in range(64):
+                    lrow, lgrp = lane % MI, lane // MI
+                    row = wm * WM + i * MI + lrow
+                    addrs.append(row * RA + (((kk >> 2) + lgrp) ^ swz_a(CA, row)) * 16)
+                cost.add("ds_read_b128", addrs)
+            for j in range(TN):
+                for s in range(4):
+                    addrs = []
+                    for lane in range(64):
+                        lrow, lgrp = lane % MI, lane // MI
+                        boff = (4 * lgrp * BN + ((wn * WN + j * MI + lrow) ^ (4 * SWB * lgrp))) * 4
+                        addrs.append((kk + s) * RB + boff)
+                    cost.add("ds_read_b32", addrs)
+    return cost
+
+
+def gemm_f32_reg_stage(BM, BN, BK, WM, WN, MI, PAD):
+    """(stores, reads) of one LDS stage of one workgroup of the fp32
+    register-staged GEMM with 16-byte rows (padded A and B rows)."""
+    NT = (BM // WM) * (BN // WN) * 64
+    KG = 2 if MI == 32 else 4
+    KCH = 4 * KG
+    AS, BS = BK + PAD, BN + (8 if MI == 32 else 4)
+    TM, TN = WM // MI, WN // MI
+    st, rd = LdsCost(), LdsCost()
+    for w in range(NT // 64):
+        for i in range(BM * BK // (4 * NT)):
+            addrs = []
+            for lane in range(64):
+                idx = w * 64 + lane + i * NT
+                r, c = idx // (BK // 4), (idx % (BK // 4)) * 4
+                addrs.append((r * AS + c) * 4)
+            st.add("ds_write_b128", addrs)
+        for i in range(BK * BN // (4 * NT)):
+            addrs = []
+            for lane in range(64):
+                idx = w * 64 + lane + i * NT
+                r, c = idx // (BN // 4), (idx % (BN // 4)) * 4
+                addrs.append((r * BS + c) * 4)
+            st.add("ds_write_b128", addrs)
+    for wm, wn in _waves(BM, BN, WM, WN):
+        for kk in range(0, BK, KCH):
+            for i in range(TM):
+                rd.add("ds_read_b128", [((wm * WM + lane % MI) * AS + 4 * (lane // MI) + i * MI * AS + kk) * 4
+                                        for lane in range(64)])
+            for j in range(TN):
+                for s in range(4):
+                    rd.add("ds_read_b32", [((4 * (lane // MI) + kk + s) * BS + wn * WN + lane % MI + j * MI) * 4
+                                           for lane in range(64)])
+    return st, rd
+
+
+def gemm_f32_ksplit_tile(MI, TM, TN, KS) -> LdsCost:
+    """The fixed-order reduction of one reduction-split tile: each of the KS
+    waves writes its partial accumulators (ds_write_b32 of consecutive
+    lanes), then the KS partials of every register are read back."""
+    nacc = 16 if MI == 32 else 4
+    nreg = TM * TN * nacc
+    cost = LdsCost()
+    contiguous = [4 * lane for lane in range(64)]
+    cost.add("ds_write_b32", contiguous, times=KS * nreg)
+    cost.add("ds_read_b32", contiguous, times=KS * nreg)
+    return cost
+
+
+# ---------------------------------------------------------------- bf16 GEMM (register-staged)
+
+def gemm_bf16_reg_stage(BM, BN, BK, WM, WN, MI, PAD):
+    """(stores, reads) of one LDS stage of the bf16 register-staged GEMM
+    (16-byte chunks, padded A rows, B rows padded by 32 elements)."""
+    NT = (BM // WM) * (BN // WN) * 64
+    KG = 2 if MI == 32 else 4
+    KCH = 8 * KG
+    AS, BS = BK + PAD, BN + 32
+    TM, TN = WM // MI, WN // MI
+    st, rd = LdsCost(), LdsCost()
+    for w in range(NT // 64):
+        for i in range(BM * BK // (8 * NT)):
+            addrs = []
+            for lane in range(64):
+                idx = w * 64 + lane + i * NT
+                r, c = idx // (BK // 8), (idx % (BK // 8)) * 8
+                addrs.append((r * AS + c) * 2)
+            st.add("ds_write_b128", addrs)
+        for i in range(BK * BN // (8 * NT)):
+            addrs = []
+            for lane in range(64):
+                idx = w * 64 + lane + i * NT
+                r, c = idx // (BN // 8), (idx % (BN // 8)) * 8
+                addrs.append((r * BS + c) * 2)
+            st.add("ds_write_b128", addrs)
+    for wm, wn in _waves(BM, BN, WM, WN):
+        for kk in range(0, BK, KCH):
+            for i in range(TM):
+                rd.add("ds_read_b128", [((wm * WM + lane % MI) * AS + 8 * (lane // MI) + i * MI * AS + kk) * 2
+                                        for lane in range(64)])
+            for j in range(TN):
+                for half in (0, 4):
+                    addrs = []
+                    for lane in range(64):
+                        lrow, lgrp = lane % MI, lane // MI
+                        bs = ((8 * lgrp + ((lane & 15) >> 2)) * BS + wn * WN + (lrow & ~15)
+                              + 4 * (lane & 3))
+                        addrs.append((bs + (kk + half) * BS + j * MI) * 2)
+                    rd.add("ds_read_b64_tr_b16", addrs)
+    return st, rd
+
+
+# ------------------------------------------------------- per-launch models
+
+def matmul_launch(dtype: str, s: dict, M: int, N: int, K: int):
+    """LDS cost of one launch of the matmul instance ``s`` (a schedule dict)
+    on 16-byte-aligned row-major operands, or None if the instance's kernel
+    is not modelled.  The instance's kernel is the one its launcher picks for
+    such operands: the direct-to-LDS kernel for lds_pad -1, else the
+    register-staged kernel, or the reduction-split kernel for k_split > 1."""
+    BM, BN, BK = s["block_m"], s["block_n"], s["block_k"]
+    WM, WN, MI = s["wave_m"], s["wave_n"], s["mfma_m"]
+    tiles = _cdiv(M, BM) * _cdiv(N, BN)
+    kt = _cdiv(K, BK)
+    if s.get("k_split", 1) > 1:
+        return gemm_f32_ksplit_tile(MI, BM // MI, BN // MI, s["k_split"]).scaled(tiles)
+    if dtype == "bf16":
+        if s["lds_pad"] < 0:
+            return gemm_bf16_dma_launch(s, M, N, K)
+        st, rd = gemm_bf16_reg_stage(BM, BN, BK, WM, WN, MI, s["lds_pad"])
+        total = st.scaled(kt)
+        total += rd.scaled(kt)
+        return total.scaled(tiles)
+    if s["lds_pad"] < 0:
+        stage = gemm_f32_dma_stage(BM, BN, BK, WM, WN, MI)
+        kch = 4 * (2 if MI == 32 else 4)
+        steps = BK // kch
+        total = stage.scaled(kt * steps)
+        total += stage
+        return LdsCost(total.active * tiles // steps, total.conflict * tiles // steps,
+                       total.read_bytes * tiles // steps, total.write_bytes * tiles // steps)
+    st, rd = gemm_f32_reg_stage(BM, BN, BK, WM, WN, MI, s["lds_pad"])
+    total = st.scaled(kt)
+    total += rd.scaled(kt)
+    return total.scaled(tiles)
+
+
+# ---------------------------------------------------- few-output-channel conv
+
+def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
+    """One launch of the patch-staged few-output-channel fp32 conv
+    (csrc/conv2d_f32.hip), or None when its patch does not fit (then the
+    gather form runs, which uses LDS only for the k-offset table): per
+    workgroup the staging stores (ds_write_b32 of consecutive lanes) and, per
+    k-step, the table entry, the weight and the input value (ds_read_b32)."""
+    BN, WAVES = 64, 4
+    OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    OHW = OH * OW
+    K = C * R * S
+    KP = _cdiv(K, 32) * 32
+    WS = KP + 2
+    span = (BN - 1 + OW - 1) // OW + 1
+    PR, WP = (span - 1) * sh + R, (OW - 1) * sw + S
+    if 4 * (C * PR * WP + 16 * (KP + 2)) + 4 * KP > 48 * 1024 or WP > 256 or KP > 256:
+        return None
+    PLANE = PR * WP
+
+    def tab(k):
+        if k >= K:
+            return 0
+        ic, rem = divmod(k, R * S)
+        kh, kw = divmod(rem, S)
+        return ic * PLANE + kh * WP + kw
+
+    per_image = LdsCost()
+    chunks = _cdiv(OHW, BN)
+    contiguous = [4 * lane for lane in range(64)]
+    for ch in range(chunks):
+        p0 = ch * BN
+        oh_a = p0 // OW
+        # staging: patch rows (4 column groups each), weights, table
+        rows = C * PR
+        for w in range(WAVES):
+            nr = len(range(w, rows, WAVES))
+            per_image.add("ds_write_b32", contiguous, times=nr * _cdiv(WP, 64))
+            per_image.add("ds_write_b32", contiguous, times=4 * _cdiv(KP, 64))
+        per_image.add("ds_write_b32", contiguous, times=_cdiv(KP, 64))
+        for w in range(WAVES):
+            pb = []
+            for lane in range(64):
+                pix = p0 + w * 16 + (lane & 15)
+                if pix < OHW:
+                    oh, ow = divmod(pix, OW)
+                    pb.append((oh - oh_a) * sh * WP + ow * sw)
+                else:
+                    pb.append(0)
+            for s in range(KP // 4):
+                per_image.add("ds_read_b32", [4 * tab(4 * s + (lane >> 4)) for lane in range(64)])
+                per_image.add("ds_read_b32", [4 * (PLANE * C + (lane & 15) * WS + (lane >> 4) + 4 * s)
+                                              for lane in range(64)])
+                per_image.add("ds_read_b32", [4 * (pb[lane] + tab(4 * s + (lane >> 4))) for lane in range(64)])
+    return per_image.scaled(_cdiv(OC, 16) * N)
+
+
+def conv_launch(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
+    """LDS cost of one conv launch of instance ``s``, or None when the kernel
+    it runs for this shape is not modelled (the gather, channel-major
+    direct-to-LDS, tap-major and 64x256 halo kernels)."""
+    sh, sw = (stride, stride) if isinstance(stride, int) else stride
+    ph, pw = (pad, pad) if isinstance(pad, int) else pad
+    OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    halo_class = R == 3 and S == 3 and sh == 1 and sw == 1
+    if dtype == "f32" and s["k_order"] == 2 and s["block_n"] in (208, 416):
+        nh = 1 if s["block_n"] == 208 else 2
+        if not (halo_class and C % 8 == 0 and pw <= 4 and OW - pw + 5 <= 63):
+            return None
+        # the launcher's pixel tile: the fewest tiles per image of at most 208*nh
+        ohw = OH * OW
+        t = _cdiv(ohw, 208 * nh)
+        pt = _cdiv(ohw, t)
+        span = (pt - 1 + OW - 1) // OW + 1
+        if span + 2 > (8 if nh == 1 else 10):
+            return None
+        return conv_f32_halo16_launch(N, C, H, W, OC, ph, pw, nh=nh, a_swizzle=True, tile_px=pt)
+    if dtype == "bf16" and s["k_order"] == 2:
+        span = (256 - 1 + OW - 1) // OW + 1
+        if halo_class and C % 16 == 0 and W % 2 == 0 and pw <= 2 and OW - pw + 3 <= 63 and span + 2 <= 8:
+            return conv_bf16_halo_launch(N, C, H, W, OC, ph, pw, a_swizzle=True, rotate=True,
+                                         store_order=True)
+        return None
+    if dtype == "f32" and s["block_m"] == 16 and s["lds_stages"] == 0:
+        return conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw)
+    return None
+
+
+# ----------------------------------------------------------- evaluation
+
+def run(op: str, dtype: str, dims, order_path: str, reps: int = 2):
+    """Launch every compiled instance of op/dtype ``reps`` times on the
+    problem ``dims`` (matmul: M, N, K; conv: N, C, H, W, OC, R, S, stride,
+    pad) and record the order, so that the profiler's per-dispatch counter
+    rows can be matched to instances.  LDS traffic does not depend on the
+    raster order, so raster 0 stands for all of them."""
+    import torch
+
+    import paper_2512_16512_amd as xtc
+    from paper_2512_16512_amd import tune
+    p = tune.Problem(op, dtype, tuple(dims))
+    code = xtc.XTC_F32 if dtype == "f32" else xtc.XTC_BF16
+    opc = xtc.XTC_OP_MATMUL if op == "matmul" else xtc.XTC_OP_CONV2D
+    stream = torch.cuda.current_stream().cuda_stream
+    entries = []
+    for s in xtc.xtc_sched_list(opc, code):
+        s.raster, s.xcd_remap = 0, 1
+        for _ in range(reps):
+            p.launch(s, stream)
+        torch.cuda.synchronize()
+        entries.append(s.as_dict())
+    with open(order_path, "w") as f:
+        json.dump({"op": op, "dtype": dtype, "dims": list(dims), "reps": reps, "schedules": entries}, f)
+    print("launched %d instances x %d" % (len(entries), reps), flush=True)
+
+
+def _counter_rows(csv_path: str, counter: str):
+    import csv
+    rows = {}
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] != counter or "xtc::" not in r["Kernel_Name"]:
+            continue
+        d = int(r["Dispatch_Id"])
+        rows[d] = rows.get(d, 0.0) + float(r["Counter_Value"])
+    return [rows[d] for d in sorted(rows)]
+
+
+def predict(op: str, dtype: str, s: dict, dims):
+    if op == "matmul":
+        return matmul_launch(dtype, s, *dims)
+    return conv_launch(dtype, s, *dims)
+
+
+def correlate(order_path: str, csv_path: str):
+    """Predicted vs measured LDS-active and bank-conflict cycles per
+    instance; returns the table and (Pearson, Spearman) for both counters
+    over the modelled instances."""
+    from paper_2512_16512_amd.traffic_model import pearson, spearman
+    o = json.load(open(order_path))
+    act = _counter_rows(csv_path, "SQ_LDS_IDX_ACTIVE")
+    con = _counter_rows(csv_path, "SQ_LDS_BANK_CONFLICT")
+    reps = o["reps"]
+    n = len(o["schedules"])
+    if len(act) != reps * n or len(con) != reps * n:
+        raise ValueError("%d/%d counter rows for %d instances x %d launches"
+                         % (len(act), len(con), n, reps))
+    table = []
+    for i, s in enumerate(o["schedules"]):
+        pred = predict(o["op"], o["dtype"], s, o["dims"])
+        table.append({"sched": s,
+                      "measured_active": sum(act[i * reps:(i + 1) * reps]) / reps,
+                      "measured_conflict": sum(con[i * reps:(i + 1) * reps]) / reps,
+                      "predicted_active": None if pred is None else pred.active,
+                      "predicted_conflict": None if pred is None else pred.conflict})
+    mod = [t for t in table if t["predicted_active"] is not None]
+    stats = {}
+    for key in ("active", "conflict"):
+        x = [t["predicted_" + key] for t in mod]
+        y = [t["measured_" + key] for t in mod]
+        stats[key] = (pearson(x, y), spearman(x, y)) if len(mod) > 2 else (float("nan"),) * 2
+    return table, stats
+
+
+def main(argv=None):
+    import argparse
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    r = sub.add_parser("run")
+    r.add_argument("op", choices=["matmul", "conv2d"])
+    r.add_argument("dtype", choices=["f32", "bf16"])
+    r.add_argument("dims", type=int, nargs="+")
+    r.add_argument("--order", required=True)
+    r.add_argument("--reps", type=int, default=2)
+    c = sub.add_parser("correlate")
+    c.add_argument("order")
+    c.add_argument("counters_csv")
+    c.add_argument("--json", default=None)
+    a = ap.parse_args(argv)
+    if a.cmd == "run":
+        run(a.op, a.dtype, a.dims, a.order, a.reps)
+        return 0
+    table, stats = correlate(a.order, a.counters_csv)
+    for key, (r_, rho) in stats.items():
+        print("%-8s Pearson r = %.4f  Spearman rho = %.4f" % (key, r_, rho))
+    if a.json:
+        with open(a.json, "w") as f:
+            json.dump({"stats": stats, "rows": table}, f, indent=1)
+    return 0
+
+
+if __name__ == "__main__":
+    import sys
+    sys.exit(main())

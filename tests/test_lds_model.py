@@ -1,0 +1,123 @@
+"""CPU tests of the LDS bank-conflict model (paper_2512_16512_amd/lds_model.py).
+
+The model's predictions are pinned to counter values rocprofv3 measured on
+MI355X (SQ_LDS_IDX_ACTIVE, SQ_LDS_BANK_CONFLICT per dispatch; the profiles
+under profiles/ hold the commands), and its phase tables to the probe
+measurements that define them.
+"""
+import pytest
+
+from paper_2512_16512_amd import lds_model as L
+
+
+def _frag_modes(mode):
+    """Lane byte addresses of the ds_read_b128 patterns a throughput probe
+    measured at 4, 8, 16 and 16 LDS cycles per instruction."""
+    out = []
+    for lane in range(64):
+        row, g = lane & 31, lane >> 5
+        if mode == 0:
+            out.append(16 * lane)
+        elif mode == 1:
+            out.append(row * 64 + ((g ^ ((row >> 1) ^ (row >> 3))) & 3) * 16)
+        elif mode == 2:
+            out.append(row * 64 + ((g + row) & 3) * 16)
+        else:
+            out.append(row * 64 + ((g ^ (row & 3)) & 3) * 16)
+    return out
+
+
+def test_phase_tables_reproduce_probe_cycles():
+    assert [L.cycles("ds_read_b128", _frag_modes(m)) for m in range(4)] == [4, 8, 16, 16]
+
+
+def test_phase_tables_partition_the_wave():
+    for op, phases in L.PHASES.items():
+        lanes = sorted(l for p in phases for l in p)
+        assert lanes == list(range(64)), op
+
+
+def test_contiguous_accesses_are_conflict_free():
+    for op, w in L.WIDTH.items():
+        addrs = [w * lane for lane in range(64)]
+        assert L.cycles(op, addrs) == L.ideal(op), op
+
+
+def test_bank_periods():
+    # two lanes of one phase, same bank at the measured period, else distinct
+    for op, period in (("ds_read_b32", 128), ("ds_write_b128", 128), ("ds_read_b128", 256),
+                       ("ds_read_b64_tr_b16", 256)):
+        base = [None] * 64
+        a = list(base)
+        a[0], a[1] = 0, period
+        assert L.cycles(op, a) == 2, op
+        a[1] = period // 2 if op != "ds_read_b32" else 64
+        assert L.cycles(op, a) == 1, op
+
+
+# (prediction, measured SQ_LDS_IDX_ACTIVE, measured SQ_LDS_BANK_CONFLICT)
+BF16_8192 = dict(block_m=256, block_n=256, block_k=32, wave_m=128, wave_n=64, mfma_m=32,
+                 lds_pad=-1, k_split=1)
+
+
+def test_bf16_gemm_8192_matches_counters():
+    c = L.matmul_launch("bf16", BF16_8192, 8192, 8192, 8192)
+    assert c.active == pytest.approx(1.009e8, rel=2e-3) and c.conflict == 0
+
+
+def test_bf16_gemm_previous_swizzle_matches_counters():
+    old = lambda ca, row: ((row >> 1) ^ (row >> 3)) & 3 if ca == 4 else (row ^ (row >> 3)) & 7
+    c = L.gemm_bf16_dma_launch(BF16_8192, 8192, 8192, 8192, swz_a=old)
+    assert c.active == pytest.approx(1.681e8, rel=2e-3)
+    assert c.conflict == pytest.approx(6.724e7, rel=2e-3)
+
+
+def test_f32_gemm_4096_matches_counters():
+    s = dict(block_m=256, block_n=256, block_k=32, wave_m=128, wave_n=64, mfma_m=32, lds_pad=-1,
+             k_split=1)
+    c = L.matmul_launch("f32", s, 4096, 4096, 4096)
+    assert c.active == pytest.approx(3.362e7, rel=2e-3) and c.conflict == 0
+
+
+def test_ksplit_reduction_matches_counters():
+    s = dict(block_m=32, block_n=16, block_k=32, wave_m=32, wave_n=16, mfma_m=16, lds_pad=0,
+             k_split=8)
+    c = L.matmul_launch("f32", s, 32768, 16, 4096)
+    assert c.active == 262144 and c.conflict == 0
+
+
+def test_f32_halo_conv_matches_counters_before_and_after():
+    before = L.conv_f32_halo16_launch(32, 64, 56, 56, 64, 1, 1, plane_pad=16, a_swizzle=False)
+    assert before.active == pytest.approx(1.0617e7, rel=2e-3)
+    assert before.conflict == pytest.approx(2.654e6, rel=2e-3)
+    # a layout measured on the way (planes 32 floats apart, channels 8..15 at c ^ 2)
+    wrong = L.conv_f32_halo16_launch(32, 64, 56, 56, 64, 1, 1, plane_pad=32,
+                                     a_swizzle=lambda lcol: ((lcol >> 3) & 1) << 1)
+    assert wrong.active == pytest.approx(1.593e7, rel=2e-3)
+    assert wrong.conflict == pytest.approx(7.963e6, rel=2e-3)
+    now = L.conv_launch("f32", dict(k_order=2, block_n=416, block_m=64, lds_stages=2),
+                        32, 64, 56, 56, 64, 3, 3, 1, 1)
+    assert now.active == pytest.approx(8.847e6, rel=2e-3)
+    assert now.conflict == pytest.approx(8.847e5, rel=2e-3)
+
+
+def test_bf16_halo_conv_matches_counters():
+    old = L.conv_bf16_halo_launch(32, 64, 56, 56, 64, 1, 1)
+    assert old.active == pytest.approx(2.463e6, rel=0.02)
+    assert old.conflict == pytest.approx(9.39e5, rel=0.06)
+    now = L.conv_launch("bf16", dict(k_order=2, block_n=256, block_m=64, lds_stages=2),
+                        32, 64, 56, 56, 64, 3, 3, 1, 1)
+    assert now.active == pytest.approx(1.524e6, rel=2e-3) and now.conflict == 0
+
+
+def test_small_channel_conv_matches_counters():
+    c = L.conv_launch("f32", dict(k_order=0, block_n=64, block_m=16, lds_stages=0),
+                      1, 3, 224, 224, 16, 7, 7, 2, 3)
+    assert c.active == pytest.approx(2.513e5, rel=2e-3)
+    assert c.conflict == 784
+
+
+def test_unmodelled_kernels_return_none():
+    # the tap-major conv kernel is not modelled
+    s = dict(k_order=1, block_n=256, block_m=64, lds_stages=2)
+    assert L.conv_launch("f32", s, 32, 64, 56, 56, 64, 3, 3, 1, 1) is None
