@@ -23,6 +23,15 @@ the sum over XCDs and groups of (distinct A row-panels) x rows x K x elt +
 (M x N x 4 bytes).  The model ignores cache-line granularity, the replacement
 policy, and timing skew between workgroups.
 
+The last-level cache.  Behind the L2s, the 256 MiB MALL is shared by all
+XCDs: an L2 miss that hits there costs no DRAM traffic.  ``predict_dram``
+replays the same tile groups, XCDs in lockstep rounds, through a 256 MiB
+least-recently-used panel cache and counts the DRAM reads.  No counter
+separates MALL hits from DRAM reads (the L2 counters see both as misses),
+so that term is evaluated against kernel time over the tile orders
+(``orders`` / ``evaluate-orders``), together with the L2 term and their
+unweighted sum.
+
 Usage (the measurement step runs under rocprofv3; see ``run``)::
 
     rocprofv3 --pmc FETCH_SIZE -f csv -d OUT -o run -- \\
@@ -85,6 +94,56 @@ def predict(M: int, N: int, K: int, elt: int, block_m: int, block_n: int, raster
     return read, 4 * M * N
 
 
+MALL_BYTES = 256 << 20
+
+
+def predict_dram(M: int, N: int, K: int, elt: int, block_m: int, block_n: int, raster: int,
+                 xcd_remap: int, occupancy: int, mall_bytes: int = MALL_BYTES):
+    """Predicted DRAM read bytes of one launch, with the last-level cache
+    (MALL, 256 MiB on MI355X, shared by the 8 XCDs) in front of HBM.
+
+    The XCDs advance through their groups of ``32 * occupancy`` tiles in
+    lockstep rounds (the same groups as ``predict``).  In a round every XCD
+    asks the MALL for the A row-panels and B column-panels of its group; a
+    panel the MALL holds is a hit, any other is read from DRAM once for all
+    the XCDs that ask for it in that round and then kept, least recently used
+    first out, within ``mall_bytes``.  The L2 misses ``predict`` counts are
+    the MALL requests; the difference is what the XCDs share in the MALL."""
+    from collections import OrderedDict
+    tiles_m = -(-M // block_m)
+    tiles_n = -(-N // block_n)
+    grid = tiles_m * tiles_n
+    conc = max(1, CUS_PER_XCD * max(1, occupancy))
+    groups = []
+    for x in range(XCDS):
+        ids = list(range(x, grid, XCDS))
+        tiles = [tile_coords(b, grid, tiles_m, tiles_n, raster, xcd_remap) for b in ids]
+        groups.append([tiles[g0:g0 + conc] for g0 in range(0, len(tiles), conc)])
+    rounds = max(len(g) for g in groups)
+    panel_bytes = lambda p: (min(block_m, M - p[1] * block_m) if p[0] == "A"
+                             else min(block_n, N - p[1] * block_n)) * K * elt
+    mall = OrderedDict()
+    held = 0
+    dram = 0
+    for r in range(rounds):
+        want = []
+        for g in groups:
+            if r < len(g):
+                want += [("A", t[0]) for t in g[r]] + [("B", t[1]) for t in g[r]]
+        for p in dict.fromkeys(want):
+            if p in mall:
+                mall.move_to_end(p)
+                continue
+            nb = panel_bytes(p)
+            dram += nb
+            mall[p] = nb
+            held += nb
+            while held > mall_bytes and len(mall) > 1:
+                _, old = mall.popitem(last=False)
+                held -= old
+    return dram
+
+
 def _ranks(v):
     """Ranks 1..n with ties given their average rank."""
     order = sorted(range(len(v)), key=lambda i: v[i])
@@ -143,6 +202,106 @@ def run(dtype: str, M: int, N: int, K: int, order_path: str, reps: int = 2, rast
     print("launched %d schedules x %d" % (len(entries), reps), flush=True)
 
 
+ORDERS = tuple((r, x) for r in (0, 1, 2, 4, 8, 16, 32) for x in (0, 1))
+
+
+def sweep_orders(dtype: str, M: int, N: int, K: int, out_path: str, warmup: int = 2, reps: int = 5,
+                 passes: int = 3, warm_s: float = 0.5):
+    """Time the default schedule of one matmul under every tile order
+    (raster x XCD remap in ORDERS).  After ``warm_s`` seconds of untimed
+    launches (the clock settles), ``passes`` passes over the orders each run
+    ``warmup`` untimed launches and ``reps`` launches between their own HIP
+    events per order; an order's time is the median of its ``passes * reps``
+    launches.  Writes the times, the launch order (``warmup + reps``
+    dispatches per order and pass, after the warm-up dispatches, for
+    matching a counter pass) and the schedule's occupancy to ``out_path``."""
+    import torch
+
+    import paper_2512_16512_amd as xtc
+    from paper_2512_16512_amd import tune
+    p = tune.Problem("matmul", dtype, (M, N, K))
+    base = xtc.xtc_default_schedule(xtc.XTC_OP_MATMUL, p.code, M, N, K)
+    occ = xtc.xtc_sched_occupancy(xtc.XTC_OP_MATMUL, p.code, K, base)
+    stream = torch.cuda.current_stream().cuda_stream
+    import time
+    nwarm = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < warm_s:
+        for _ in range(4):
+            p.launch(base, stream)
+        nwarm += 4
+        torch.cuda.synchronize()
+    times = {o: [] for o in ORDERS}
+    for _ in range(passes):
+        for raster, remap in ORDERS:
+            s = xtc.Sched(**base.as_dict())
+            s.raster, s.xcd_remap = raster, remap
+            for _ in range(warmup):
+                p.launch(s, stream)
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(reps)]
+            for e0, e1 in ev:
+                e0.record()
+                p.launch(s, stream)
+                e1.record()
+            torch.cuda.synchronize()
+            times[(raster, remap)] += [e0.elapsed_time(e1) for e0, e1 in ev]
+    rows = []
+    for raster, remap in ORDERS:
+        t = sorted(times[(raster, remap)])
+        rows.append({"raster": raster, "xcd_remap": remap, "median_ms": t[len(t) // 2]})
+    with open(out_path, "w") as f:
+        json.dump({"dtype": dtype, "M": M, "N": N, "K": K, "warmup": warmup, "reps": reps,
+                   "passes": passes, "warm_dispatches": nwarm, "sched": base.as_dict(),
+                   "occupancy": occ, "orders": rows}, f)
+    print("timed %d tile orders" % len(rows), flush=True)
+
+
+def evaluate_orders(sweep_path: str, fetch_csv: str = None, fetch_scale: float = 2.0,
+                    fetch_order: str = None):
+    """Per tile order: the L2-miss bytes ``predict`` gives, the DRAM bytes
+    ``predict_dram`` gives, the measured time and (with a FETCH_SIZE pass
+    of the same sweep) the measured L2-miss bytes; returns the rows and the
+    Pearson / Spearman coefficients of each prediction against time (and of
+    the L2-miss prediction against FETCH_SIZE).  ``fetch_order`` is the
+    record the counter pass wrote (its warm-up count may differ from the
+    timing pass's); the timing pass's own record by default."""
+    o = json.load(open(sweep_path))
+    fo = json.load(open(fetch_order)) if fetch_order else o
+    s = o["sched"]
+    elt = 4 if o["dtype"] == "f32" else 2
+    fetch = None
+    if fetch_csv:
+        vals = _counter_rows(fetch_csv, "FETCH_SIZE")
+        per, nord, npass = fo["warmup"] + fo["reps"], len(fo["orders"]), fo.get("passes", 1)
+        skip = fo.get("warm_dispatches", 0)
+        if len(vals) != skip + npass * per * nord:
+            raise ValueError("%d counter rows for %d + %d passes x %d orders x %d launches"
+                             % (len(vals), skip, npass, nord, per))
+        fetch = []
+        for i in range(nord):
+            got = [v for q in range(npass)
+                   for v in vals[skip + (q * nord + i) * per + fo["warmup"]:skip + (q * nord + i + 1) * per]]
+            fetch.append(sum(got) / len(got) * 1024 * fetch_scale)
+    rows = []
+    for i, r in enumerate(o["orders"]):
+        l2, _ = predict(o["M"], o["N"], o["K"], elt, s["block_m"], s["block_n"], r["raster"],
+                        r["xcd_remap"], o["occupancy"])
+        dram = predict_dram(o["M"], o["N"], o["K"], elt, s["block_m"], s["block_n"], r["raster"],
+                            r["xcd_remap"], o["occupancy"])
+        rows.append(dict(r, l2_pred=l2, dram_pred=dram, fetch=None if fetch is None else fetch[i]))
+    t = [r["median_ms"] for r in rows]
+    comb = [r["l2_pred"] + r["dram_pred"] for r in rows]
+    stats = {"l2_vs_time": (pearson([r["l2_pred"] for r in rows], t), spearman([r["l2_pred"] for r in rows], t)),
+             "dram_vs_time": (pearson([r["dram_pred"] for r in rows], t),
+                              spearman([r["dram_pred"] for r in rows], t)),
+             "l2+dram_vs_time": (pearson(comb, t), spearman(comb, t))}
+    if fetch is not None:
+        stats["l2_vs_fetch"] = (pearson([r["l2_pred"] for r in rows], fetch),
+                                spearman([r["l2_pred"] for r in rows], fetch))
+    return rows, stats
+
+
 def _counter_rows(csv_path: str, counter: str):
     import csv
     rows = {}
@@ -187,6 +346,17 @@ def main(argv=None):
     r.add_argument("K", type=int)
     r.add_argument("--order", required=True)
     r.add_argument("--reps", type=int, default=2)
+    w = sub.add_parser("orders")
+    w.add_argument("dtype", choices=["f32", "bf16"])
+    w.add_argument("M", type=int)
+    w.add_argument("N", type=int)
+    w.add_argument("K", type=int)
+    w.add_argument("--out", required=True)
+    e = sub.add_parser("evaluate-orders")
+    e.add_argument("sweep")
+    e.add_argument("--fetch-csv", default=None)
+    e.add_argument("--fetch-scale", type=float, default=2.0)
+    e.add_argument("--fetch-order", default=None)
     c = sub.add_parser("correlate")
     c.add_argument("order")
     c.add_argument("fetch_csv")
@@ -195,6 +365,18 @@ def main(argv=None):
     a = ap.parse_args(argv)
     if a.cmd == "run":
         run(a.dtype, a.M, a.N, a.K, a.order, a.reps)
+        return 0
+    if a.cmd == "orders":
+        sweep_orders(a.dtype, a.M, a.N, a.K, a.out)
+        return 0
+    if a.cmd == "evaluate-orders":
+        rows, stats = evaluate_orders(a.sweep, a.fetch_csv, a.fetch_scale, a.fetch_order)
+        for r in rows:
+            print("raster %2d xcd %d  %.4f ms  L2 pred %.2f GB  DRAM pred %.3f GB%s" % (
+                r["raster"], r["xcd_remap"], r["median_ms"], r["l2_pred"] / 1e9, r["dram_pred"] / 1e9,
+                "" if r["fetch"] is None else "  FETCH %.2f GB" % (r["fetch"] / 1e9)))
+        for k, (r_, rho) in stats.items():
+            print("%-14s Pearson r = %.3f  Spearman rho = %.3f" % (k, r_, rho))
         return 0
     table, r_, rho = correlate(a.order, a.fetch_csv, a.fetch_scale)
     print("schedules %d  Pearson r = %.3f  Spearman rho = %.3f" % (len(table), r_, rho))

@@ -90,3 +90,31 @@ def test_correlate_matches_rows_to_schedules(tmp_path):
     # both schedules fit the same resident footprint: a constant prediction
     assert table[0]["predicted"] == table[1]["predicted"]
     assert r != r and rho != rho          # NaN: correlation undefined
+
+
+# ---------------------------------------------------- DRAM behind the MALL
+
+
+def test_dram_is_compulsory_when_operands_fit_the_mall():
+    # 8192^3 bf16: A and B are 256 MiB, the MALL's size; every order reads them once
+    for raster in (0, 1, 4, 8):
+        for xcd in (0, 1):
+            d = tm.predict_dram(8192, 8192, 8192, 2, 256, 256, raster, xcd, 1)
+            assert d == 2 * 8192 * 8192 * 2
+
+
+def test_dram_between_compulsory_and_l2_misses():
+    M, N, K = 16384, 16384, 8192
+    for raster in (0, 1, 2, 4, 8, 16, 32):
+        for xcd in (0, 1):
+            d = tm.predict_dram(M, N, K, 2, 256, 256, raster, xcd, 1)
+            l2, _ = tm.predict(M, N, K, 2, 256, 256, raster, xcd, 1)
+            assert (M + N) * K * 2 <= d <= l2
+
+
+def test_dram_falls_with_a_larger_last_level_cache():
+    M, N, K = 16384, 16384, 8192
+    small = tm.predict_dram(M, N, K, 2, 256, 256, 0, 0, 1, mall_bytes=64 << 20)
+    mid = tm.predict_dram(M, N, K, 2, 256, 256, 0, 0, 1, mall_bytes=256 << 20)
+    huge = tm.predict_dram(M, N, K, 2, 256, 256, 0, 0, 1, mall_bytes=4 << 30)
+    assert small >= mid >= huge == (M + N) * K * 2
