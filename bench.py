@@ -52,7 +52,7 @@ KERNEL_SOURCES = {
     "f32": ["gemm_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h"],
     "bf16": ["gemm_bf16.hip", "mfma_bf16.h", "tile_map.h", "lds_dma.h"],
     "conv": ["conv2d_f32.hip", "mfma_f32.h", "tile_map.h", "lds_dma.h", "unroll.h"],
-    "conv_bf16": ["conv2d_bf16.hip", "mfma_bf16.h", "tile_map.h"],
+    "conv_bf16": ["conv2d_bf16.hip", "lds_dma.h", "mfma_bf16.h", "tile_map.h"],
 }
 
 

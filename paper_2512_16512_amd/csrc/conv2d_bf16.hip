@@ -13,6 +13,7 @@
 // 16-byte aligned).  The fragments are those of the bf16 GEMM: one
 // ds_read_b128 per A fragment from k-contiguous padded rows, and two gfx950
 // transpose reads per B fragment from the pixel-contiguous B tile.
+#include "lds_dma.h"
 #include "mfma_bf16.h"
 #include "tile_map.h"
 #include "xtc_internal.h"
@@ -263,7 +264,7 @@ static_assert(2 * BM <= NT, "one weight slab per thread");
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-__global__ void __launch_bounds__(halo_bf16::NT)
+__global__ void __launch_bounds__(halo_bf16::NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 conv2d_bf16_halo_kernel(ConvArgs p) {
     using namespace halo_bf16;
     typedef Bf16Mfma<MI> MF;
@@ -285,11 +286,10 @@ conv2d_bf16_halo_kernel(ConvArgs p) {
     const int ih0 = oh0 - p.ph;               // input row of patch row 0
     const int KT = C / CC;
 
-    const unsigned *__restrict__ X = reinterpret_cast<const unsigned *>(p.X);    // bf16 pairs
-    const u32x4_t *__restrict__ Wv = reinterpret_cast<const u32x4_t *>(p.Wt);   // 16-byte chunks
-
-    // Patch loads: patch row pr, column pair cp (input columns 2cp - CO, +1).
-    // Out-of-image pairs read a clamped in-range dword and are stored as zero.
+    // Patch loads: patch row pr, column pair cp (input columns 2cp - CO, +1),
+    // through a buffer resource: one offset per thread, the channel step in a
+    // scalar offset, and pairs outside the image at an out-of-range offset,
+    // which reads zeros.
     const int pr = tid >> 5, cp = tid & 31;
     const int prot = (pr * OW) & 15;            // rotation of this patch row
     const bool sw = (cp >> 2) & 1;              // store order of the two cells
@@ -297,8 +297,15 @@ conv2d_bf16_halo_kernel(ConvArgs p) {
     const int cell1 = (pr * PCA + 2 * cp + prot + (sw ? 0 : 1)) * CELL;
     const int ih = ih0 + pr, iw = 2 * cp - CO;
     const bool pok = ih >= 0 && ih < H && iw >= 0 && iw + 1 < Wd;
-    const int HW2 = H * Wd / 2;                                     // dwords per channel plane
-    const int pbase = pok ? img * C * HW2 + (ih * Wd + iw) / 2 : 0;
+    // dwords per channel plane; read into a scalar register, since the
+    // compiler otherwise recomputes it on both sides of the divergent select
+    // below and then holds it per lane, which turns every buffer load that
+    // takes it as a scalar offset into a loop over lanes
+    const int HW2 = __builtin_amdgcn_readfirstlane(H * Wd / 2);
+    const int xoff = pok ? (img * C * HW2 + (ih * Wd + iw) / 2) * 4 : kOOB;
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short *>(reinterpret_cast<const unsigned short *>(p.X)), 0,
+        p.Nb * C * HW2 * 4, 0x00020000);
     // Weight loads (threads 0 .. 2*BM-1): output channel m0 + woc, channels
     // 8*wh .. 8*wh+7 of the stage, all nine taps: nine 16-byte chunks.
     const int woc = tid >> 1, wh = tid & 1;
@@ -307,31 +314,43 @@ conv2d_bf16_halo_kernel(ConvArgs p) {
     const int wslot = (woc * CC + 8 * (wh ^ ((woc >> 3) & 1))) * 2;
     const bool wthr = tid < 2 * BM;
     const bool wok = wthr && m0 + woc < OC;
-    const int wbase = wok ? ((m0 + woc) * C + 8 * wh) / 8 * NTAP : 0;
+    const int woff = wok ? ((m0 + woc) * C + 8 * wh) * NTAP * 2 : kOOB;
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short *>(reinterpret_cast<const unsigned short *>(p.Wt)), 0,
+        OC * C * NTAP * 2, 0x00020000);
 
-    unsigned xs[CC];
-    u32x4_t ws[NTAP];
-    auto gload = [&](int kt) __attribute__((always_inline)) {
-        const int c0 = kt * CC;
+    // two register sets, so that the loads of a stage are in flight for two
+    // stages' worth of matrix work before they are stored
+    unsigned xs[2][CC];
+    u32x4_t ws[2][NTAP];
+    // Loads of stage kt into set S.  Past the last stage (live false) the
+    // offsets are out of range: the loads return zeros without touching
+    // memory.  Loads under a branch would make the compiler's wait before
+    // each store count conservatively, and wait for loads it does not need.
+    auto gload = [&](auto S, int kt, bool live) __attribute__((always_inline)) {
+        const int c0 = live ? kt * CC : 0;
+        const int xo = live ? xoff : kOOB, wo = live ? woff : kOOB;
 #pragma unroll
-        for (int c = 0; c < CC; ++c) xs[c] = X[pbase + (c0 + c) * HW2];
-        if (wthr) {
+        for (int c = 0; c < CC; ++c)
+            xs[S][c] = __builtin_amdgcn_raw_buffer_load_b32(rx, xo, (c0 + c) * HW2 * 4, 0);
+        // every thread issues the weight loads (threads without a slab at an
+        // out-of-range offset), so that all waves count the same loads
 #pragma unroll
-            for (int q = 0; q < NTAP; ++q) ws[q] = Wv[wbase + c0 / 8 * NTAP + q];
-        }
+        for (int q = 0; q < NTAP; ++q)
+            ws[S][q] = __builtin_amdgcn_raw_buffer_load_b128(rw, wo, c0 * NTAP * 2 + q * 16, 0);
     };
-    // halfword e (0 .. 71) of the weight slab
-    auto wv = [&](int e) __attribute__((always_inline)) {
-        return (ws[e >> 3][(e >> 1) & 3] >> (16 * (e & 1))) & 0xffffu;
+    // halfword e (0 .. 71) of the weight slab in set S
+    auto wv = [&](auto S, int e) __attribute__((always_inline)) {
+        return (ws[S][e >> 3][(e >> 1) & 3] >> (16 * (e & 1))) & 0xffffu;
     };
-    auto lstore = [&](int buf) __attribute__((always_inline)) {
-        unsigned char *P = smem + buf * STAGE_BYTES;
+    auto lstore = [&](auto S) __attribute__((always_inline)) {
+        unsigned char *P = smem + S * STAGE_BYTES;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             u32x4_t lo, hi;   // columns 2cp and 2cp + 1
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const unsigned a = pok ? xs[8 * h + 2 * j] : 0u, b = pok ? xs[8 * h + 2 * j + 1] : 0u;
+                const unsigned a = xs[S][8 * h + 2 * j], b = xs[S][8 * h + 2 * j + 1];
                 lo[j] = (a & 0xffffu) | (b << 16);
                 hi[j] = (a >> 16) | (b & 0xffff0000u);
             }
@@ -349,7 +368,7 @@ conv2d_bf16_halo_kernel(ConvArgs p) {
                 u32x4_t v;
 #pragma unroll
                 for (int d = 0; d < 4; ++d)
-                    v[d] = wok ? (wv(2 * d * NTAP + t) | (wv((2 * d + 1) * NTAP + t) << 16)) : 0u;
+                    v[d] = wv(S, 2 * d * NTAP + t) | (wv(S, (2 * d + 1) * NTAP + t) << 16);
                 *reinterpret_cast<u32x4_t *>(Wl + t * BM * CC * 2 + wslot) = v;
             }
         }
@@ -401,23 +420,34 @@ conv2d_bf16_halo_kernel(ConvArgs p) {
             for (int j = 0; j < TN; ++j) acc[i][j] = MF::mma(af[fb][i], bfr[fb][j], acc[i][j]);
     };
 
-    // Register-staged double buffer, branch-free: the loads of stage kt + 1
-    // (stage kt again on the last iteration) are issued before the nine taps
-    // of stage kt and stored into the other buffer after them.
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < KT; ++kt) {
-        const int cur = kt & 1;
-        gload(kt + 1 < KT ? kt + 1 : kt);
-        load_frags(cur, 0, 0);
+    // Stage kt is computed from LDS buffer kt % 2, which register set kt % 2
+    // filled; that set then takes the loads of stage kt + 2, and set
+    // (kt + 1) % 2, loaded a stage earlier, is stored into the other buffer
+    // after the nine taps.
+    const std::integral_constant<int, 0> S0;
+    const std::integral_constant<int, 1> S1;
+    auto stage = [&](auto S, int kt) __attribute__((always_inline)) {
+        constexpr int NS = 1 - decltype(S)::value;
+        gload(S, kt + 2, kt + 2 < KT);
+        // keep the loads ahead of the taps (the scheduler would otherwise sink
+        // them to the end of the stage, one stage before their use)
+        __builtin_amdgcn_sched_barrier(0);
+        load_frags(S, 0, 0);
 #pragma unroll
         for (int t = 0; t < NTAP; ++t) {
-            if (t + 1 < NTAP) load_frags(cur, t + 1, (t + 1) & 1);
+            if (t + 1 < NTAP) load_frags(S, t + 1, (t + 1) & 1);
             mfmas(t & 1);
         }
-        lstore(cur ^ 1);
+        if (kt + 1 < KT) lstore(std::integral_constant<int, NS>());
         __syncthreads();
+    };
+    gload(S0, 0, true);
+    gload(S1, 1, KT > 1);
+    lstore(S0);
+    __syncthreads();
+    for (int kt = 0; kt < KT; kt += 2) {
+        stage(S0, kt);
+        if (kt + 1 < KT) stage(S1, kt + 1);
     }
 
     float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;

@@ -78,6 +78,8 @@ def test_matmul_workload_parity(x, ci):
     (2, 32, 54, 52, 70, 3, 3, 1, 1),    # halo: OC = 70 (ragged second weight tile), two stages
     (1, 16, 57, 56, 20, 3, 3, 1, 0),    # halo: no padding (55 x 54 output)
     (1, 48, 56, 58, 16, 3, 3, 1, 2),    # halo: pad 2 (60-wide output rows), three stages
+    (1, 64, 56, 56, 64, 3, 3, 1, 1),    # halo: four stages (both register sets twice)
+    (1, 80, 21, 56, 40, 3, 3, 1, 1),    # halo: five stages, OC = 40
 ])
 def test_conv_bf16_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape
