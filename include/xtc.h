@@ -113,7 +113,15 @@ typedef enum {
  *                  bf16: chunks of 16, k = ((ic/16)*R*S + kh*S + kw)*16 +
  *                  ic%16, needs C % 16 == 0, even W, pad_w <= 2,
  *                  OW - pad_w <= 60, a 4-byte-aligned X and a 16-byte-
- *                  aligned W; other shapes run the channel-major kernel.
+ *                  aligned W; other shapes run the channel-major kernel;
+ *                3: bf16 only, row streaming for 3x3 stride-1 layers of 64
+ *                input channels: a workgroup walks down a band of output
+ *                rows of one image with all C*R*S weights of its 64 output
+ *                channels resident; k = ((kw*4 + ic/16)*3 + kh)*16 + ic%16
+ *                per output row.  Needs C == 64, even W, OW % 4 == 0,
+ *                OW <= 64, pad_w <= 2, OW + 3 - pad_w <= 63, a 4-byte-
+ *                aligned X and 16-byte-aligned W and Y; other shapes run the
+ *                k_order 2 kernel.
  *                Results differ only by rounding order.
  *  k_split       waves that share one workgroup tile, each reducing every
  *                k_split-th group of block_k reduction steps (a parallel

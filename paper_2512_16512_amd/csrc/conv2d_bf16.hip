@@ -491,6 +491,356 @@ hipError_t launch_conv_bf16_halo(const ConvArgs &a, hipStream_t s) {
                            dim3(halo_bf16::NT), kargs, 0, s);
 }
 
+// ---------------------------------------------------------------------------
+// Row-streaming bf16 kernel (k_order = 3) for stride-1 3x3 convolutions of 64
+// input channels with output rows of at most 64 pixels.  With bf16 inputs such
+// a layer does about 190 FLOP per HBM byte, below the matrix cores' ridge
+// (about 315), so the kernel is laid out for streaming X in and Y out at HBM
+// rate rather than for matrix-core reuse:
+//  - a workgroup owns 64 output channels of one image and a band of
+//    consecutive output rows, and walks down the band RO = 2 output rows per
+//    step, so that each input row enters LDS once per band and the output
+//    of a step is written while the following rows are computed;
+//  - all C*R*S = 576 weights of its 64 output channels stay in LDS for the
+//    whole band (72 KiB, loaded once);
+//  - input rows pass through a ring of NR = 8 LDS rows: the four rows a step
+//    reads, the two the next step adds (stored at the start of the step,
+//    published by the step's barrier) and two slots free for refilling; the
+//    loads of the rows a step adds are issued two steps ahead, into one of
+//    two register sets;
+//  - wave w computes 32 output channels (half w & 1) x 32 pixels (half
+//    w >> 1) of both output rows with 32x32x16 instructions, pixels as the
+//    row operand and output channels as the column operand;
+//  - one fragment of input row r (32 pixels, 8 channels, one column shift
+//    kw) serves every output row of the step that reads row r, one per
+//    kernel row kh: four input rows feed the 2 x 3 (output row, kh) pairs.
+//    Per 16-channel k-step a wave reads 4 + 3 fragments for 6 instructions,
+//    which keeps LDS below the matrix cores' rate and a group's reads within
+//    the 15 the LDS counter can wait past;
+//  - an input row is stored channel-innermost, one 16-byte cell of 8
+//    channels per (column, 8-channel group), 64 columns with input column iw
+//    at column iw + CO and zeros outside the image.  Group g of column c sits
+//    at slot g ^ h(c), h(c) = ((c >> 1) ^ (c & ~3)) & 7, which keeps both the
+//    fragment reads (each phase: 16 lanes of a 32-column run, one group) and
+//    the staging writes (8 lanes of consecutive column pairs per phase, each
+//    lane writing its two cells in an order that alternates every four
+//    lanes) free of bank conflicts at every column shift;
+//  - a weight cell holds 8 channels of one (tap, output channel); the eight
+//    cells of output channel o sit at slots g ^ h(o), the same pattern, since
+//    a weight fragment (32 output channels x two groups) is addressed like a
+//    pixel fragment.
+namespace rows_bf16 {
+constexpr int NT = 256;                   // four waves
+constexpr int BM = 64;                    // output channels per workgroup
+constexpr int CH = 64;                    // input channels (all resident)
+constexpr int NCG = CH / 8;               // 8-channel cells per column
+constexpr int NKS = CH / 16;              // 16-channel instruction k-steps per tap
+constexpr int NTAP = 9;
+constexpr int RO = 2;                     // output rows per step
+constexpr int NR = 8;                     // input rows in the ring
+constexpr int PC = 64;                    // stored columns per input row
+constexpr int CO = 2;                     // stored column of input column 0 (even)
+constexpr int ROWB = PC * NCG * 16;       // bytes per stored input row
+constexpr int RING_BYTES = NR * ROWB;
+constexpr int W_BYTES = NTAP * BM * NCG * 16;
+constexpr int LDS_BYTES = RING_BYTES + W_BYTES;
+static_assert(NT == 32 * NCG, "one (column pair, cell group) per thread");
+static_assert(2 * NT == BM * NCG, "two weight slabs per thread");
+static_assert(NR >= 3 * RO + 2, "ring: a step's rows, the next step's, and the slots being refilled");
+// slot swizzle of the cells of one column (or output channel)
+__device__ __forceinline__ int swz(int c) { return ((c >> 1) ^ (c & ~3)) & 7; }
+}  // namespace rows_bf16
+
+__global__ void __launch_bounds__(rows_bf16::NT)
+conv2d_bf16_rows_kernel(ConvArgs p) {
+    using namespace rows_bf16;
+    typedef Bf16Mfma<32> MF;
+    __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, lg = lane >> 5;
+
+    const int H = p.H, Wd = p.W, OC = p.OC, OH = p.OH, OW = p.OW;
+    const int band_rows = p.tile_px;
+    const int nbands = (OH + band_rows - 1) / band_rows;
+    const int tiles_m = (OC + BM - 1) / BM, tiles_n = p.Nb * nbands;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, p.raster, p.xcd_remap, tm, tn);
+    const int m0 = tm * BM;
+    const int img = tn / nbands, band = tn - img * nbands;
+    const int oh_a = band * band_rows;
+    const int rows = min(band_rows, OH - oh_a);   // output rows of the band
+    const int nsteps = (rows + RO - 1) / RO;
+    const int ih0 = oh_a - p.ph;                   // input row of band row 0
+    const int nin = RO * nsteps + 2;               // input rows the band reads
+
+    // ---- input rows: thread (q, g) loads column pair q (input columns
+    // 2q - CO, +1) of channels 8g .. 8g+7, one dword per channel; rows and
+    // pairs outside the image are read at an out-of-range offset (zeros).
+    const int q = tid & 31, g = tid >> 5;
+    const int iwp = 2 * q - CO;
+    const bool colok = iwp >= 0 && iwp + 1 < Wd;
+    const int plane = __builtin_amdgcn_readfirstlane(H * Wd * 2);      // bytes per channel plane
+    const int xcol = ((img * CH + 8 * g) * H) * Wd * 2 + iwp * 2;
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(p.X), 0, p.Nb * CH * plane, 0x00020000);
+    // Two register sets.  Loads and output stores are unconditional
+    // (out-of-range offsets instead of branches), so the compiler's counted
+    // waits before a set is stored do not include the stores issued after
+    // its loads.
+    unsigned xv[2][RO][8];
+    auto load_rows = [&](auto S, int r0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < RO; ++i) {
+            const int r = r0 + i, ih = ih0 + r;
+            const bool ok = colok & (r < nin) & (ih >= 0) & (ih < H);
+            const int o = ok ? xcol + ih * Wd * 2 : kOOB;
+#pragma unroll
+            for (int c = 0; c < 8; ++c)
+                xv[S][i][c] = __builtin_amdgcn_raw_buffer_load_b32(rx, o, c * plane, 0);
+        }
+    };
+    // the thread's two cells; lanes with bit 2 of q set write their odd
+    // column first
+    const bool wodd = (q >> 2) & 1;
+    const int c0 = 2 * q + (wodd ? 1 : 0), c1 = 2 * q + (wodd ? 0 : 1);
+    const int cell0 = c0 * (NCG * 16) + ((g ^ swz(c0)) << 4);
+    const int cell1 = c1 * (NCG * 16) + ((g ^ swz(c1)) << 4);
+    auto store_rows = [&](auto S, int r0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < RO; ++i) {
+            unsigned char *R = smem + ((r0 + i) % NR) * ROWB;
+            u32x4_t ev, od;   // columns 2q and 2q + 1
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const unsigned a = xv[S][i][2 * j], b = xv[S][i][2 * j + 1];
+                ev[j] = (a & 0xffffu) | (b << 16);
+                od[j] = (a >> 16) | (b & 0xffff0000u);
+            }
+            *reinterpret_cast<u32x4_t *>(R + cell0) = wodd ? od : ev;
+            *reinterpret_cast<u32x4_t *>(R + cell1) = wodd ? ev : od;
+        }
+    };
+
+    // ---- weights: slab s (= tid, tid + NT) is output channel s >> 3,
+    // channels 8(s & 7) .. +7, all nine taps: 72 contiguous values of the
+    // OIHW row, nine 16-byte loads, repacked into one cell per tap.
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(p.Wt), 0, OC * CH * NTAP * 2, 0x00020000);
+    unsigned char *const Wl = smem + RING_BYTES;
+    const std::integral_constant<int, 0> S0;
+    const std::integral_constant<int, 1> S1;
+    // prologue: the weights first (they come from L2, and the in-order
+    // memory counter would otherwise make their wait include the input
+    // rows' HBM latency), then band rows 0 .. 3; rows 4, 5 (set 1) and 6, 7
+    // (set 0) stay in flight
+    u32x4_t ws[2][NTAP];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int s = tid + h * NT;
+        const int oc = s >> 3, wg = s & 7;
+        const int off = m0 + oc < OC ? ((m0 + oc) * CH + 8 * wg) * NTAP * 2 : kOOB;
+#pragma unroll
+        for (int t = 0; t < NTAP; ++t) ws[h][t] = __builtin_amdgcn_raw_buffer_load_b128(rw, off, 16 * t, 0);
+    }
+    load_rows(S0, 0);
+    load_rows(S1, RO);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int s = tid + h * NT;
+        const int oc = s >> 3, wg = s & 7;
+        auto wv = [&](int e) __attribute__((always_inline)) {   // halfword e = channel e / 9, tap e % 9
+            return (ws[h][e >> 3][(e >> 1) & 3] >> (16 * (e & 1))) & 0xffffu;
+        };
+        const int slot = oc * (NCG * 16) + ((wg ^ swz(oc)) << 4);
+#pragma unroll
+        for (int t = 0; t < NTAP; ++t) {
+            u32x4_t v;
+#pragma unroll
+            for (int d = 0; d < 4; ++d) v[d] = wv(2 * d * NTAP + t) | (wv((2 * d + 1) * NTAP + t) << 16);
+            *reinterpret_cast<u32x4_t *>(Wl + t * BM * NCG * 16 + slot) = v;
+        }
+    }
+    store_rows(S0, 0);
+    store_rows(S1, RO);
+    load_rows(S1, 2 * RO);
+    load_rows(S0, 3 * RO);
+    __syncthreads();
+
+    // ---- fragment offsets.  B (weights): output channel 32*(wave & 1) +
+    // l32, group 2*kstep + lg.  A (pixels): pixel 32*(wave >> 1) + l32 of the
+    // output row (lanes past OW read a valid cell and are not stored),
+    // column shift kw, group 2*kstep + lg.
+    const int oc_l = 32 * (wave & 1) + l32;
+    // lanes past OW take the pixel 32 to the left (same banks, so the read
+    // stays conflict-free), or the last pixel when there is none
+    int px_l = 32 * (wave >> 1) + l32;
+    if (px_l >= OW) px_l = px_l >= 32 && px_l - 32 < OW ? px_l - 32 : OW - 1;
+    int b_off[NKS], a_off[3][NKS];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+        b_off[ks] = oc_l * (NCG * 16) + (((2 * ks + lg) ^ swz(oc_l)) << 4);
+#pragma unroll
+        for (int kw = 0; kw < 3; ++kw) {
+            const int col = px_l + kw - p.pw + CO;
+            a_off[kw][ks] = col * (NCG * 16) + (((2 * ks + lg) ^ swz(col)) << 4);
+        }
+    }
+
+    // ---- output: lane (l32, lg) of wave w holds, per output row, pixels
+    // 32*(w >> 1) + 8i + 4lg .. +3 (i = 0..3) of output channel m0 + oc_l:
+    // four 16-byte stores per row, at an out-of-range offset where the
+    // channel, row or pixels are outside Y (the store is then dropped).
+    const int oc_st = m0 + oc_l;
+    const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
+        p.Y, 0, p.Nb * OC * OH * OW * 4, 0x00020000);
+    const int ybase = ((img * OC + min(oc_st, OC - 1)) * OH + oh_a) * OW * 4;
+    const int px_st = 32 * (wave >> 1) + 4 * lg;
+    // A step's outputs are stored during the next step, one store per
+    // k-step group, and its row loads are spread the same way: with one
+    // wave per SIMD a burst of memory instructions stalls the wave at the
+    // memory queue while its matrix instructions wait behind them.
+    constexpr int NPART = RO * 4;               // output stores (and load pairs) per step
+    f32x4 pend[NPART];
+    int pend_off[NPART];
+#pragma unroll
+    for (int k = 0; k < NPART; ++k) pend_off[k] = kOOB;
+    auto store_part = [&](int k) __attribute__((always_inline)) {
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, pend[k]), ry, pend_off[k], 0, 0);
+    };
+    // loads of band rows r0, r0 + 1 into set S, part k: row k / 4, channels
+    // 2(k % 4), +1
+    auto load_part = [&](auto S, int r0, int k) __attribute__((always_inline)) {
+        const int i = k / 4, r = r0 + i, ih = ih0 + r;
+        const bool ok = colok & (r < nin) & (ih >= 0) & (ih < H);
+        const int o = ok ? xcol + ih * Wd * 2 : kOOB;
+#pragma unroll
+        for (int c = 2 * (k % 4); c < 2 * (k % 4) + 2; ++c)
+            xv[S][i][c] = __builtin_amdgcn_raw_buffer_load_b32(rx, o, c * plane, 0);
+    };
+
+    // Fragments: the (kw, k-step) groups of a step in order, double-buffered
+    // in registers.  The reads of the next group are issued between the
+    // matrix instructions of the current one (a run of reads would likewise
+    // stall the wave at the LDS queue), and the last group of a step reads
+    // the first group of the next step.
+    constexpr int NGRP = 3 * NKS;
+    constexpr int NREAD = 3 + RO + 2;            // reads per group
+    constexpr int NMMA = 3 * RO;                 // instructions per group
+    static_assert(NGRP % 2 == 0 && NREAD >= NMMA && NGRP - 1 >= NPART, "group parity and interleave");
+    u16x8 af[2][RO + 2], bf[2][3];
+    auto frags = [&](int fb, int grp, int st) __attribute__((always_inline)) {
+        const int kw = grp / NKS, ks = grp % NKS;
+#pragma unroll
+        for (int kh = 0; kh < 3; ++kh)
+            bf[fb][kh] = *reinterpret_cast<const u16x8 *>(Wl + (kh * 3 + kw) * BM * NCG * 16 + b_off[ks]);
+#pragma unroll
+        for (int i = 0; i < RO + 2; ++i)
+            af[fb][i] = *reinterpret_cast<const u16x8 *>(smem + ((RO * st + i) % NR) * ROWB + a_off[kw][ks]);
+    };
+    auto interleave = [&](bool mem) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < NMMA; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+            if (mem && i == 1) __builtin_amdgcn_sched_group_barrier(0x040, 1, 0);   // the store
+            if (mem && i == 3) __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);   // the loads
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, NREAD - NMMA, 0);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    auto step = [&](auto S, int st) __attribute__((always_inline)) {
+        // the next step's new rows into the ring (their slots were last read
+        // two steps ago); the loads of the rows three steps ahead go into
+        // the set this frees, spread over the groups below
+        store_rows(S, RO * st + RO + 2);
+        typename MF::acc_t acc[RO];
+#pragma unroll
+        for (int o = 0; o < RO; ++o)
+#pragma unroll
+            for (int r = 0; r < MF::NACC; ++r) acc[o][r] = 0.f;
+        auto mmas = [&](int fb) __attribute__((always_inline)) {
+#pragma unroll
+            for (int kh = 0; kh < 3; ++kh)
+#pragma unroll
+                for (int o = 0; o < RO; ++o) acc[o] = MF::mma(af[fb][o + kh], bf[fb][kh], acc[o]);
+        };
+#pragma unroll
+        for (int grp = 0; grp + 1 < NGRP; ++grp) {
+            frags((grp + 1) & 1, grp + 1, st);
+            mmas(grp & 1);
+            if (grp < NPART) {
+                store_part(grp);
+                load_part(S, RO * st + 3 * RO + 2, grp);
+            }
+            interleave(grp < NPART);
+        }
+        // every wave has stored the next step's rows and finished the
+        // previous step's reads
+        __syncthreads();
+        frags(0, 0, st + 1);
+        mmas(1);
+        interleave(false);
+        // this step's outputs, stored during the next step
+#pragma unroll
+        for (int o = 0; o < RO; ++o) {
+            const bool rok = (oc_st < OC) & (RO * st + o < rows);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int k = 4 * o + i, px = px_st + 8 * i;
+                pend_off[k] = (rok & (px < OW)) ? ybase + ((RO * st + o) * OW + px) * 4 : kOOB;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float v = acc[o][4 * i + r];
+                    // write-back stores: the pieces of a line written by
+                    // several instructions merge in L2 (nontemporal stores
+                    // of partial lines cost whole lines of HBM writes)
+                    pend[k][r] = (p.relu && v < 0.f) ? 0.f : v;
+                }
+            }
+        }
+    };
+    frags(0, 0, 0);
+    for (int st = 0; st < nsteps; st += 2) {
+        step(S1, st);
+        if (st + 1 < nsteps) step(S0, st + 1);
+    }
+#pragma unroll
+    for (int k = 0; k < NPART; ++k) store_part(k);
+}
+
+// Shapes the row-streaming kernel covers; anything else runs the halo-tiled
+// kernel (which itself falls back to the gather kernel).
+inline bool bf16_rows_eligible(const ConvArgs &a) {
+    using namespace rows_bf16;
+    if (a.R != 3 || a.S != 3 || a.sh != 1 || a.sw != 1) return false;
+    if (a.C != CH || a.W % 2 != 0 || a.pw > CO || a.OW % 4 != 0 || a.OW > 64) return false;
+    if (a.OW + 1 - a.pw + CO > PC - 1) return false;   // last stored column a fragment reads
+    if ((reinterpret_cast<uintptr_t>(a.X) & 3) != 0 || (reinterpret_cast<uintptr_t>(a.Wt) & 15) != 0 ||
+        (reinterpret_cast<uintptr_t>(a.Y) & 15) != 0)
+        return false;
+    return true;
+}
+
+hipError_t launch_conv_bf16_rows(const ConvArgs &a, hipStream_t s) {
+    if (!bf16_rows_eligible(a)) return launch_conv_bf16_halo(a, s);
+    // bands sized so that the workgroups (one per CU: the LDS holds one)
+    // cover the 256 CUs about once
+    const int octiles = (a.OC + rows_bf16::BM - 1) / rows_bf16::BM;
+    const int per_img = octiles * a.Nb;
+    int nb = (256 + per_img - 1) / per_img;
+    ConvArgs args = a;
+    args.tile_px = (a.OH + nb - 1) / nb;   // output rows per band, at least a step's
+    if (args.tile_px < rows_bf16::RO) args.tile_px = rows_bf16::RO;
+    const int nbands = (a.OH + args.tile_px - 1) / args.tile_px;
+    args.xcd_remap = 1;
+    void *kargs[] = {&args};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_bf16_rows_kernel),
+                           dim3((unsigned)(per_img * nbands)), dim3(rows_bf16::NT), kargs, 0, s);
+}
+
 #define XTC_CONV_BF16_INSTANCE(BM, BN, BK, WM, WN, MI, PAD)                                   \
     ConvInstance {                                                                            \
         make_sched(BM, BN, BK, WM, WN, MI, MI, (MI == 32 ? 16 : 32), 2, PAD, 0),               \
@@ -503,6 +853,9 @@ const ConvInstance kConvBf16Instances[] = {
     ConvInstance{make_sched(64, 256, 16, 64, 64, 32, 32, 16, 2, -1, 0, 2),  // halo, 3x3 stride 1
                  &launch_conv_bf16_halo,
                  &occupancy_of<&conv2d_bf16_halo_kernel, halo_bf16::NT, 0>},
+    ConvInstance{make_sched(64, 64, 16, 32, 32, 32, 32, 16, 2, -1, 0, 3),  // row streaming, 3x3 s1, C 64
+                 &launch_conv_bf16_rows,
+                 &occupancy_of<&conv2d_bf16_rows_kernel, rows_bf16::NT, 0>},
     XTC_CONV_BF16_INSTANCE(64, 128, 32, 32, 64, 32, 8),   // default for OC <= 64
     XTC_CONV_BF16_INSTANCE(128, 128, 32, 64, 64, 32, 8),  // default for OC > 64
     XTC_CONV_BF16_INSTANCE(64, 64, 32, 32, 32, 32, 8),    // few output pixels

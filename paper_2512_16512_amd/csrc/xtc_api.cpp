@@ -85,7 +85,7 @@ xtc_status legal(xtc_op op, xtc_dtype dt, const xtc_sched &s) {
     if (s.unroll_k < 0) return XTC_ERR_BAD_SCHEDULE;
     if (s.raster < 0 || s.raster > kMaxRaster || s.xcd_remap < 0 || s.xcd_remap > 1)
         return XTC_ERR_BAD_SCHEDULE;
-    if (s.k_order < 0 || s.k_order > 2 || (op == XTC_OP_MATMUL && s.k_order != 0))
+    if (s.k_order < 0 || s.k_order > 3 || (op == XTC_OP_MATMUL && s.k_order != 0))
         return XTC_ERR_BAD_SCHEDULE;
     // LDS budget of the staged tiles
     const int elt = dt == XTC_F32 ? 4 : 2;
@@ -161,11 +161,14 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     const int64_t cus = 256;
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     if (op == XTC_OP_CONV2D && dt == XTC_BF16) {
-        // the halo-tiled kernel (64x256 tiles; it runs the 64x128 gather
-        // kernel for shapes outside its class: not 3x3 stride 1, odd widths,
-        // rows far from 56 pixels); the gather kernel with 128x128 tiles for
-        // more than 64 output channels, 64x64 when 64x128 tiles leave CUs idle
-        *out = make_sched(64, 256, 16, 64, 64, 32, 32, 16, 2, -1, 0, 2);
+        // the row-streaming kernel (3x3 stride 1, 64 input channels, rows of
+        // at most 64 pixels; 32x64x56x56 -> 64: 15.3 us kernel span against
+        // 17 us for the halo-tiled kernel), which runs the halo-tiled kernel
+        // outside its class, and that one the 64x128 gather kernel outside
+        // its own (not 3x3 stride 1, odd widths, rows far from 56 pixels);
+        // the gather kernel with 128x128 tiles for more than 64 output
+        // channels, 64x64 when 64x128 tiles leave CUs idle
+        *out = make_sched(64, 64, 16, 32, 32, 32, 32, 16, 2, -1, 0, 3);
         if (M > 64)
             *out = make_sched(128, 128, 32, 64, 64, 32, 32, 16, 2, 8, 0);
         else if (tiles(64, 128) < cus)

@@ -335,6 +335,84 @@ def conv_bf16_halo_launch(N, C, H, W, OC, pad_h, pad_w, a_swizzle=False, rotate=
     return total.scaled(_cdiv(OC, BM) * N)
 
 
+def rows_swz(c: int) -> int:
+    """Cell-slot swizzle of the bf16 row-streaming conv (csrc/conv2d_bf16.hip)."""
+    return ((c >> 1) ^ (c & ~3)) & 7
+
+
+def conv_bf16_rows_launch(N, C, H, W, OC, pad_h, pad_w) -> LdsCost:
+    """One launch of the bf16 row-streaming conv (3x3, stride 1, 64 input
+    channels; csrc/conv2d_bf16.hip, k_order 3).  Per workgroup: the weight
+    cells (ds_write_b128, two slabs of nine taps per thread) and band rows 0
+    .. 3 once; per step of two output rows, the two new input rows (two
+    ds_write_b128 per thread and row) and, per wave and (kw, 16-channel
+    k-step) group, three weight and four pixel fragments (ds_read_b128);
+    plus the first group of the step after the last."""
+    assert C == 64
+    BM, NCG, RO, CO = 64, 8, 2, 2
+    OH, OW = H + 2 * pad_h - 2, W + 2 * pad_w - 2
+    per_img = _cdiv(OC, BM) * N
+    nb = _cdiv(256, per_img)
+    band = max(_cdiv(OH, nb), RO)
+    nbands = _cdiv(OH, band)
+    row_w = LdsCost()           # one input row into the ring (every thread)
+    for wave in range(4):
+        for second in range(2):
+            addrs = []
+            for lane in range(64):
+                tid = wave * 64 + lane
+                q, g = tid & 31, tid >> 5
+                wodd = (q >> 2) & 1
+                col = 2 * q + (wodd ^ second)
+                addrs.append(col * NCG * 16 + ((g ^ rows_swz(col)) << 4))
+            row_w.add("ds_write_b128", addrs)
+    weights = LdsCost()
+    for wave in range(4):
+        for h in range(2):
+            for t in range(9):
+                addrs = []
+                for lane in range(64):
+                    s_ = wave * 64 + lane + 256 * h
+                    oc, wg = s_ >> 3, s_ & 7
+                    addrs.append(t * BM * NCG * 16 + oc * NCG * 16 + ((wg ^ rows_swz(oc)) << 4))
+                weights.add("ds_write_b128", addrs)
+    group = LdsCost()           # all (kw, k-step) groups of one step, all waves
+    first_group = LdsCost()     # group (0, 0): also read ahead for the step after the last
+    for wave in range(4):
+        oc_l = [32 * (wave & 1) + lane % 32 for lane in range(64)]
+        px_l = []
+        for lane in range(64):
+            px = 32 * (wave >> 1) + lane % 32
+            if px >= OW:
+                px = px - 32 if (px >= 32 and px - 32 < OW) else OW - 1
+            px_l.append(px)
+        for kw in range(3):
+            for ks in range(C // 16):
+                g = LdsCost()
+                for kh in range(3):
+                    g.add("ds_read_b128", [oc_l[l] * NCG * 16 + (((2 * ks + l // 32) ^ rows_swz(oc_l[l])) << 4)
+                                           for l in range(64)])
+                for i in range(RO + 2):
+                    addrs = []
+                    for l in range(64):
+                        col = px_l[l] + kw - pad_w + CO
+                        addrs.append(col * NCG * 16 + (((2 * ks + l // 32) ^ rows_swz(col)) << 4))
+                    g.add("ds_read_b128", addrs)
+                group += g
+                if kw == 0 and ks == 0:
+                    first_group += g
+    total = LdsCost()
+    for band_i in range(nbands):
+        rows = min(band, OH - band_i * band)
+        nsteps = _cdiv(rows, RO)
+        total += weights
+        total += row_w.scaled(2 * RO)                  # prologue: band rows 0 .. 3
+        total += row_w.scaled(RO * nsteps)             # each step stores the next step's rows
+        total += group.scaled(nsteps)
+        total += first_group
+    return total.scaled(per_img)
+
+
 # ---------------------------------------------------------------- fp32 GEMM
 
 def swz_a_f32(ca: int, row: int) -> int:
@@ -580,6 +658,10 @@ def conv_launch(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
         if span + 2 > (8 if nh == 1 else 10):
             return None
         return conv_f32_halo16_launch(N, C, H, W, OC, ph, pw, nh=nh, a_swizzle=True, tile_px=pt)
+    if dtype == "bf16" and s["k_order"] == 3:
+        if halo_class and C == 64 and W % 2 == 0 and pw <= 2 and OW % 4 == 0 and OW <= 64 and OW + 1 - pw + 2 <= 63:
+            return conv_bf16_rows_launch(N, C, H, W, OC, ph, pw)
+        s = dict(s, k_order=2, block_n=256)   # the launcher falls back to the halo kernel
     if dtype == "bf16" and s["k_order"] == 2:
         span = (256 - 1 + OW - 1) // OW + 1
         if halo_class and C % 16 == 0 and W % 2 == 0 and pw <= 2 and OW - pw + 3 <= 63 and span + 2 <= 8:

@@ -80,6 +80,13 @@ def test_matmul_workload_parity(x, ci):
     (1, 48, 56, 58, 16, 3, 3, 1, 2),    # halo: pad 2 (60-wide output rows), three stages
     (1, 64, 56, 56, 64, 3, 3, 1, 1),    # halo: four stages (both register sets twice)
     (1, 80, 21, 56, 40, 3, 3, 1, 1),    # halo: five stages, OC = 40
+    (2, 64, 9, 8, 40, 3, 3, 1, 1),      # rows: 8-pixel rows, OC = 40 (partial channel tile)
+    (1, 64, 7, 58, 128, 3, 3, 1, 0),    # rows: no padding, 5 output rows, two channel tiles
+    (3, 64, 13, 54, 16, 3, 3, 1, 2),    # rows: pad 2 (56-wide output), OC = 16
+    (1, 64, 56, 56, 70, 3, 3, 1, 1),    # rows: OC = 70
+    (2, 64, 3, 4, 64, 3, 3, 1, 1),      # rows: 4 x 4 output, band taller than the image
+    (16, 64, 40, 16, 64, 3, 3, 1, 1),   # rows: bands of 3 rows (last step half used)
+    (32, 64, 30, 8, 64, 3, 3, 1, 1),    # rows: bands of 4 rows (two full steps), shorter last band
 ])
 def test_conv_bf16_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape
