@@ -1419,7 +1419,7 @@ __host__ __device__ inline PatchGeom patch_geom(const ConvArgs &a, int bn) {
 }
 }  // namespace smallm
 
-template <int NB>
+template <int NB, int NCH>
 __global__ void __launch_bounds__(smallm::NT)
 conv2d_f32_smallm_patch_kernel(ConvArgs p) {
     typedef F32Mfma<16> MF;
@@ -1557,28 +1557,26 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
             for (int r = 0; r < MF::NACC; ++r) acc[h][j][r] = 0.f;
     __syncthreads();
 
-    // k-step s: lane group g takes k = 4s + g.  Steps run in chunks of 8
-    // (KP is a multiple of 32: padded steps have zero weights), through two
-    // register sets: the table entries and weights of chunk c + 1 are read
-    // while chunk c's MFMAs run, and its input values right after them, so
-    // the dependent LDS reads of a step are not waited for one at a time.
-    // Even and odd steps accumulate into two chains.
+    // k-step s: lane group g takes k = 4s + g.  Steps run in NCH chunks of
+    // 8 (KP = 32 * NCH: padded steps have zero weights).  The table entries
+    // of every chunk are read first, in one batch, so that no input read
+    // waits on a table read: the input values and weights of chunk c + 1
+    // are then read while chunk c's MFMAs run.  Even and odd steps
+    // accumulate into two chains.
     const float *wrow = wl + l16 * WS + g;
-    const int NCH = KP / 32;
-    int tv[2][8];
+    int tv[NCH][8];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) tv[c][i] = ktab[32 * c + 4 * i + g];
     float av[2][8], bv[2][NB][8];
-    auto rd_ta = [&](int buf, int c) __attribute__((always_inline)) {
+    auto rd = [&](int buf, int c) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            tv[buf][i] = ktab[32 * c + 4 * i + g];
             av[buf][i] = wrow[32 * c + 4 * i];
+#pragma unroll
+            for (int j = 0; j < NB; ++j) bv[buf][j][i] = patch[pb[j] + tv[c][i]];
         }
-    };
-    auto rd_b = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-#pragma unroll
-            for (int j = 0; j < NB; ++j) bv[buf][j][i] = patch[pb[j] + tv[buf][i]];
     };
     auto mm = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
@@ -1586,17 +1584,22 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
 #pragma unroll
             for (int j = 0; j < NB; ++j) acc[i & 1][j] = MF::mma(av[buf][i], bv[buf][j][i], acc[i & 1][j]);
     };
-    rd_ta(0, 0);
-    rd_b(0);
-    for (int c = 0; c < NCH; c += 2) {
-        const bool n1 = c + 1 < NCH, n2 = c + 2 < NCH;   // uniform
-        if (n1) rd_ta(1, c + 1);
-        mm(0);
-        if (!n1) break;
-        rd_b(1);
-        if (n2) rd_ta(0, c + 2);
-        mm(1);
-        if (n2) rd_b(0);
+    rd(0, 0);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (c + 1 < NCH) rd((c + 1) & 1, c + 1);
+        mm(c & 1);
+        if (c + 1 < NCH) {
+            // the next chunk's reads between this chunk's instructions: in
+            // one run they would exceed the 15 reads the LDS counter can
+            // wait past, and each instruction would wait for some of them
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, NB, 0);          // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1 + NB, 0);      // LDS reads
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
 
     float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
@@ -1623,8 +1626,18 @@ hipError_t launch_conv_f32_smallm(const ConvArgs &a, hipStream_t s) {
             (unsigned)(((a.OC + 15) / 16) * a.Nb * ((OHW + BN - 1) / BN));
         ConvArgs args = a;
         void *kargs[] = {&args};
-        return hipLaunchKernel(reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB>),
-                               dim3(tiles), dim3(smallm::NT), kargs, (size_t)geo.bytes, s);
+        static const void *const fns[8] = {
+            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 1>),
+            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 2>),
+            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 3>),
+            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 4>),
+            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 5>),
+            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 6>),
+            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 7>),
+            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 8>)};
+        // patch_geom admits K up to 256 (KP / 32 = 1 .. 8 chunks)
+        const int nch = (a.C * a.R * a.S + 31) / 32;
+        return hipLaunchKernel(fns[nch - 1], dim3(tiles), dim3(smallm::NT), kargs, (size_t)geo.bytes, s);
     }
     const int N = a.Nb * a.OH * a.OW, K = a.C * a.R * a.S;
     const unsigned tiles = (unsigned)(((a.OC + 15) / 16) * ((N + BN - 1) / BN));
