@@ -254,7 +254,7 @@ def conv_f32_halo16_launch(N, C, H, W, OC, pad_h, pad_w, nh=2, plane_pad=16,
 # --------------------------------------------------- bf16 halo-tiled conv
 
 def conv_bf16_halo_launch(N, C, H, W, OC, pad_h, pad_w, a_swizzle=False, rotate=False,
-                          store_order=False) -> LdsCost:
+                          store_order=False, trailing_store=False) -> LdsCost:
     """One launch of the bf16 halo-tiled conv (3x3, stride 1,
     csrc/conv2d_bf16.hip): per stage and wave, the register-staged patch and
     weight stores (ds_write_b128) and, per tap, TM ds_read_b128 A fragments
@@ -263,7 +263,9 @@ def conv_bf16_halo_launch(N, C, H, W, OC, pad_h, pad_w, a_swizzle=False, rotate=
     halves swapped; ``rotate``: patch row r is stored rotated by
     (r * OW) mod 16 cells in rows of 80 cells (else unrotated rows of 64);
     ``store_order``: a thread writes its two patch cells in the order bit 2
-    of its column pair selects (else even cells first)."""
+    of its column pair selects (else even cells first); ``trailing_store``:
+    the last stage also stores a (never read) next stage, as the kernel did
+    before its loads went two stages ahead."""
     BM, BN, WM, WN, MI = 64, 256, 64, 64, 32
     TM, TN, CC, PR, CO = WM // MI, WN // MI, 16, 8, 2
     PC = 80 if rotate else 64
@@ -329,9 +331,11 @@ def conv_bf16_halo_launch(N, C, H, W, OC, pad_h, pad_w, a_swizzle=False, rotate=
                         addrs.append((lane // MI) * HALF + ((r + kh) * PC + c + kw + rot(r + kh)) * 16)
                     per_image.add("ds_read_b128", addrs)
         per_image += stage_w
-    # every stage's stores, plus the prologue's store of stage 0
+    # the prologue's store of stage 0 and one store per stage but the last
+    # (plus the last one's when ``trailing_store``)
     total = per_image.scaled(C // CC)
-    total += stage_w.scaled(chunks)
+    if trailing_store:
+        total += stage_w.scaled(chunks)
     return total.scaled(_cdiv(OC, BM) * N)
 
 
