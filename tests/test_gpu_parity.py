@@ -86,7 +86,10 @@ def test_matmul_workload_parity(x, ci):
     (1, 64, 56, 56, 70, 3, 3, 1, 1),    # rows: OC = 70
     (2, 64, 3, 4, 64, 3, 3, 1, 1),      # rows: 4 x 4 output, band taller than the image
     (16, 64, 40, 16, 64, 3, 3, 1, 1),   # rows: bands of 3 rows (last step half used)
-    (32, 64, 30, 8, 64, 3, 3, 1, 1),    # rows: bands of 4 rows (two full steps), shorter last band
+    (32, 64, 30, 8, 64, 3, 3, 1, 1),    # rows: bands of 4 rows, shorter last band
+    (100, 64, 60, 8, 64, 3, 3, 1, 1),   # rows: bands of 20 rows (five steps: both register sets twice)
+    (64, 64, 26, 8, 40, 3, 3, 1, 1),    # rows: bands of 7 rows (last step has three), OC = 40
+    (64, 64, 21, 10, 64, 3, 3, 1, 0),   # rows: no padding, bands of 5 rows (two steps, one row in the last)
 ])
 def test_conv_bf16_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape
