@@ -128,10 +128,14 @@ typedef enum {
  *                split of the reduction for problems with too few tiles to
  *                fill the chip); their partial sums are added in a fixed
  *                order through LDS, so results stay deterministic.  1 = no
- *                split.  With k_split > 1 each wave covers the whole
+ *                split.  With lds_stages = 0 each wave covers the whole
  *                workgroup tile (wave_m = block_m, wave_n = block_n) and
- *                lds_stages = 0: operands go from memory straight to the
- *                matrix-core registers, double-buffered in registers.
+ *                operands go from memory straight to the matrix-core
+ *                registers, double-buffered in registers.  With
+ *                lds_stages >= 1 (matmul only) k_split groups of
+ *                (block_m/wave_m)*(block_n/wave_n) waves each run the
+ *                LDS-staged pipeline on every k_split-th K-step of the
+ *                tile, each group on its own LDS ring.
  *
  * block_*, wave_*, mfma_*, lds_stages, lds_pad, unroll_k, k_order and k_split
  * select a compiled kernel instance; raster and xcd_remap are run-time choices valid

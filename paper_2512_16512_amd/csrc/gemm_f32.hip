@@ -239,16 +239,27 @@ struct F32DmaCfg {
     static_assert((STAGES - 1) * LOADS < 64, "vmcnt range");
 };
 
-template <int BM, int BN, int BK, int WM, int WN, int MI_, int STAGES>
-__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+// KSW > 1: the workgroup holds KSW groups of waves, each running the whole
+// pipeline below on its own LDS ring over every KSW-th K-step (group g takes
+// K-steps g, g + KSW, ...), with the same number of iterations in every
+// group (zero-filled K-steps past the end), so that each SIMD holds KSW
+// waves and one wave's LDS and barrier waits overlap another's matrix
+// instructions.  At the end the groups' accumulators are added through LDS
+// in the fixed order 0, 1, ..., KSW-1 (deterministic results).
+template <int BM, int BN, int BK, int WM, int WN, int MI_, int STAGES, int KSW = 1>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64 * KSW)
 gemm_f32_dma_kernel(GemmArgs p) {
     typedef F32DmaCfg<BM, BN, BK, WM, WN, MI_, STAGES> G;
     typedef typename G::MF MF;
     constexpr int MI = G::MI;
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * G::STAGE_BYTES];
+    static_assert(KSW * STAGES * G::STAGE_BYTES <= 160 * 1024, "LDS budget");
+    __shared__ __attribute__((aligned(1024))) unsigned char smem_all[KSW * STAGES * G::STAGE_BYTES];
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63;
+    const int kg = __builtin_amdgcn_readfirstlane((tid >> 6) / G::NWAVES);   // K group of this wave
+    const int wave = (tid >> 6) % G::NWAVES;        // wave inside its group
+    unsigned char *const smem = smem_all + kg * STAGES * G::STAGE_BYTES;
     const int wm = wave / G::NWN, wn = wave % G::NWN;
     const int lrow = lane % MI, lgrp = lane / MI;
 
@@ -280,7 +291,7 @@ gemm_f32_dma_kernel(GemmArgs p) {
 
     int offA[G::A_PER_WAVE], offB[G::B_PER_WAVE];
     auto prepare = [&](int kt) {
-        const int k0 = kt * BK;
+        const int k0 = (kt * KSW + kg) * BK;
 #pragma unroll
         for (int q = 0; q < G::A_PER_WAVE; ++q) {
             const int gm = m0 + a_row[q], gk = k0 + a_col[q];
@@ -382,7 +393,7 @@ gemm_f32_dma_kernel(GemmArgs p) {
     // Branch-free main loop: every stage index issues LOADS copies per wave
     // (zero-fill copies past the end of K), so one vmcnt value is exact in
     // every iteration and the compiler's LDS waits stay tight.
-    const int KT = (K + BK - 1) / BK;
+    const int KT = ((K + BK - 1) / BK + KSW - 1) / KSW;   // iterations of every group
 #pragma unroll
     for (int s = 0; s < STAGES; ++s) {
         prepare(s);
@@ -414,6 +425,38 @@ gemm_f32_dma_kernel(GemmArgs p) {
     }
     wait_vmcnt<0>();  // no copy may still be writing LDS when the workgroup ends
 
+    if constexpr (KSW > 1) {
+        // groups 1 .. KSW-1 leave their sums in LDS (each lane its own
+        // registers, lane-contiguous); group 0 adds them in group order
+        constexpr int NREG = G::TM * G::TN * MF::NACC;
+        static_assert((KSW - 1) * G::NWAVES * NREG * 64 * 4 <= KSW * STAGES * G::STAGE_BYTES,
+                      "partial sums fit in the rings");
+        float *red = reinterpret_cast<float *>(smem_all);
+        __syncthreads();   // every group's last fragment reads are done
+        if (kg > 0) {
+#pragma unroll
+            for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+                    for (int r = 0; r < MF::NACC; ++r)
+                        red[((((kg - 1) * G::NWAVES + wave) * G::TM + i) * G::TN + j) * MF::NACC * 64 + r * 64 + lane] =
+                            acc[i][j][r];
+        }
+        __syncthreads();
+        if (kg > 0) return;
+#pragma unroll
+        for (int g = 1; g < KSW; ++g)
+#pragma unroll
+            for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < G::TN; ++j)
+#pragma unroll
+                    for (int r = 0; r < MF::NACC; ++r)
+                        acc[i][j][r] += red[((((g - 1) * G::NWAVES + wave) * G::TM + i) * G::TN + j) * MF::NACC * 64 +
+                                            r * 64 + lane];
+    }
+
     float *__restrict__ C = p.C;
     const int ldc = p.ldc;
 #pragma unroll
@@ -429,15 +472,15 @@ gemm_f32_dma_kernel(GemmArgs p) {
         }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES>
+template <int BM, int BN, int BK, int WM, int WN, int MI, int STAGES, int KSW = 1>
 hipError_t launch_f32_dma(const GemmArgs &a, hipStream_t s) {
     typedef F32DmaCfg<BM, BN, BK, WM, WN, MI, STAGES> G;
     const unsigned tiles = (unsigned)(((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN));
     GemmArgs args = a;
     void *kargs[] = {&args};
     return hipLaunchKernel(
-        reinterpret_cast<const void *>(&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES>),
-        dim3(tiles), dim3(G::NT), kargs, 0, s);
+        reinterpret_cast<const void *>(&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, MI, STAGES, KSW>),
+        dim3(tiles), dim3(G::NT * KSW), kargs, 0, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -626,6 +669,17 @@ hipError_t launch_f32_ksplit(const GemmArgs &a, hipStream_t s) {
                           (BM / WM) * (BN / WN) * 64, 0>                                      \
     }
 
+// In-workgroup reduction split: KSW groups of waves on one tile (k_split =
+// KSW with LDS staging); the fallback is the unsplit register-staged kernel.
+#define XTC_F32_DMA_KSW_INSTANCE(BM, BN, BK, WM, WN, STAGES, KSW)                             \
+    GemmInstance {                                                                            \
+        make_sched(BM, BN, BK, WM, WN, 32, 32, 2, STAGES, -1, 0, 0, KSW),                     \
+            &launch_f32_dma<BM, BN, BK, WM, WN, 32, STAGES, KSW>,                             \
+            &launch_f32<BM, BN, BK, WM, WN, 32, 4, false>, kWholeChunks,                      \
+            &occupancy_of<&gemm_f32_dma_kernel<BM, BN, BK, WM, WN, 32, STAGES, KSW>,          \
+                          (BM / WM) * (BN / WN) * 64 * KSW, 0>                                \
+    }
+
 // 256x256 tiles: the register-staged kernel with the same tiles would spill,
 // so the fallback runs 128x128 tiles of four 64x64 waves.
 #define XTC_F32_DMA_BIG_INSTANCE(BM, BN, BK, WM, WN, STAGES)                                  \
@@ -661,6 +715,8 @@ const GemmInstance kF32Instances[] = {
     XTC_F32_DMA_INSTANCE(64, 128, 32, 32, 64, 3),    // mid-size problems
     XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 4),
     XTC_F32_DMA_INSTANCE(64, 64, 32, 32, 32, 2),
+    XTC_F32_DMA_KSW_INSTANCE(64, 64, 32, 32, 32, 2, 2),   // two K groups of four 32x32 waves
+    XTC_F32_DMA_KSW_INSTANCE(64, 64, 32, 32, 32, 2, 4),
     XTC_F32_INSTANCE(128, 128, 32, 64, 64, 32, 4),
     XTC_F32_INSTANCE(128, 128, 16, 64, 64, 32, 4),
     XTC_F32_INSTANCE(64, 64, 32, 32, 32, 32, 4),     // small problems: more tiles

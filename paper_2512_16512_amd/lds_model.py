@@ -557,11 +557,30 @@ def matmul_launch(dtype: str, s: dict, M: int, N: int, K: int):
     on 16-byte-aligned row-major operands, or None if the instance's kernel
     is not modelled.  The instance's kernel is the one its launcher picks for
     such operands: the direct-to-LDS kernel for lds_pad -1, else the
-    register-staged kernel, or the reduction-split kernel for k_split > 1."""
+    register-staged kernel, or for k_split > 1 the reduction-split kernel
+    (lds_stages 0) or the direct-to-LDS kernel in k_split wave groups."""
     BM, BN, BK = s["block_m"], s["block_n"], s["block_k"]
     WM, WN, MI = s["wave_m"], s["wave_n"], s["mfma_m"]
     tiles = _cdiv(M, BM) * _cdiv(N, BN)
     kt = _cdiv(K, BK)
+    if s.get("k_split", 1) > 1 and s.get("lds_stages", 0) > 0 and dtype == "f32" and s["lds_pad"] < 0:
+        # k_split groups of waves, each the direct-to-LDS pipeline on every
+        # k_split-th K-step (the same number of iterations in every group),
+        # then the partial sums of groups 1.. through LDS, one lane-
+        # contiguous dword per register, written once and read once
+        ks = s["k_split"]
+        stage = gemm_f32_dma_stage(BM, BN, BK, WM, WN, MI)
+        steps = BK // (4 * (2 if MI == 32 else 4))
+        ktg = _cdiv(kt, ks)
+        one = stage.scaled(ktg * steps)
+        one += stage
+        tile = LdsCost(one.active * ks // steps, one.conflict * ks // steps,
+                       one.read_bytes * ks // steps, one.write_bytes * ks // steps)
+        nreg = (BM // WM) * (BN // WN) * (WM // MI) * (WN // MI) * (MI * MI // 64)
+        lanes = [4 * l for l in range(64)]
+        tile.add("ds_write_b32", lanes, times=(ks - 1) * nreg)
+        tile.add("ds_read_b32", lanes, times=(ks - 1) * nreg)
+        return tile.scaled(tiles)
     if s.get("k_split", 1) > 1:
         return gemm_f32_ksplit_tile(MI, BM // MI, BN // MI, s["k_split"]).scaled(tiles)
     if dtype == "bf16":

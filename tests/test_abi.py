@@ -224,15 +224,24 @@ def test_one_hip_runtime_whatever_the_import_order():
 
 
 def test_k_split_rules(x):
-    ks = [s for s in x.xtc_sched_list(0, 0) if s.k_split > 1]
+    # register-fed split: each wave covers the whole tile, nothing in LDS
+    ks = [s for s in x.xtc_sched_list(0, 0) if s.k_split > 1 and s.lds_stages == 0]
     assert ks, "no reduction-split fp32 instance compiled"
     s = x.Sched(**ks[0].as_dict())
     assert x.xtc_sched_check(0, 0, s) == 0
     bad = x.Sched(**s.as_dict())
-    bad.wave_m = s.block_m // 2            # split waves must cover the whole tile
+    bad.wave_m = s.block_m // 2            # register-fed split waves must cover the whole tile
     assert x.xtc_sched_check(0, 0, bad) == 5
     bad = x.Sched(**s.as_dict())
-    bad.lds_stages = 2                     # the split kernels stage nothing in LDS
+    bad.lds_stages = 2                     # legal (an LDS-staged split), not compiled for this tile
+    assert x.xtc_sched_check(0, 0, bad) == 6
+    # LDS-staged split: groups of waves, each running the staged pipeline on
+    # its share of the K-steps
+    st = [s for s in x.xtc_sched_list(0, 0) if s.k_split > 1 and s.lds_stages > 0]
+    assert st and all(t.wave_m < t.block_m for t in st)
+    assert x.xtc_sched_check(0, 0, st[0]) == 0
+    bad = x.Sched(**st[0].as_dict())
+    bad.lds_stages = 0                     # smaller waves than the tile need the LDS pipeline
     assert x.xtc_sched_check(0, 0, bad) == 5
     bad = x.Sched(**s.as_dict())
     bad.k_split = 2                        # legal value, not compiled

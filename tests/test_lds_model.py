@@ -142,3 +142,14 @@ def test_unmodelled_kernels_return_none():
     # the tap-major conv kernel is not modelled
     s = dict(k_order=1, block_n=256, block_m=64, lds_stages=2)
     assert L.conv_launch("f32", s, 32, 64, 56, 56, 64, 3, 3, 1, 1) is None
+
+
+def test_staged_k_split_matches_counters():
+    # the fp32 direct-to-LDS kernel in two and four K groups on 1000^3:
+    # SQ_LDS_IDX_ACTIVE 1662976 and 1818624 per launch (unsplit: 1585152),
+    # no conflicts
+    base = dict(block_m=64, block_n=64, block_k=32, wave_m=32, wave_n=32, mfma_m=32,
+                lds_stages=2, lds_pad=-1)
+    for ks, cyc in ((1, 1585152), (2, 1662976), (4, 1818624)):
+        c = L.matmul_launch("f32", dict(base, k_split=ks), 1000, 1000, 1000)
+        assert c.active == cyc and c.conflict == 0
