@@ -602,10 +602,13 @@ gemm_f32_ksplit_kernel(GemmArgs p) {
     };
 
     // D K-steps per iteration (unrolled) so that every register buffer is
-    // named by a constant.  This wave's steps are g, g + KS, ...  The loop
-    // is branch-free: steps past the end are loaded (as zeros, every offset
-    // being out of range) and multiplied like the others, so every step
-    // issues the same loads and the compiler's wait counts stay exact.
+    // named by a constant.  This wave's steps are g, g + KS, ...  The loads
+    // are branch-free: steps past the end are loaded (as zeros, every offset
+    // being out of range), so every step issues the same loads and the
+    // compiler's wait counts stay exact.  Only the matrix instructions of
+    // steps past the end are skipped (a uniform branch with no memory
+    // instruction in it): with a short reduction most of an iteration's
+    // steps can lie past it (K = 128 on 32x32 tiles: three of four).
     const int KT = (K + BK - 1) / BK;
 #pragma unroll
     for (int d = 0; d + 1 < D; ++d) load(d, g + d * KS);
@@ -613,7 +616,7 @@ gemm_f32_ksplit_kernel(GemmArgs p) {
 #pragma unroll
         for (int d = 0; d < D; ++d) {
             load((d + D - 1) % D, base + (d + D - 1) * KS);
-            compute(d);
+            if (d == 0 || base + d * KS < KT) compute(d);
         }
     }
 
