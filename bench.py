@@ -674,6 +674,13 @@ def vendor_line(steps: int, warmup: int, ours: dict):
     out["conv"] = {"workload": cfg["name"], "ms_per_launch": round(ms, 4),
                    "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2),
                    "ours_TFLOP/s": ours["also"].get("conv", {}).get("value")}
+    # bf16 inputs: MIOpen returns a bf16 output (half the bytes of ours)
+    xb, wb = xd.to(torch.bfloat16), wd.to(torch.bfloat16)
+    f = lambda: torch.nn.functional.conv2d(xb, wb, stride=cfg["stride"], padding=cfg["pad"])
+    ms = time_launches(f, steps, warmup)
+    out["conv_bf16"] = {"workload": cfg["name"].replace("fp32", "bf16"), "ms_per_launch": round(ms, 4),
+                        "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2), "output_dtype": "bfloat16",
+                        "ours_TFLOP/s": ours["also"].get("conv_bf16", {}).get("value")}
     return out
 
 
