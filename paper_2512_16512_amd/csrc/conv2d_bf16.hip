@@ -543,7 +543,8 @@ constexpr int CO = 2;                     // stored column of input column 0 (ev
 constexpr int ROWB = PC * NCG * 16;       // bytes per stored input row
 constexpr int RING_BYTES = NR * ROWB;
 constexpr int W_BYTES = NTAP * BM * NCG * 16;
-constexpr int LDS_BYTES = RING_BYTES + W_BYTES;
+constexpr int STG_BYTES = 32 * 128;       // per wave: one output row, 32 channels x 32 pixels
+constexpr int LDS_BYTES = RING_BYTES + W_BYTES + (NT / 64) * STG_BYTES;
 static_assert(NT == 32 * NCG, "one (column pair, cell group) per thread");
 static_assert(2 * NT == BM * NCG, "two weight slabs per thread");
 static_assert(NR >= 3 * RO + 2, "ring: a step's rows, the next step's, and the slots being refilled");
@@ -689,14 +690,33 @@ conv2d_bf16_rows_kernel(ConvArgs p) {
     }
 
     // ---- output: lane (l32, lg) of wave w holds, per output row, pixels
-    // 32*(w >> 1) + 8i + 4lg .. +3 (i = 0..3) of output channel m0 + oc_l:
-    // four 16-byte stores per row, at an out-of-range offset where the
-    // channel, row or pixels are outside Y (the store is then dropped).
-    const int oc_st = m0 + oc_l;
+    // 32*(w >> 1) + 8i + 4lg .. +3 (i = 0..3) of output channel m0 + oc_l.
+    // Stored as they are, each 16-byte store instruction would write 32
+    // pieces of 32 bytes (one per channel).  Instead each row goes through
+    // the wave's own LDS area ([channel][8 chunks of 4 pixels], chunk slot
+    // c ^ (channel & 7): conflict-free both ways) and is read back so that
+    // lane j holds chunk j & 7 of channel 8s + (j >> 3): four stores per row,
+    // each of 8 runs of 128 bytes.  A store whose channel, row or pixels lie
+    // outside Y goes to an out-of-range offset and is dropped.
     const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
         p.Y, 0, p.Nb * OC * OH * OW * 4, 0x00020000);
-    const int ybase = ((img * OC + min(oc_st, OC - 1)) * OH + oh_a) * OW * 4;
-    const int px_st = 32 * (wave >> 1) + 4 * lg;
+    unsigned char *const stg = smem + RING_BYTES + W_BYTES + wave * STG_BYTES;
+    const int ch_rd = lane & 7, oc_rd = lane >> 3;   // chunk and channel (within 8) read back
+    const int px_rd = 32 * (wave >> 1) + 4 * ch_rd;
+    // byte offset in Y of band row 0 for each of the lane's four stores of a
+    // row (out of range where the channel or the pixels lie outside Y); a
+    // row adds its row offset, which keeps an out-of-range offset out of
+    // range (unsigned, and Y spans less than 2^31 bytes)
+    unsigned soff[4];
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+        const int oc = m0 + 32 * (wave & 1) + 8 * s4 + oc_rd;
+        soff[s4] = (oc < OC) & (px_rd < OW) ? (unsigned)((((img * OC + oc) * OH + oh_a) * OW + px_rd) * 4)
+                                             : (unsigned)kOOB;
+    }
+    // relu as a lower bound (-inf: none); accumulators start at +0, so a
+    // -0 result, which the bound would not keep, cannot occur
+    const float lo = p.relu ? 0.f : -__builtin_inff();
     // A step's outputs are stored during the next step, one store per
     // k-step group, and its row loads are spread the same way: with one
     // wave per SIMD a burst of memory instructions stalls the wave at the
@@ -783,22 +803,27 @@ conv2d_bf16_rows_kernel(ConvArgs p) {
         frags(0, 0, st + 1);
         mmas(1);
         interleave(false);
-        // this step's outputs, stored during the next step
+        // this step's outputs, through the staging area, stored during the
+        // next step (write-back stores: nontemporal ones of lines that other
+        // workgroups' stores complete would cost whole lines of HBM writes).
+        // The wave's LDS operations run in order, so row 1 may overwrite
+        // the area row 0 was read from.
 #pragma unroll
         for (int o = 0; o < RO; ++o) {
-            const bool rok = (oc_st < OC) & (RO * st + o < rows);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int k = 4 * o + i, px = px_st + 8 * i;
-                pend_off[k] = (rok & (px < OW)) ? ybase + ((RO * st + o) * OW + px) * 4 : kOOB;
+                f32x4 v;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float v = acc[o][4 * i + r];
-                    // write-back stores: the pieces of a line written by
-                    // several instructions merge in L2 (nontemporal stores
-                    // of partial lines cost whole lines of HBM writes)
-                    pend[k][r] = (p.relu && v < 0.f) ? 0.f : v;
-                }
+                for (int r = 0; r < 4; ++r) v[r] = __builtin_fmaxf(acc[o][4 * i + r], lo);
+                *reinterpret_cast<f32x4 *>(stg + l32 * 128 + (((2 * i + lg) ^ (l32 & 7)) << 4)) = v;
+            }
+            const bool rok = RO * st + o < rows;   // uniform
+            const unsigned roff = (unsigned)((RO * st + o) * OW * 4);
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const int k = 4 * o + s4;
+                pend[k] = *reinterpret_cast<const f32x4 *>(stg + (8 * s4 + oc_rd) * 128 + ((ch_rd ^ oc_rd) << 4));
+                pend_off[k] = rok ? (int)(soff[s4] + roff) : kOOB;
             }
         }
     };

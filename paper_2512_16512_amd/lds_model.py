@@ -351,7 +351,9 @@ def conv_bf16_rows_launch(N, C, H, W, OC, pad_h, pad_w) -> LdsCost:
     .. 3 once; per step of two output rows, the two new input rows (two
     ds_write_b128 per thread and row) and, per wave and (kw, 16-channel
     k-step) group, three weight and four pixel fragments (ds_read_b128);
-    plus the first group of the step after the last."""
+    plus the first group of the step after the last; and per wave and output
+    row of a step, the staging of the row for the stores (four ds_write_b128
+    and four ds_read_b128)."""
     assert C == 64
     BM, NCG, RO, CO = 64, 8, 2, 2
     OH, OW = H + 2 * pad_h - 2, W + 2 * pad_w - 2
@@ -405,6 +407,14 @@ def conv_bf16_rows_launch(N, C, H, W, OC, pad_h, pad_w) -> LdsCost:
                 group += g
                 if kw == 0 and ks == 0:
                     first_group += g
+    staging = LdsCost()         # one output row of every wave, out and back
+    for wave in range(4):
+        for i in range(4):
+            staging.add("ds_write_b128", [(l % 32) * 128 + (((2 * i + l // 32) ^ (l % 32 & 7)) << 4)
+                                          for l in range(64)])
+        for s4 in range(4):
+            staging.add("ds_read_b128", [(8 * s4 + (l >> 3)) * 128 + (((l & 7) ^ (l >> 3)) << 4)
+                                         for l in range(64)])
     total = LdsCost()
     for band_i in range(nbands):
         rows = min(band, OH - band_i * band)
@@ -414,6 +424,7 @@ def conv_bf16_rows_launch(N, C, H, W, OC, pad_h, pad_w) -> LdsCost:
         total += row_w.scaled(RO * nsteps)             # each step stores the next step's rows
         total += group.scaled(nsteps)
         total += first_group
+        total += staging.scaled(RO * nsteps)
     return total.scaled(per_img)
 
 
