@@ -528,7 +528,11 @@ hipError_t launch_conv_bf16_halo(const ConvArgs &a, hipStream_t s) {
 //  - a weight cell holds 8 channels of one (tap, output channel); the eight
 //    cells of output channel o sit at slots g ^ h(o), the same pattern, since
 //    a weight fragment (32 output channels x two groups) is addressed like a
-//    pixel fragment.
+//    pixel fragment;
+//  - each wave turns its output rows around through a 4 KiB LDS area of its
+//    own before storing them, so that a store instruction writes runs of 128
+//    bytes of one channel row (ring 64 KiB + weights 72 KiB + 4 x 4 KiB:
+//    152 KiB, one workgroup per CU).
 namespace rows_bf16 {
 constexpr int NT = 256;                   // four waves
 constexpr int BM = 64;                    // output channels per workgroup
