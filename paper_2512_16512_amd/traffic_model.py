@@ -336,6 +336,197 @@ def correlate(order_path: str, fetch_csv: str, fetch_scale: float):
     return table, pearson(x, y), spearman(x, y)
 
 
+# ------------------------------------------------------------------- conv
+
+def _cdiv(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+def conv_grid(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
+    """The tile grid of the kernel the library runs for conv instance ``s``
+    on this shape: (BM, tiles_m, tiles_n, segments, forced XCD remap or
+    None), where ``segments(tn)`` lists the (image, first output row, last
+    output row, input rows read) of pixel tile ``tn``.  Follows the
+    launchers' choice of kernel and tile (the balanced halo kernel's pixel
+    tile, the row-streaming kernel's bands, the fallbacks outside a kernel's
+    class); None where the choice is not modelled."""
+    sh = sw = stride
+    ph = pw = pad
+    OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    OHW = OH * OW
+    halo_class = R == 3 and S == 3 and sh == 1 and sw == 1
+
+    def rows_of(oh0, oh1):
+        return max(0, oh0 * sh - ph), min(H - 1, oh1 * sh - ph + R - 1)
+
+    def per_image(pt):
+        chunks = _cdiv(OHW, pt)
+
+        def seg(tn):
+            img, c = divmod(tn, chunks)
+            p0, p1 = c * pt, min((c + 1) * pt, OHW)
+            oh0, oh1 = p0 // OW, (p1 - 1) // OW
+            return [(img,) + rows_of(oh0, oh1)]
+        return N * chunks, seg
+
+    def flattened(bn):
+        tot = N * OHW
+
+        def seg(tn):
+            q0, q1 = tn * bn, min((tn + 1) * bn, tot)
+            out = []
+            while q0 < q1:
+                img, p0 = divmod(q0, OHW)
+                p1 = min(q1 - img * OHW, OHW)
+                out.append((img,) + rows_of(p0 // OW, (p1 - 1) // OW))
+                q0 = img * OHW + p1
+            return out
+        return _cdiv(tot, bn), seg
+
+    bm, force = s["block_m"], None
+    if dtype == "bf16" and s["k_order"] == 3:
+        if halo_class and C == 64 and W % 2 == 0 and pw <= 2 and OW % 4 == 0 and OW <= 64 and OW + 1 - pw + 2 <= 63:
+            per_img = _cdiv(OC, 64) * N
+            band = max(_cdiv(OH, _cdiv(256, per_img)), 2)
+            nb = _cdiv(OH, band)
+
+            def seg(tn):
+                img, b = divmod(tn, nb)
+                rows = min(band, OH - b * band)
+                nin = 2 * _cdiv(rows, 2) + 2          # the band's input rows, as the kernel reads them
+                lo = b * band - ph
+                return [(img, max(0, lo), min(H - 1, lo + nin - 1))]
+            return 64, _cdiv(OC, 64), N * nb, seg, 1
+        s = dict(s, k_order=2, block_n=256)
+    if dtype == "bf16" and s["k_order"] == 2:
+        span = (256 - 1 + OW - 1) // OW + 1
+        if halo_class and C % 16 == 0 and W % 2 == 0 and pw <= 2 and OW - pw + 3 <= 63 and span + 2 <= 8:
+            tn, seg = per_image(256)
+            return 64, _cdiv(OC, 64), tn, seg, None
+        s = dict(s, block_m=64, block_n=128)           # the gather kernel's 64x128 tiles
+        bm = 64
+    if dtype == "bf16":
+        tn, seg = flattened(s["block_n"])
+        return bm, _cdiv(OC, bm), tn, seg, None
+    if s["k_order"] == 2 and s["block_n"] in (208, 416):
+        nh = 1 if s["block_n"] == 208 else 2
+        if halo_class and C % 8 == 0 and pw <= 4 and OW - pw + 5 <= 63:
+            t = _cdiv(OHW, 208 * nh)
+            pt = _cdiv(OHW, t)
+            if (pt - 1 + OW - 1) // OW + 1 + 2 <= (8 if nh == 1 else 10):
+                tn, seg = per_image(pt)
+                return 64, _cdiv(OC, 64), tn, seg, None
+        s = dict(s, block_n=256)
+    if s["k_order"] == 2:
+        span = (256 - 1 + OW - 1) // OW + 1
+        if halo_class and C % 16 == 0 and pw <= 4 and OW - pw + 5 <= 63 and span + 2 <= 8:
+            tn, seg = per_image(256)
+            return 64, _cdiv(OC, 64), tn, seg, None
+        tn, seg = flattened(256)                       # the tap-major 64x256 fallback
+        return 64, _cdiv(OC, 64), tn, seg, None
+    if bm == 16:
+        return None                                    # patch-staged or gather: not modelled
+    tn, seg = flattened(s["block_n"])
+    return bm, _cdiv(OC, bm), tn, seg, None
+
+
+def predict_conv(dtype: str, s: dict, dims, occupancy: int, l2_bytes: int = L2_BYTES):
+    """Predicted HBM (read, write) bytes of one conv launch of instance
+    ``s`` (``dims`` = N, C, H, W, OC, R, S, stride, pad), or None where the
+    kernel's tiles are not modelled.
+
+    A workgroup reads the weights of its output-channel tile and, of each
+    image its pixel tile touches, every input row its output rows reach
+    (all channels, whole rows).  As in ``predict``, an XCD whose workgroups
+    together touch at most its L2 reads each row and weight panel once;
+    otherwise each group of ``32 * occupancy`` workgroups that run at once
+    reads the union of what it touches.  The output is written once."""
+    N, C, H, W, OC, R, S, stride, pad = dims
+    g = conv_grid(dtype, s, *dims)
+    if g is None:
+        return None
+    bm, tiles_m, tiles_n, seg, force = g
+    raster = s["raster"]
+    remap = s["xcd_remap"] if force is None else force
+    elt = 4 if dtype == "f32" else 2
+    row_bytes = C * W * elt
+    K = C * R * S
+    grid = tiles_m * tiles_n
+    conc = max(1, CUS_PER_XCD * max(1, occupancy))
+
+    def footprint(tiles):
+        wts = {t[0] for t in tiles}
+        rows = set()
+        for t in tiles:
+            for img, lo, hi in seg(t[1]):
+                rows.update((img, r) for r in range(lo, hi + 1))
+        return sum(min(bm, OC - m * bm) for m in wts) * K * elt + len(rows) * row_bytes
+
+    read = 0
+    for x in range(XCDS):
+        tiles = [tile_coords(b, grid, tiles_m, tiles_n, raster, remap) for b in range(x, grid, XCDS)]
+        if not tiles:
+            continue
+        f = footprint(tiles)
+        if f <= l2_bytes:
+            read += f
+            continue
+        read += sum(footprint(tiles[g0:g0 + conc]) for g0 in range(0, len(tiles), conc))
+    OH, OW = (H + 2 * pad - R) // stride + 1, (W + 2 * pad - S) // stride + 1
+    return read, 4 * N * OC * OH * OW
+
+
+CONV_ORDERS = ((0, 1), (0, 0), (1, 1), (1, 0), (8, 1))
+
+
+def run_conv(dtype: str, dims, order_path: str, reps: int = 2, orders=CONV_ORDERS):
+    """Launch every conv instance under every tile order in ``orders``
+    ``reps`` times, in a fixed order, and write that order (with each
+    schedule's occupancy) to ``order_path`` (the measurement step of
+    ``correlate_conv``, run under the counter profiler)."""
+    import torch
+
+    import paper_2512_16512_amd as xtc
+    from paper_2512_16512_amd import tune
+    p = tune.Problem("conv2d", dtype, tuple(dims))
+    N, C, H, W, OC, R, S, stride, pad = dims
+    entries = []
+    stream = torch.cuda.current_stream().cuda_stream
+    for base in xtc.xtc_sched_list(xtc.XTC_OP_CONV2D, p.code):
+        for raster, remap in orders:
+            s = xtc.Sched(**base.as_dict())
+            s.raster, s.xcd_remap = raster, remap
+            occ = xtc.xtc_sched_occupancy(xtc.XTC_OP_CONV2D, p.code, C * R * S, s)
+            for _ in range(reps):
+                p.launch(s, stream)
+            torch.cuda.synchronize()
+            entries.append({"sched": s.as_dict(), "occupancy": occ})
+    with open(order_path, "w") as f:
+        json.dump({"dtype": dtype, "dims": list(dims), "reps": reps, "schedules": entries}, f)
+    print("launched %d conv schedules x %d" % (len(entries), reps), flush=True)
+
+
+def correlate_conv(order_path: str, fetch_csv: str, fetch_scale: float):
+    """Predicted vs measured (FETCH_SIZE x 1024 x fetch_scale) bytes per
+    conv schedule; the correlation is over the modelled schedules."""
+    o = json.load(open(order_path))
+    vals = _counter_rows(fetch_csv, "FETCH_SIZE")
+    reps = o["reps"]
+    if len(vals) != reps * len(o["schedules"]):
+        raise ValueError("%d counter rows for %d schedules x %d launches"
+                         % (len(vals), len(o["schedules"]), reps))
+    table = []
+    for i, e in enumerate(o["schedules"]):
+        meas = sum(vals[i * reps:(i + 1) * reps]) / reps * 1024 * fetch_scale
+        pred = predict_conv(o["dtype"], e["sched"], tuple(o["dims"]), e["occupancy"])
+        table.append({"sched": e["sched"], "occupancy": e["occupancy"],
+                      "predicted": None if pred is None else pred[0], "measured": meas})
+    mod = [t for t in table if t["predicted"] is not None]
+    x = [t["predicted"] for t in mod]
+    y = [t["measured"] for t in mod]
+    return table, pearson(x, y), spearman(x, y)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -362,9 +553,30 @@ def main(argv=None):
     c.add_argument("fetch_csv")
     c.add_argument("--fetch-scale", type=float, required=True)
     c.add_argument("--json", default=None)
+    rc = sub.add_parser("run-conv")
+    rc.add_argument("dtype", choices=["f32", "bf16"])
+    rc.add_argument("dims", type=int, nargs=9, help="N C H W OC R S stride pad")
+    rc.add_argument("--order", required=True)
+    rc.add_argument("--reps", type=int, default=2)
+    cc = sub.add_parser("correlate-conv")
+    cc.add_argument("order")
+    cc.add_argument("fetch_csv")
+    cc.add_argument("--fetch-scale", type=float, required=True)
+    cc.add_argument("--json", default=None)
     a = ap.parse_args(argv)
     if a.cmd == "run":
         run(a.dtype, a.M, a.N, a.K, a.order, a.reps)
+        return 0
+    if a.cmd == "run-conv":
+        run_conv(a.dtype, tuple(a.dims), a.order, a.reps)
+        return 0
+    if a.cmd == "correlate-conv":
+        table, r_, rho = correlate_conv(a.order, a.fetch_csv, a.fetch_scale)
+        n = sum(t["predicted"] is not None for t in table)
+        print("conv schedules %d (modelled %d)  Pearson r = %.3f  Spearman rho = %.3f" % (len(table), n, r_, rho))
+        if a.json:
+            with open(a.json, "w") as f:
+                json.dump({"pearson": r_, "spearman": rho, "rows": table}, f, indent=1)
         return 0
     if a.cmd == "orders":
         sweep_orders(a.dtype, a.M, a.N, a.K, a.out)

@@ -118,3 +118,74 @@ def test_dram_falls_with_a_larger_last_level_cache():
     mid = tm.predict_dram(M, N, K, 2, 256, 256, 0, 0, 1, mall_bytes=256 << 20)
     huge = tm.predict_dram(M, N, K, 2, 256, 256, 0, 0, 1, mall_bytes=4 << 30)
     assert small >= mid >= huge == (M + N) * K * 2
+
+
+# ---------------------------------------------------------------- conv model
+
+def _sched(**kw):
+    d = dict(block_m=64, block_n=128, block_k=32, wave_m=32, wave_n=64, mfma_m=32, mfma_n=32,
+             mfma_k=2, lds_stages=3, lds_pad=-1, unroll_k=0, raster=0, xcd_remap=1, k_order=0, k_split=1)
+    d.update(kw)
+    return d
+
+
+def test_conv_one_image_per_xcd_reads_input_once():
+    # 8 images of 16x16 (one 64x256 flattened tile each), XCD remap: each XCD
+    # reads exactly one image and the weights of the one output-channel tile
+    dims = (8, 32, 16, 16, 64, 3, 3, 1, 1)
+    r, w = tm.predict_conv("f32", _sched(block_n=256), dims, 1)
+    assert r == 8 * 32 * 16 * 16 * 4 + 8 * 64 * 32 * 9 * 4
+    assert w == 8 * 64 * 16 * 16 * 4
+
+
+def test_conv_halo_rows_are_read_by_both_neighbouring_xcds():
+    # one 32x32 image cut into 8 flattened tiles of 4 output rows: with
+    # round-robin XCDs every tile sits on its own XCD and reads its 4 rows
+    # plus the rows above and below it (3x3, pad 1), clipped at the image edge
+    N, C, H, W = 1, 16, 32, 32
+    dims = (N, C, H, W, 64, 3, 3, 1, 1)
+    r, _ = tm.predict_conv("f32", _sched(block_n=128, xcd_remap=0), dims, 1)
+    rows = sum(min(H - 1, 4 * t + 4) - max(0, 4 * t - 1) + 1 for t in range(8))
+    assert rows == 8 * 6 - 2
+    assert r == rows * C * W * 4 + 8 * 64 * C * 9 * 4
+
+
+def test_conv_grid_follows_the_launchers():
+    # the benchmark layer: balanced halo tiles of 196 (one half) or 392
+    # pixels (two halves), row-streaming bands of 7 rows for bf16
+    dims = (32, 64, 56, 56, 64, 3, 3, 1, 1)
+    bm, tmm, tn, seg, force = tm.conv_grid("f32", _sched(block_n=208, k_order=2, block_k=8), *dims)
+    assert (bm, tmm, tn, force) == (64, 1, 32 * 16, None)
+    assert seg(17) == [(1, 2, 7)]             # image 1, pixels 196..391: output rows 3..6
+    bm, tmm, tn, seg, force = tm.conv_grid("f32", _sched(block_n=416, k_order=2, block_k=8), *dims)
+    assert tn == 32 * 8
+    bm, tmm, tn, seg, force = tm.conv_grid("bf16", _sched(block_n=64, k_order=3), *dims)
+    assert (tn, force) == (32 * 8, 1) and seg(9) == [(1, 6, 15)]   # band 1: input rows 6 .. 15
+    # 28x28 rows are too short for the halo tiles: the tap-major 64x256
+    # fallback, whose flattened tiles run across images
+    small = (8, 128, 28, 28, 256, 3, 3, 1, 1)
+    bm, tmm, tn, seg, force = tm.conv_grid("f32", _sched(block_n=208, k_order=2, block_k=8), *small)
+    assert (bm, tmm, tn) == (64, 4, -(-8 * 784 // 256))
+    assert seg(3) == [(0, 26, 27), (1, 0, 9)]   # pixels 768..1023 span images 0 and 1
+    # bf16 with 128 channels: no row streaming, no halo tile; the gather kernel's 64x128 tiles
+    bm, tmm, tn, seg, force = tm.conv_grid("bf16", _sched(block_n=64, k_order=3), *small)
+    assert (bm, tn) == (64, 8 * 784 // 128)
+
+
+# FETCH_SIZE x 1024 x 1.9998 bytes per launch (mean of two), one counter pass
+# per shape: (dtype, dims, instance fields, raster, remap, occupancy) -> bytes
+MEASURED_CONV = [
+    ("f32", (32, 64, 56, 56, 64, 3, 3, 1, 1), dict(block_n=416, block_k=8, k_order=2, lds_stages=2), 0, 1, 1, 28.06e6),
+    ("f32", (32, 64, 56, 56, 64, 3, 3, 1, 1), dict(block_n=256, k_order=1, lds_stages=2), 0, 1, 2, 27.70e6),
+    ("f32", (8, 128, 28, 28, 256, 3, 3, 1, 1), dict(block_n=128, k_order=1, lds_stages=2), 0, 0, 3, 24.59e6),
+    ("f32", (8, 128, 28, 28, 256, 3, 3, 1, 1), dict(block_n=64, k_order=1, lds_stages=2), 1, 0, 5, 28.22e6),
+    ("f32", (8, 128, 28, 28, 256, 3, 3, 1, 1), dict(block_m=128, block_n=128, k_order=1, lds_stages=2), 0, 1, 2, 12.32e6),
+    ("bf16", (32, 64, 56, 56, 64, 3, 3, 1, 1), dict(block_n=64, block_k=16, k_order=3, lds_stages=2), 0, 0, 1, 13.64e6),
+    ("bf16", (8, 128, 28, 28, 256, 3, 3, 1, 1), dict(block_n=64, k_order=0, lds_stages=2), 0, 0, 5, 17.68e6),
+]
+
+
+@pytest.mark.parametrize("dtype,dims,fields,raster,remap,occ,measured", MEASURED_CONV)
+def test_conv_model_against_counters(dtype, dims, fields, raster, remap, occ, measured):
+    r, _ = tm.predict_conv(dtype, _sched(raster=raster, xcd_remap=remap, **fields), dims, occ)
+    assert 0.9 <= r / measured <= 1.0
