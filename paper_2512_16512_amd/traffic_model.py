@@ -1,5 +1,5 @@
-"""Analytic model of the HBM traffic of a matmul schedule, and its evaluation
-against hardware counters.
+"""Analytic model of the HBM traffic of a matmul or conv schedule, and its
+evaluation against hardware counters.
 
 The GPU counterpart of the paper's cache-model study (Sec. 6.3, Fig. 13,
 Table 2): a model predicts, for every schedule of a design space, the misses
@@ -32,11 +32,19 @@ so that term is evaluated against kernel time over the tile orders
 (``orders`` / ``evaluate-orders``), together with the L2 term and their
 unweighted sum.
 
+Convolutions (``conv_grid``, ``predict_conv``) follow the same L2 rule with
+the launchers' own tile grids; a workgroup's footprint is the weights of its
+output-channel tile and the input rows its output rows reach.
+
 Usage (the measurement step runs under rocprofv3; see ``run``)::
 
     rocprofv3 --pmc FETCH_SIZE -f csv -d OUT -o run -- \\
         python3 -m paper_2512_16512_amd.traffic_model run f32 4096 4096 4096 --order ORDER.json
     python -m paper_2512_16512_amd.traffic_model correlate ORDER.json OUT/run_counter_collection.csv \\
+        --fetch-scale 2.0
+    rocprofv3 --pmc FETCH_SIZE -f csv -d OUT -o run -- \\
+        python3 -m paper_2512_16512_amd.traffic_model run-conv f32 32 64 56 56 64 3 3 1 1 --order ORDER.json
+    python -m paper_2512_16512_amd.traffic_model correlate-conv ORDER.json OUT/run_counter_collection.csv \\
         --fetch-scale 2.0
 """
 from __future__ import annotations
