@@ -1395,9 +1395,12 @@ conv2d_f32_smallm_kernel(ConvArgs p) {
 //  - the k-offset table relative to the patch, k -> c*PR*WP + kh*WP + kw.
 // An output pixel's B value at k is then patch[pix_base + ktab[k]] with
 // pix_base = (oh*stride_h - pad_h - ih_lo)*WP + ow*stride_w: no bounds
-// checks in the K loop, which reads only LDS.
+// checks in the K loop, which reads only LDS.  Eight waves stage; waves 0-3
+// and 4-7 then reduce the two halves of K for the same pixel blocks, and the
+// second half's partial sums reach the first through the patch area.
 namespace smallm {
 constexpr int PATCH_MAX_BYTES = 48 * 1024;
+constexpr int PWAVES = 8, PNT = 64 * PWAVES;   // patch-staged kernel: two reduction halves of 4 waves
 
 // Geometry of the patch-staged kernel for a launch: rows PR and padded
 // width WP of the patch, or PR = 0 when the patch does not fit.
@@ -1411,7 +1414,10 @@ __host__ __device__ inline PatchGeom patch_geom(const ConvArgs &a, int bn) {
     g.WP = (a.OW - 1) * a.sw + a.S;
     const long long K = (long long)a.C * a.R * a.S;
     const long long kp = (K + 31) / 32 * 32;
-    const long long bytes = 4LL * ((long long)a.C * g.PR * g.WP + 16 * (kp + 2)) + 4 * kp;
+    // the patch area also holds the second half's partial sums at the end
+    // (4 waves x 64 lanes x 2 chains x bn / 64 blocks x 4 floats)
+    const long long area = max((long long)a.C * g.PR * g.WP, 32LL * bn);
+    const long long bytes = 4LL * (area + 16 * (kp + 2)) + 4 * kp;
     // the staging loops cover up to 256 padded columns and 256 k
     g.bytes = (bytes <= PATCH_MAX_BYTES && g.WP <= 256 && kp <= 256) ? (int)bytes : 0;
     if (g.bytes == 0) g.PR = 0;
@@ -1420,7 +1426,7 @@ __host__ __device__ inline PatchGeom patch_geom(const ConvArgs &a, int bn) {
 }  // namespace smallm
 
 template <int NB, int NCH>
-__global__ void __launch_bounds__(smallm::NT)
+__global__ void __launch_bounds__(smallm::PNT)
 conv2d_f32_smallm_patch_kernel(ConvArgs p) {
     typedef F32Mfma<16> MF;
     constexpr int BN = 16 * NB * smallm::WAVES;
@@ -1429,6 +1435,9 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int l16 = lane & 15, g = lane >> 4;
+    // waves 0-3 and 4-7 take the two halves of the reduction over the same
+    // pixel blocks (two waves per SIMD); all eight stage
+    const int half = wave >> 2, wq = wave & 3;
 
     const int C = p.C, H = p.H, Wd = p.W, R = p.R, S = p.S;
     const int OC = p.OC, OW = p.OW, OHW = p.OH * OW;
@@ -1449,8 +1458,9 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
     // output channels x 2 lane groups) then covers 32 distinct banks (KP is
     // a multiple of 32, so rows KP apart would all share one bank)
     const int WS = KP + 2;
+    const int AREA = max(C * PLANE, 32 * BN);           // the patch, later the partial sums
     float *patch = sm;                                  // [C][PR][WP]
-    float *wl = sm + C * PLANE;                         // [16][WS]
+    float *wl = sm + AREA;                              // [16][WS]
     int *ktab = reinterpret_cast<int *>(wl + 16 * WS);  // [KP]
 
     const __amdgpu_buffer_rsrc_t rw =
@@ -1459,18 +1469,18 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
         __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(p.X), 0, p.Nb * C * H * Wd * 4, 0x00020000);
 
     // Stage the patch, the weights and the table (zeros where out of range).
-    // Wave w takes patch rows w, w + 4, ...; lane l takes columns l + 64q
+    // Wave w takes patch rows w, w + 8, ...; lane l takes columns l + 64q
     // (WP <= 256); every load of a batch is issued before its LDS stores.
     const int xb = img * C * H * Wd;
     const int nrows = C * PR;
-    constexpr int RPW = 8;   // rows per wave per batch
-    // Weights first (wave w takes output channels w, w + 4, w + 8, w + 12),
-    // so that their loads and the patch's are in flight together: one round
-    // trip to memory for the whole staging.
-    float wv[4][4];
+    constexpr int RPW = 4;   // rows per wave per batch
+    // Weights first (wave w takes output channels w and w + 8), so that
+    // their loads and the patch's are in flight together: one round trip to
+    // memory for the whole staging.
+    float wv[2][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int o = wave + smallm::WAVES * i;
+    for (int i = 0; i < 2; ++i) {
+        const int o = wave + smallm::PWAVES * i;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int k = lane + 64 * q;
@@ -1487,16 +1497,16 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
         const int kh = rem / S, kw = rem - kh * S;
         tk = ic * PLANE + kh * WP + kw;
     }
-    // (channel, patch row) of row `wave`, stepped by 4 rows without division
+    // (channel, patch row) of row `wave`, stepped by 8 rows without division
     int c_next = wave / PR, r_next = wave - c_next * PR;
-    for (int rb = wave; rb < nrows; rb += smallm::WAVES * RPW) {
+    for (int rb = wave; rb < nrows; rb += smallm::PWAVES * RPW) {
         float v[RPW][4];
         int c = c_next, r = r_next;
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
-            const int row = rb + smallm::WAVES * i;
+            const int row = rb + smallm::PWAVES * i;
             if (i > 0) {
-                r += smallm::WAVES;
+                r += smallm::PWAVES;
                 while (r >= PR) {   // uniform
                     r -= PR;
                     ++c;
@@ -1514,12 +1524,12 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
         }
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
-            const int row = rb + smallm::WAVES * i;
+            const int row = rb + smallm::PWAVES * i;
 #pragma unroll
             for (int q = 0; q < 4; ++q)
                 if (row < nrows && lane + 64 * q < WP) patch[row * WP + lane + 64 * q] = v[i][q];
         }
-        r += smallm::WAVES;   // the next batch's first row
+        r += smallm::PWAVES;   // the next batch's first row
         while (r >= PR) {
             r -= PR;
             ++c;
@@ -1529,14 +1539,14 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
     }
     // the weights' stores, after the patch: their loads were issued first
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            if (lane + 64 * q < KP) wl[(wave + smallm::WAVES * i) * WS + lane + 64 * q] = wv[i][q];
+            if (lane + 64 * q < KP) wl[(wave + smallm::PWAVES * i) * WS + lane + 64 * q] = wv[i][q];
     if (tid < KP) ktab[tid] = tk;
 
     // this lane's pixel of each of its blocks (position 0 past the image)
-    const int n0 = p0 + wave * 16 * NB;
+    const int n0 = p0 + wq * 16 * NB;
     int pb[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
@@ -1558,59 +1568,85 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
     __syncthreads();
 
     // k-step s: lane group g takes k = 4s + g.  Steps run in NCH chunks of
-    // 8 (KP = 32 * NCH: padded steps have zero weights).  The table entries
-    // of every chunk are read first, in one batch, so that no input read
-    // waits on a table read: the input values and weights of chunk c + 1
-    // are then read while chunk c's MFMAs run.  Even and odd steps
+    // 8 (KP = 32 * NCH: padded steps have zero weights); the first half of
+    // the waves takes chunks 0 .. NC0 - 1, the second half the rest.  A
+    // half's table entries are read first, in one batch, so that no input
+    // read waits on a table read: the input values and weights of chunk
+    // c + 1 are then read while chunk c's MFMAs run.  Even and odd steps
     // accumulate into two chains.
+    constexpr int NC0 = (NCH + 1) / 2;
     const float *wrow = wl + l16 * WS + g;
-    int tv[NCH][8];
+    auto reduce_chunks = [&](auto C0, auto C1) __attribute__((always_inline)) {
+        constexpr int CA = decltype(C0)::value, CB = decltype(C1)::value;
+        if constexpr (CB > CA) {
+            int tv[CB - CA][8];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c)
+            for (int c = CA; c < CB; ++c)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) tv[c][i] = ktab[32 * c + 4 * i + g];
-    float av[2][8], bv[2][NB][8];
-    auto rd = [&](int buf, int c) __attribute__((always_inline)) {
+                for (int i = 0; i < 8; ++i) tv[c - CA][i] = ktab[32 * c + 4 * i + g];
+            float av[2][8], bv[2][NB][8];
+            auto rd = [&](int buf, int c) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            av[buf][i] = wrow[32 * c + 4 * i];
+                for (int i = 0; i < 8; ++i) {
+                    av[buf][i] = wrow[32 * c + 4 * i];
 #pragma unroll
-            for (int j = 0; j < NB; ++j) bv[buf][j][i] = patch[pb[j] + tv[c][i]];
-        }
-    };
-    auto mm = [&](int buf) __attribute__((always_inline)) {
+                    for (int j = 0; j < NB; ++j) bv[buf][j][i] = patch[pb[j] + tv[c - CA][i]];
+                }
+            };
+            auto mm = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+                for (int i = 0; i < 8; ++i)
 #pragma unroll
-            for (int j = 0; j < NB; ++j) acc[i & 1][j] = MF::mma(av[buf][i], bv[buf][j][i], acc[i & 1][j]);
-    };
-    rd(0, 0);
+                    for (int j = 0; j < NB; ++j) acc[i & 1][j] = MF::mma(av[buf][i], bv[buf][j][i], acc[i & 1][j]);
+            };
+            rd(0, CA);
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-        if (c + 1 < NCH) rd((c + 1) & 1, c + 1);
-        mm(c & 1);
-        if (c + 1 < NCH) {
-            // the next chunk's reads between this chunk's instructions: in
-            // one run they would exceed the 15 reads the LDS counter can
-            // wait past, and each instruction would wait for some of them
+            for (int c = CA; c < CB; ++c) {
+                if (c + 1 < CB) rd((c + 1 - CA) & 1, c + 1);
+                mm((c - CA) & 1);
+                if (c + 1 < CB) {
+                    // the next chunk's reads between this chunk's instructions: in
+                    // one run they would exceed the 15 reads the LDS counter can
+                    // wait past, and each instruction would wait for some of them
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                __builtin_amdgcn_sched_group_barrier(0x008, NB, 0);          // MFMA
-                __builtin_amdgcn_sched_group_barrier(0x100, 1 + NB, 0);      // LDS reads
+                    for (int i = 0; i < 8; ++i) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, NB, 0);          // MFMA
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1 + NB, 0);      // LDS reads
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
-            __builtin_amdgcn_sched_barrier(0);
         }
+    };
+    if (half == 0)
+        reduce_chunks(std::integral_constant<int, 0>(), std::integral_constant<int, NC0>());
+    else
+        reduce_chunks(std::integral_constant<int, NC0>(), std::integral_constant<int, NCH>());
+
+    // the second half's partial sums through the patch area (every wave is
+    // done reading the patch), added by the first half in a fixed order
+    __syncthreads();
+    f32x4 *part = reinterpret_cast<f32x4 *>(patch);   // [wq][chain][block][lane]
+    if (half == 1) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int j = 0; j < NB; ++j) part[((wq * 2 + h) * NB + j) * 64 + lane] = acc[h][j];
     }
+    __syncthreads();
+    if (half == 1) return;
 
     float *__restrict__ Y = p.Y + (size_t)img * OC * OHW;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
         const int pix = n0 + 16 * j + l16;
+        const f32x4 q0 = part[((wq * 2 + 0) * NB + j) * 64 + lane];
+        const f32x4 q1 = part[((wq * 2 + 1) * NB + j) * 64 + lane];
         if (pix >= OHW) continue;
 #pragma unroll
         for (int r = 0; r < MF::NACC; ++r) {
             const int o = m0 + MF::row(lane, r);
-            const float v = acc[0][j][r] + acc[1][j][r];
+            const float v = (acc[0][j][r] + acc[1][j][r]) + (q0[r] + q1[r]);
             if (o < OC) Y[(size_t)o * OHW + pix] = (p.relu && v < 0.f) ? 0.f : v;
         }
     }
@@ -1637,7 +1673,7 @@ hipError_t launch_conv_f32_smallm(const ConvArgs &a, hipStream_t s) {
             reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 8>)};
         // patch_geom admits K up to 256 (KP / 32 = 1 .. 8 chunks)
         const int nch = (a.C * a.R * a.S + 31) / 32;
-        return hipLaunchKernel(fns[nch - 1], dim3(tiles), dim3(smallm::NT), kargs, (size_t)geo.bytes, s);
+        return hipLaunchKernel(fns[nch - 1], dim3(tiles), dim3(smallm::PNT), kargs, (size_t)geo.bytes, s);
     }
     const int N = a.Nb * a.OH * a.OW, K = a.C * a.R * a.S;
     const unsigned tiles = (unsigned)(((a.OC + 15) / 16) * ((N + BN - 1) / BN));

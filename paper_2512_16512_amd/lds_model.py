@@ -621,9 +621,12 @@ def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
     """One launch of the patch-staged few-output-channel fp32 conv
     (csrc/conv2d_f32.hip), or None when its patch does not fit (then the
     gather form runs, which uses LDS only for the k-offset table): per
-    workgroup the staging stores (ds_write_b32 of consecutive lanes) and, per
-    k-step, the table entry, the weight and the input value (ds_read_b32)."""
-    BN, WAVES = 64, 4
+    workgroup the staging stores (ds_write_b32 of consecutive lanes, spread
+    over eight waves), per k-step and pixel block the table entry, the weight
+    and the input value (ds_read_b32; the two halves of the waves take the
+    two halves of the k-steps), and the second half's partial sums written
+    and read back once (ds_write_b128 / ds_read_b128, lane-contiguous)."""
+    BN, WAVES, SWAVES = 64, 4, 8
     OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
     OHW = OH * OW
     K = C * R * S
@@ -631,7 +634,8 @@ def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
     WS = KP + 2
     span = (BN - 1 + OW - 1) // OW + 1
     PR, WP = (span - 1) * sh + R, (OW - 1) * sw + S
-    if 4 * (C * PR * WP + 16 * (KP + 2)) + 4 * KP > 48 * 1024 or WP > 256 or KP > 256:
+    AREA = max(C * PR * WP, 32 * BN)            # the patch, later the partial sums
+    if 4 * (AREA + 16 * (KP + 2)) + 4 * KP > 48 * 1024 or WP > 256 or KP > 256:
         return None
     PLANE = PR * WP
 
@@ -650,11 +654,14 @@ def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
         oh_a = p0 // OW
         # staging: patch rows (4 column groups each), weights, table
         rows = C * PR
-        for w in range(WAVES):
-            nr = len(range(w, rows, WAVES))
+        for w in range(SWAVES):
+            nr = len(range(w, rows, SWAVES))
             per_image.add("ds_write_b32", contiguous, times=nr * _cdiv(WP, 64))
-            per_image.add("ds_write_b32", contiguous, times=4 * _cdiv(KP, 64))
+            per_image.add("ds_write_b32", contiguous, times=2 * _cdiv(KP, 64))
         per_image.add("ds_write_b32", contiguous, times=_cdiv(KP, 64))
+        red = [16 * lane for lane in range(64)]
+        per_image.add("ds_write_b128", red, times=WAVES * 2)
+        per_image.add("ds_read_b128", red, times=WAVES * 2)
         for w in range(WAVES):
             pb = []
             for lane in range(64):
@@ -666,7 +673,7 @@ def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
                     pb.append(0)
             for s in range(KP // 4):
                 per_image.add("ds_read_b32", [4 * tab(4 * s + (lane >> 4)) for lane in range(64)])
-                per_image.add("ds_read_b32", [4 * (PLANE * C + (lane & 15) * WS + (lane >> 4) + 4 * s)
+                per_image.add("ds_read_b32", [4 * (AREA + (lane & 15) * WS + (lane >> 4) + 4 * s)
                                               for lane in range(64)])
                 per_image.add("ds_read_b32", [4 * (pb[lane] + tab(4 * s + (lane >> 4))) for lane in range(64)])
     return per_image.scaled(_cdiv(OC, 16) * N)
