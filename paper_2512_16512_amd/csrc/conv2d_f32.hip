@@ -1395,23 +1395,29 @@ conv2d_f32_smallm_kernel(ConvArgs p) {
 //  - the k-offset table relative to the patch, k -> c*PR*WP + kh*WP + kw.
 // An output pixel's B value at k is then patch[pix_base + ktab[k]] with
 // pix_base = (oh*stride_h - pad_h - ih_lo)*WP + ow*stride_w: no bounds
-// checks in the K loop, which reads only LDS.  Eight waves stage; waves 0-3
-// and 4-7 then reduce the two halves of K for the same pixel blocks, and the
-// second half's partial sums reach the first through the patch area.
+// checks in the K loop, which reads only LDS.  Eight waves stage (16-byte
+// chunks of the input rows where the width allows); waves 0-3 and 4-7 then
+// reduce the two halves of K for the same pixel blocks, and the second
+// half's partial sums reach the first through the patch area.
 namespace smallm {
 constexpr int PATCH_MAX_BYTES = 48 * 1024;
 constexpr int PWAVES = 8, PNT = 64 * PWAVES;   // patch-staged kernel: two reduction halves of 4 waves
 
-// Geometry of the patch-staged kernel for a launch: rows PR and padded
-// width WP of the patch, or PR = 0 when the patch does not fit.
+// Geometry of the patch-staged kernel for a launch: rows PR and width WP
+// of the patch and the patch column PADL of input column 0, or PR = 0 when
+// the patch does not fit.  With 16-byte row loads (vec) PADL and WP are
+// multiples of 4, so that every 4-column chunk of the patch is one aligned
+// chunk of an input row or lies wholly outside it.
 struct PatchGeom {
-    int PR, WP, bytes;
+    int PR, WP, PADL, bytes;
 };
-__host__ __device__ inline PatchGeom patch_geom(const ConvArgs &a, int bn) {
+__host__ __device__ inline PatchGeom patch_geom(const ConvArgs &a, int bn, bool vec) {
     const int span = (bn - 1 + a.OW - 1) / a.OW + 1;   // output rows a tile can touch
     PatchGeom g;
     g.PR = (span - 1) * a.sh + a.R;
-    g.WP = (a.OW - 1) * a.sw + a.S;
+    g.PADL = vec ? (a.pw + 3) / 4 * 4 : a.pw;
+    g.WP = (a.OW - 1) * a.sw + a.S - a.pw + g.PADL;
+    if (vec) g.WP = (g.WP + 3) / 4 * 4;
     const long long K = (long long)a.C * a.R * a.S;
     const long long kp = (K + 31) / 32 * 32;
     // the patch area also holds the second half's partial sums at the end
@@ -1425,12 +1431,12 @@ __host__ __device__ inline PatchGeom patch_geom(const ConvArgs &a, int bn) {
 }
 }  // namespace smallm
 
-template <int NB, int NCH>
+template <int NB, int NCH, bool VEC>
 __global__ void __launch_bounds__(smallm::PNT)
 conv2d_f32_smallm_patch_kernel(ConvArgs p) {
     typedef F32Mfma<16> MF;
     constexpr int BN = 16 * NB * smallm::WAVES;
-    extern __shared__ float sm[];
+    extern __shared__ __attribute__((aligned(16))) float sm[];   // 16-byte patch rows and partial sums
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -1443,8 +1449,8 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
     const int OC = p.OC, OW = p.OW, OHW = p.OH * OW;
     const int K = C * R * S, KP = (K + 31) / 32 * 32;
     const int RS = R * S;
-    const smallm::PatchGeom geo = smallm::patch_geom(p, BN);
-    const int PR = geo.PR, WP = geo.WP, PLANE = PR * WP;
+    const smallm::PatchGeom geo = smallm::patch_geom(p, BN, VEC);
+    const int PR = geo.PR, WP = geo.WP, PADL = geo.PADL, PLANE = PR * WP;
 
     const int chunks = (OHW + BN - 1) / BN;   // tiles per image
     const int tiles_m = (OC + 15) / 16, tiles_n = p.Nb * chunks;
@@ -1470,7 +1476,8 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
 
     // Stage the patch, the weights and the table (zeros where out of range).
     // Wave w takes patch rows w, w + 8, ...; lane l takes columns l + 64q
-    // (WP <= 256); every load of a batch is issued before its LDS stores.
+    // (WP <= 256), or with 16-byte loads columns 4l .. 4l + 3; every load of
+    // a batch is issued before its LDS stores.
     const int xb = img * C * H * Wd;
     const int nrows = C * PR;
     constexpr int RPW = 4;   // rows per wave per batch
@@ -1514,20 +1521,39 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
             }
             const int ih = ih_lo + r;
             const bool rok = row < nrows && (unsigned)ih < (unsigned)H;
+            if constexpr (VEC) {
+                // W and PADL are multiples of 4: a chunk is wholly inside the row or outside it
+                const int iw = 4 * lane - PADL;
+                const bool in = rok && 4 * lane < WP && (unsigned)iw < (unsigned)Wd;
+                const f32x4 t = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                              rx, in ? (xb + (c * H + ih) * Wd + iw) * 4 : kOOB, 0, 0));
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int iw = lane + 64 * q - p.pw;
-                const bool in = rok && lane + 64 * q < WP && (unsigned)iw < (unsigned)Wd;
-                v[i][q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                                        rx, in ? (xb + (c * H + ih) * Wd + iw) * 4 : kOOB, 0, 0));
+                for (int q = 0; q < 4; ++q) v[i][q] = t[q];
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int iw = lane + 64 * q - PADL;
+                    const bool in = rok && lane + 64 * q < WP && (unsigned)iw < (unsigned)Wd;
+                    v[i][q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                            rx, in ? (xb + (c * H + ih) * Wd + iw) * 4 : kOOB, 0, 0));
+                }
             }
         }
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             const int row = rb + smallm::PWAVES * i;
+            if constexpr (VEC) {
+                if (row < nrows && 4 * lane < WP) {
+                    f32x4 t;
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                if (row < nrows && lane + 64 * q < WP) patch[row * WP + lane + 64 * q] = v[i][q];
+                    for (int q = 0; q < 4; ++q) t[q] = v[i][q];
+                    *reinterpret_cast<f32x4 *>(patch + row * WP + 4 * lane) = t;
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (row < nrows && lane + 64 * q < WP) patch[row * WP + lane + 64 * q] = v[i][q];
+            }
         }
         r += smallm::PWAVES;   // the next batch's first row
         while (r >= PR) {
@@ -1554,7 +1580,7 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
         pb[j] = 0;
         if (pix < OHW) {
             const int oh = pix / OW, ow = pix - oh * OW;
-            pb[j] = (oh * p.sh - p.ph - ih_lo) * WP + ow * p.sw;
+            pb[j] = (oh * p.sh - p.ph - ih_lo) * WP + ow * p.sw + PADL - p.pw;
         }
     }
 
@@ -1655,25 +1681,34 @@ conv2d_f32_smallm_patch_kernel(ConvArgs p) {
 template <int NB, int KC>
 hipError_t launch_conv_f32_smallm(const ConvArgs &a, hipStream_t s) {
     constexpr int BN = 16 * NB * smallm::WAVES, KCH = 4 * KC;
-    const smallm::PatchGeom geo = smallm::patch_geom(a, BN);
+    // 16-byte patch loads need 16-byte aligned input rows
+    bool vec = a.W % 4 == 0 && (reinterpret_cast<uintptr_t>(a.X) & 15) == 0;
+    smallm::PatchGeom geo = smallm::patch_geom(a, BN, vec);
+    if (vec && geo.PR == 0) {
+        vec = false;
+        geo = smallm::patch_geom(a, BN, false);
+    }
     if (geo.PR > 0) {
         const int OHW = a.OH * a.OW;
         const unsigned tiles =
             (unsigned)(((a.OC + 15) / 16) * a.Nb * ((OHW + BN - 1) / BN));
         ConvArgs args = a;
         void *kargs[] = {&args};
-        static const void *const fns[8] = {
-            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 1>),
-            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 2>),
-            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 3>),
-            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 4>),
-            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 5>),
-            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 6>),
-            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 7>),
-            reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 8>)};
+#define XTC_PATCH_FNS(V)                                                                    \
+    {reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 1, V>),               \
+     reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 2, V>),               \
+     reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 3, V>),               \
+     reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 4, V>),               \
+     reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 5, V>),               \
+     reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 6, V>),               \
+     reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 7, V>),               \
+     reinterpret_cast<const void *>(&conv2d_f32_smallm_patch_kernel<NB, 8, V>)}
+        static const void *const fns[2][8] = {XTC_PATCH_FNS(false), XTC_PATCH_FNS(true)};
+#undef XTC_PATCH_FNS
         // patch_geom admits K up to 256 (KP / 32 = 1 .. 8 chunks)
         const int nch = (a.C * a.R * a.S + 31) / 32;
-        return hipLaunchKernel(fns[nch - 1], dim3(tiles), dim3(smallm::PNT), kargs, (size_t)geo.bytes, s);
+        return hipLaunchKernel(fns[vec ? 1 : 0][nch - 1], dim3(tiles), dim3(smallm::PNT), kargs,
+                               (size_t)geo.bytes, s);
     }
     const int N = a.Nb * a.OH * a.OW, K = a.C * a.R * a.S;
     const unsigned tiles = (unsigned)(((a.OC + 15) / 16) * ((N + BN - 1) / BN));

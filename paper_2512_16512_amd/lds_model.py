@@ -617,7 +617,7 @@ def matmul_launch(dtype: str, s: dict, M: int, N: int, K: int):
 
 # ---------------------------------------------------- few-output-channel conv
 
-def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
+def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw, vec=None):
     """One launch of the patch-staged few-output-channel fp32 conv
     (csrc/conv2d_f32.hip), or None when its patch does not fit (then the
     gather form runs, which uses LDS only for the k-offset table): per
@@ -625,17 +625,35 @@ def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
     over eight waves), per k-step and pixel block the table entry, the weight
     and the input value (ds_read_b32; the two halves of the waves take the
     two halves of the k-steps), and the second half's partial sums written
-    and read back once (ds_write_b128 / ds_read_b128, lane-contiguous)."""
+    and read back once (ds_write_b128 / ds_read_b128, lane-contiguous).
+    ``vec``: 16-byte patch rows (the launcher's choice for widths that are
+    a multiple of 4 and 16-byte aligned inputs, taken here for every such
+    width): one ds_write_b128 per lane and row, the patch origin at a
+    multiple of 4 columns."""
     BN, WAVES, SWAVES = 64, 4, 8
+    if vec is None:
+        vec = W % 4 == 0
     OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
     OHW = OH * OW
     K = C * R * S
     KP = _cdiv(K, 32) * 32
     WS = KP + 2
     span = (BN - 1 + OW - 1) // OW + 1
-    PR, WP = (span - 1) * sh + R, (OW - 1) * sw + S
-    AREA = max(C * PR * WP, 32 * BN)            # the patch, later the partial sums
-    if 4 * (AREA + 16 * (KP + 2)) + 4 * KP > 48 * 1024 or WP > 256 or KP > 256:
+
+    def geom(v):
+        padl = _cdiv(pw, 4) * 4 if v else pw
+        wp = (OW - 1) * sw + S - pw + padl
+        if v:
+            wp = _cdiv(wp, 4) * 4
+        pr = (span - 1) * sh + R
+        area = max(C * pr * wp, 32 * BN)        # the patch, later the partial sums
+        fits = 4 * (area + 16 * (KP + 2)) + 4 * KP <= 48 * 1024 and wp <= 256 and KP <= 256
+        return fits, pr, wp, padl, area
+    fits, PR, WP, PADL, AREA = geom(vec)
+    if vec and not fits:
+        vec = False
+        fits, PR, WP, PADL, AREA = geom(False)
+    if not fits:
         return None
     PLANE = PR * WP
 
@@ -656,7 +674,12 @@ def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
         rows = C * PR
         for w in range(SWAVES):
             nr = len(range(w, rows, SWAVES))
-            per_image.add("ds_write_b32", contiguous, times=nr * _cdiv(WP, 64))
+            if vec:
+                # lanes past the row are masked; counted like the rest, as
+                # for the 4-byte stores
+                per_image.add("ds_write_b128", [16 * lane for lane in range(64)], times=nr)
+            else:
+                per_image.add("ds_write_b32", contiguous, times=nr * _cdiv(WP, 64))
             per_image.add("ds_write_b32", contiguous, times=2 * _cdiv(KP, 64))
         per_image.add("ds_write_b32", contiguous, times=_cdiv(KP, 64))
         red = [16 * lane for lane in range(64)]
@@ -668,7 +691,7 @@ def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw):
                 pix = p0 + w * 16 + (lane & 15)
                 if pix < OHW:
                     oh, ow = divmod(pix, OW)
-                    pb.append((oh - oh_a) * sh * WP + ow * sw)
+                    pb.append((oh - oh_a) * sh * WP + ow * sw + PADL - pw)
                 else:
                     pb.append(0)
             for s in range(KP // 4):

@@ -217,6 +217,9 @@ def test_conv_asymmetric_exact_every_instance(x, dtype, shape):
     (1, 8, 61, 59, 64, 3, 3, 1, 1),     # balanced halo: 400-pixel tiles, second half 12 blocks
     (1, 8, 69, 58, 64, 3, 3, 1, 1),     # balanced halo: 401-pixel tiles, second half 13 blocks
     (2, 8, 7, 57, 48, 3, 3, 1, 1),      # balanced halo: 399-pixel tiles, one tile per image
+    (1, 3, 30, 28, 16, 7, 7, 2, 3),     # few channels, 16-byte patch rows: 7x7 stride 2, origin 4
+    (2, 4, 16, 16, 12, 3, 3, 1, 0),     # 16-byte patch rows, no padding (origin 0), OC = 12
+    (1, 2, 12, 16, 16, 3, 3, 1, 4),     # 16-byte patch rows, pad 4 (origin 4, 20-wide output)
 ])
 def test_conv_small_int_exact_every_instance(x, shape):
     N, C, H, W_, OC, R, S, stride, pad = shape

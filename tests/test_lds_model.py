@@ -133,12 +133,16 @@ def test_bf16_row_streaming_conv_matches_counters():
 
 
 def test_small_channel_conv_matches_counters():
-    # measured on the patch-staged kernel with two reduction halves:
-    # 272048 LDS-active cycles and 784 conflict cycles per launch
-    c = L.conv_launch("f32", dict(k_order=0, block_n=64, block_m=16, lds_stages=0),
-                      1, 3, 224, 224, 16, 7, 7, 2, 3)
-    assert c.active == pytest.approx(272048, rel=1e-2)
-    assert c.conflict == 784
+    # measured on the patch-staged kernel with two reduction halves and
+    # 16-byte patch rows: 279888 LDS-active cycles and 8624 conflict cycles
+    # per launch (7x7 layer), 373184 and 18816 (4x16x56x56 -> 16, 3x3)
+    s = dict(k_order=0, block_n=64, block_m=16, lds_stages=0)
+    c = L.conv_launch("f32", s, 1, 3, 224, 224, 16, 7, 7, 2, 3)
+    assert c.active == pytest.approx(279888, rel=1e-2)
+    assert c.conflict == 8624
+    c = L.conv_launch("f32", s, 4, 16, 56, 56, 16, 3, 3, 1, 1)
+    assert c.active == pytest.approx(373184, rel=1e-2)
+    assert c.conflict == 18816
 
 
 def test_unmodelled_kernels_return_none():
