@@ -504,10 +504,11 @@ hipError_t launch_conv_bf16_halo(const ConvArgs &a, hipStream_t s) {
 //  - all C*R*S = 576 weights of its 64 output channels stay in LDS for the
 //    whole band (72 KiB, loaded once);
 //  - input rows pass through a ring of NR = 8 LDS rows: the four rows a step
-//    reads, the two the next step adds (stored at the start of the step,
+//    reads, the two the next step adds (stored at the end of the step,
 //    published by the step's barrier) and two slots free for refilling; the
-//    loads of the rows a step adds are issued two steps ahead, into one of
-//    two register sets;
+//    loads of the rows a step adds are issued during the step before (so
+//    that the first step's own instructions cover the arrival of those
+//    rows), into one of two register sets;
 //  - wave w computes 32 output channels (half w & 1) x 32 pixels (half
 //    w >> 1) of both output rows with 32x32x16 instructions, pixels as the
 //    row operand and output channels as the column operand;
@@ -638,8 +639,8 @@ conv2d_bf16_rows_kernel(ConvArgs p) {
     const std::integral_constant<int, 1> S1;
     // prologue: the weights first (they come from L2, and the in-order
     // memory counter would otherwise make their wait include the input
-    // rows' HBM latency), then band rows 0 .. 3; rows 4, 5 (set 1) and 6, 7
-    // (set 0) stay in flight
+    // rows' HBM latency), then band rows 0 .. 3; rows 4, 5 (set 0), which
+    // the first step stores at its end, stay in flight
     u32x4_t ws[2][NTAP];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -669,8 +670,7 @@ conv2d_bf16_rows_kernel(ConvArgs p) {
     }
     store_rows(S0, 0);
     store_rows(S1, RO);
-    load_rows(S1, 2 * RO);
-    load_rows(S0, 3 * RO);
+    load_rows(S0, 2 * RO);
     __syncthreads();
 
     // ---- fragment offsets.  B (weights): output channel 32*(wave & 1) +
@@ -775,11 +775,9 @@ conv2d_bf16_rows_kernel(ConvArgs p) {
         __builtin_amdgcn_sched_barrier(0);
     };
 
-    auto step = [&](auto S, int st) __attribute__((always_inline)) {
-        // the next step's new rows into the ring (their slots were last read
-        // two steps ago); the loads of the rows three steps ahead go into
-        // the set this frees, spread over the groups below
-        store_rows(S, RO * st + RO + 2);
+    // step st: its groups load, into set SL, the rows the next step stores;
+    // at its end it stores, from set SS, the rows the step after it adds
+    auto step = [&](auto SL, auto SS, int st) __attribute__((always_inline)) {
         typename MF::acc_t acc[RO];
 #pragma unroll
         for (int o = 0; o < RO; ++o)
@@ -797,12 +795,14 @@ conv2d_bf16_rows_kernel(ConvArgs p) {
             mmas(grp & 1);
             if (grp < NPART) {
                 store_part(grp);
-                load_part(S, RO * st + 3 * RO + 2, grp);
+                load_part(SL, RO * st + 2 * RO + 2, grp);
             }
             interleave(grp < NPART);
         }
-        // every wave has stored the next step's rows and finished the
-        // previous step's reads
+        // the next step's new rows into the ring (loaded during the previous
+        // step; their slots were last read two steps ago), then a barrier:
+        // every wave has stored them and finished the previous step's reads
+        store_rows(SS, RO * st + RO + 2);
         __syncthreads();
         frags(0, 0, st + 1);
         mmas(1);
@@ -833,8 +833,8 @@ conv2d_bf16_rows_kernel(ConvArgs p) {
     };
     frags(0, 0, 0);
     for (int st = 0; st < nsteps; st += 2) {
-        step(S1, st);
-        if (st + 1 < nsteps) step(S0, st + 1);
+        step(S1, S0, st);
+        if (st + 1 < nsteps) step(S0, S1, st + 1);
     }
 #pragma unroll
     for (int k = 0; k < NPART; ++k) store_part(k);
