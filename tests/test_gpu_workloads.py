@@ -62,6 +62,7 @@ def test_matmul_relu_exact_every_instance(x, dtype, M, N, K):
     (2, 8, 17, 19, 70, 3, 3, 1, 1),     # channel-major kernels (C % 32 != 0), ragged edges
     (2, 64, 9, 10, 40, 3, 3, 1, 1),     # tap-major kernels
     (1, 3, 30, 30, 16, 7, 7, 2, 3),     # the 7x7 stride-2 shape, scaled down
+    (1, 3, 30, 28, 16, 7, 7, 2, 3),     # the same with 16-byte patch rows (width a multiple of 4)
     (1, 16, 56, 56, 40, 3, 3, 1, 1),    # halo-tiled kernel
     (2, 64, 9, 8, 40, 3, 3, 1, 1),      # bf16 row-streaming kernel (C = 64, OW % 4 == 0)
 ])
