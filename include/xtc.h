@@ -96,7 +96,11 @@ typedef enum {
  *                one contiguous band of the tile order; 0: hardware order.
  *  k_order       conv2d only (0 for matmul): order of the reduction over
  *                (ic, kh, kw).  0: channel-major, k = (ic*R + kh)*S + kw (the
- *                OIHW weight layout); 1: tap-major, k = (kh*S + kw)*C + ic
+ *                OIHW weight layout; with block_m = 16, for few output
+ *                channels, the workgroup's input patch is staged in LDS
+ *                once when it fits, and its two halves of K are reduced by
+ *                two groups of waves and added in a fixed order); 1:
+ *                tap-major, k = (kh*S + kw)*C + ic
  *                (needs C % 32 == 0, else the channel-major kernel with the
  *                same tiles runs); 2: chunks of channels, and inside a
  *                chunk the R*S taps, with each chunk's input patch staged
@@ -207,8 +211,8 @@ xtc_status xtc_matmul(int64_t M, int64_t N, int64_t K,
  *  stride_h, stride_w, pad_h, pad_w, H, W, H + 2*pad_h and W + 2*pad_w are
  *  at most 2^30 (input coordinates stay in 32-bit arithmetic), else
  *  XTC_ERR_TOO_LARGE.
- *  dtype XTC_F32 or XTC_BF16 (else XTC_ERR_BAD_DTYPE); the bf16 kernels
- *  reduce in OIHW order (k_order 0).
+ *  dtype XTC_F32 or XTC_BF16 (else XTC_ERR_BAD_DTYPE); each reduces in
+ *  the order its schedule's k_order selects (bf16: 0, 2 or 3).
  *  sched NULL selects the default conv schedule.
  * Errors as for xtc_matmul; XTC_ERR_TOO_LARGE also when C*R*S exceeds the
  * kernel's k-offset table capacity (xtc_conv_max_k()).
