@@ -856,13 +856,16 @@ inline bool bf16_rows_eligible(const ConvArgs &a) {
 hipError_t launch_conv_bf16_rows(const ConvArgs &a, hipStream_t s) {
     if (!bf16_rows_eligible(a)) return launch_conv_bf16_halo(a, s);
     // bands sized so that the workgroups (one per CU: the LDS holds one)
-    // cover the 256 CUs about once
+    // cover the 256 CUs about once, rounded up to whole steps: a band's
+    // time is its step count, so a last step with one row does the work of
+    // two (32x64x56x56: 7 bands of 8 rows, 224 workgroups, against 8 bands
+    // of 7: 18.9 -> 18.5 us between events)
     const int octiles = (a.OC + rows_bf16::BM - 1) / rows_bf16::BM;
     const int per_img = octiles * a.Nb;
     int nb = (256 + per_img - 1) / per_img;
     ConvArgs args = a;
-    args.tile_px = (a.OH + nb - 1) / nb;   // output rows per band, at least a step's
-    if (args.tile_px < rows_bf16::RO) args.tile_px = rows_bf16::RO;
+    args.tile_px = (a.OH + nb - 1) / nb;   // output rows per band, whole steps
+    args.tile_px = (args.tile_px + rows_bf16::RO - 1) / rows_bf16::RO * rows_bf16::RO;
     const int nbands = (a.OH + args.tile_px - 1) / args.tile_px;
     args.xcd_remap = 1;
     void *kargs[] = {&args};

@@ -359,7 +359,7 @@ def conv_bf16_rows_launch(N, C, H, W, OC, pad_h, pad_w) -> LdsCost:
     OH, OW = H + 2 * pad_h - 2, W + 2 * pad_w - 2
     per_img = _cdiv(OC, BM) * N
     nb = _cdiv(256, per_img)
-    band = max(_cdiv(OH, nb), RO)
+    band = _cdiv(_cdiv(OH, nb), RO) * RO         # whole steps, as the launcher sizes bands
     nbands = _cdiv(OH, band)
     row_w = LdsCost()           # one input row into the ring (every thread)
     for wave in range(4):

@@ -395,7 +395,7 @@ def conv_grid(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
     if dtype == "bf16" and s["k_order"] == 3:
         if halo_class and C == 64 and W % 2 == 0 and pw <= 2 and OW % 4 == 0 and OW <= 64 and OW + 1 - pw + 2 <= 63:
             per_img = _cdiv(OC, 64) * N
-            band = max(_cdiv(OH, _cdiv(256, per_img)), 2)
+            band = _cdiv(_cdiv(OH, _cdiv(256, per_img)), 2) * 2    # whole 2-row steps
             nb = _cdiv(OH, band)
 
             def seg(tn):

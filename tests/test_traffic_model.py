@@ -152,7 +152,8 @@ def test_conv_halo_rows_are_read_by_both_neighbouring_xcds():
 
 def test_conv_grid_follows_the_launchers():
     # the benchmark layer: balanced halo tiles of 196 (one half) or 392
-    # pixels (two halves), row-streaming bands of 7 rows for bf16
+    # pixels (two halves), row-streaming bands of 8 rows (whole two-row
+    # steps, 7 per image) for bf16
     dims = (32, 64, 56, 56, 64, 3, 3, 1, 1)
     bm, tmm, tn, seg, force = tm.conv_grid("f32", _sched(block_n=208, k_order=2, block_k=8), *dims)
     assert (bm, tmm, tn, force) == (64, 1, 32 * 16, None)
@@ -160,7 +161,8 @@ def test_conv_grid_follows_the_launchers():
     bm, tmm, tn, seg, force = tm.conv_grid("f32", _sched(block_n=416, k_order=2, block_k=8), *dims)
     assert tn == 32 * 8
     bm, tmm, tn, seg, force = tm.conv_grid("bf16", _sched(block_n=64, k_order=3), *dims)
-    assert (tn, force) == (32 * 8, 1) and seg(9) == [(1, 6, 15)]   # band 1: input rows 6 .. 15
+    assert (tn, force) == (32 * 7, 1) and seg(8) == [(1, 7, 16)]   # band 1: input rows 7 .. 16
+    assert seg(6) == [(0, 47, 55)]            # last band: input rows 47 .. 55, row 56 is padding
     # 28x28 rows are too short for the halo tiles: the tap-major 64x256
     # fallback, whose flattened tiles run across images
     small = (8, 128, 28, 28, 256, 3, 3, 1, 1)
