@@ -24,11 +24,24 @@ constexpr int kMaxRaster = 64;
 constexpr int64_t kMaxConvExtent = int64_t(1) << 30;
 constexpr int kLdsBytes = 160 * 1024;                  // LDS per CU on gfx950
 
+// Products and sums of non-negative extents, saturated at INT64_MAX: the
+// entry points take any int64 sizes, and a product that wrapped around
+// would pass the span limits.
+int64_t sat_mul(int64_t a, int64_t b) {
+    int64_t r;
+    return __builtin_mul_overflow(a, b, &r) ? INT64_MAX : r;
+}
+int64_t sat_add(int64_t a, int64_t b) {
+    int64_t r;
+    return __builtin_add_overflow(a, b, &r) ? INT64_MAX : r;
+}
+int64_t cdiv(int64_t a, int64_t b) { return a / b + (a % b != 0); }   // a >= 0, b > 0
+
 // Bytes from the first to one past the last addressed element of a
-// rows x cols row-major operand with row stride ld (0 if empty).
+// rows x cols row-major operand with row stride ld (0 if empty; saturated).
 int64_t span_bytes(int64_t rows, int64_t cols, int64_t ld, int64_t elt) {
     if (rows <= 0 || cols <= 0) return 0;
-    return ((rows - 1) * ld + cols) * elt;
+    return sat_mul(sat_add(sat_mul(rows - 1, ld), cols), elt);
 }
 
 bool same_instance(const xtc_sched &a, const xtc_sched &b) {
@@ -162,7 +175,7 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     if (op != XTC_OP_MATMUL && op != XTC_OP_CONV2D) return XTC_ERR_BAD_SHAPE;
     if (M < 0 || N < 0 || K < 0) return XTC_ERR_BAD_SHAPE;
     const int64_t cus = 256;
-    auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
+    auto tiles = [&](int bm, int bn) { return sat_mul(cdiv(M, bm), cdiv(N, bn)); };
     if (op == XTC_OP_CONV2D && dt == XTC_BF16) {
         // the row-streaming kernel (3x3 stride 1, 64 input channels, rows of
         // at most 64 pixels; 32x64x56x56 -> 64: 15.3 us kernel span against
@@ -402,7 +415,7 @@ xtc_status conv_impl(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int
     if (H + 2 * pad_h < R || W + 2 * pad_w < S) return XTC_ERR_BAD_SHAPE;
     const int64_t OH = (H + 2 * pad_h - R) / stride_h + 1;
     const int64_t OW = (W + 2 * pad_w - S) / stride_w + 1;
-    const int64_t Mg = OC, Ng = N * OH * OW, Kg = C * R * S;
+    const int64_t Mg = OC, Ng = sat_mul(sat_mul(N, OH), OW), Kg = sat_mul(sat_mul(C, R), S);
     xtc_sched s;
     if (sched) {
         const xtc_status st = xtc_sched_check(XTC_OP_CONV2D, dtype, sched);
@@ -416,8 +429,8 @@ xtc_status conv_impl(int64_t N, int64_t C, int64_t H, int64_t W, int64_t OC, int
     const int64_t xelt = dtype == XTC_F32 ? 4 : 2;
     if (!aligned_to(X, xelt) || !aligned_to(Wt, xelt) || !aligned_to(Y, 4)) return XTC_ERR_MISALIGNED;
     const int64_t elt = dtype == XTC_F32 ? 4 : 2;
-    if (N * C * H * W * elt > kMaxSpan || OC * Kg * elt > kMaxSpan ||
-        N * OC * OH * OW * 4 > kMaxSpan)
+    if (sat_mul(sat_mul(sat_mul(sat_mul(N, C), H), W), elt) > kMaxSpan ||
+        sat_mul(sat_mul(OC, Kg), elt) > kMaxSpan || sat_mul(sat_mul(OC, Ng), 4) > kMaxSpan)
         return XTC_ERR_TOO_LARGE;
     if (Kg > kConvMaxK) return XTC_ERR_TOO_LARGE;
     const ConvInstance *inst = find_conv(dtype, s);

@@ -69,6 +69,9 @@ BAD = 0x10  # a dummy non-NULL pointer: dereferencing it would fault
     ((1 << 16, 1 << 15, 1 << 15, BAD, 1 << 15, BAD, 1 << 15, BAD, 1 << 15, 0), 7),  # span >= 2^31
     ((3, 3, 1 << 30, BAD, 1 << 30, BAD, 3, BAD, 3, 1), 7),
     ((1, 1, 0x1FFFFFF5, BAD, 0x1FFFFFF5, BAD, 1, BAD, 1, 0), 7),  # span 0x7FFFFFD4 > 0x7FFFFFD0
+    # (M - 1) * ld = 2^64 would wrap to 0 and leave spans of 16 bytes
+    (((1 << 62) + 1, 4, 4, BAD, 4, BAD, 4, BAD, 4, 0), 7),
+    ((2**63 - 1, 2**63 - 1, 2**63 - 1, BAD, 2**63 - 1, BAD, 2**63 - 1, BAD, 2**63 - 1, 1), 7),
     ((4, 4, 4, BAD + 2, 4, BAD, 4, BAD, 4, 0), 9),       # fp32 A on a 2-byte boundary
     ((4, 4, 4, BAD, 4, BAD + 1, 4, BAD, 4, 1), 9),       # bf16 B on an odd byte
     ((4, 4, 4, BAD, 4, BAD, 4, BAD + 2, 4, 1), 9),       # C (fp32) on a 2-byte boundary
@@ -107,6 +110,10 @@ def test_matmul_empty_is_noop(x):
     ((1, 1, 3, 3, 1, 3, 3, 1, 1 << 31, 0, 0, BAD, BAD, BAD, 0), 7),
     ((1, 1, 3, 3, 1, 3, 3, 1, 1, 0, (1 << 30) + 1, BAD, BAD, BAD, 0), 7),
     ((1, 1, 3, 3, 1, 3, 3, 1, 1, 1 << 29, 0, BAD, BAD, BAD, 0), 7),   # H + 2*pad_h > 2^30
+    # X and Y spans of 2^61 x 16 x 4 bytes would wrap to 0
+    ((1 << 61, 1, 4, 4, 1, 3, 3, 1, 1, 0, 0, BAD, BAD, BAD, 0), 7),
+    ((1, 1 << 62, 4, 4, 1, 3, 3, 1, 1, 0, 0, BAD, BAD, BAD, 0), 7),   # C * R * S wraps
+    ((2**63 - 1, 2**63 - 1, 3, 3, 2**63 - 1, 3, 3, 1, 1, 0, 0, BAD, BAD, BAD, 1), 7),
 ])
 def test_conv_validation(x, args, expected):
     assert x.xtc_conv2d_nchw(*args) == expected
@@ -203,6 +210,12 @@ def test_default_schedules_are_compiled(x):
         assert x.xtc_sched_check(op, dt, s) == 0, (op, dt, M, N, K, s)
     with pytest.raises(x.XtcError):
         x.xtc_default_schedule(1, 2, 64, 64, 64)
+    # extents up to 2^63 - 1 (tile counts saturate instead of wrapping)
+    for op in (0, 1):
+        for dt in (0, 1):
+            for M, N in [(2**63 - 1, 2**63 - 1), (1, 2**63 - 1), (2**63 - 1, 1)]:
+                s = x.xtc_default_schedule(op, dt, M, N, 2**63 - 1)
+                assert x.xtc_sched_check(op, dt, s) == 0
 
 
 def test_no_hip_error_recorded_by_validation(x):
