@@ -33,13 +33,16 @@ def test_sched_check_total_and_sound(x, vals, op, dt):
 
 
 @settings(max_examples=300, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
-@given(M=st.integers(-5, 2 ** 40), N=st.integers(-5, 2 ** 40), K=st.integers(-5, 2 ** 40),
+@given(M=st.integers(-5, 2 ** 63 - 1), N=st.integers(-5, 2 ** 63 - 1), K=st.integers(-5, 2 ** 63 - 1),
+       pads=st.tuples(*[st.one_of(st.just(0), st.integers(0, 2 ** 63 - 1))] * 3),
        dt=st.sampled_from([0, 1]))
-def test_huge_or_negative_shapes_refused_before_launch(x, M, N, K, dt):
-    # leading dimensions equal to the extents; pointers are dummies, so only
-    # the no-op (M or N == 0) or a refusal may come back
+def test_huge_or_negative_shapes_refused_before_launch(x, M, N, K, pads, dt):
+    # leading dimensions at least the extents, up to 2^63 - 1 (products of
+    # such sizes overflow 64 bits); pointers are dummies, so only the no-op
+    # (M or N == 0) or a refusal may come back
     BAD = 0x10
-    lda, ldb, ldc = max(K, 1), max(N, 1), max(N, 1)
+    lim = 2 ** 63 - 1
+    lda, ldb, ldc = (min(max(e, 1) + p, lim) for e, p in zip((K, N, N), pads))
     # Only calls that are clearly invalid are made: negative or zero extents,
     # or an operand span of at least twice the 2^31-byte limit.  Anything
     # near the limit is skipped, so that no call can reach a launch on the
@@ -54,11 +57,15 @@ def test_huge_or_negative_shapes_refused_before_launch(x, M, N, K, dt):
         assert st_ == 2
     elif M == 0 or N == 0:
         assert st_ == 0
+    else:
+        assert st_ == 7   # an operand span past the limit, however large
 
 
 @settings(max_examples=200, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
 @given(op=st.sampled_from([0, 1]), dt=st.sampled_from([0, 1]),
-       M=st.integers(0, 1 << 20), N=st.integers(0, 1 << 24), K=st.integers(0, 1 << 16))
+       M=st.one_of(st.integers(0, 1 << 20), st.integers(0, 2 ** 63 - 1)),
+       N=st.one_of(st.integers(0, 1 << 24), st.integers(0, 2 ** 63 - 1)),
+       K=st.one_of(st.integers(0, 1 << 16), st.integers(0, 2 ** 63 - 1)))
 def test_default_schedule_is_always_compiled(x, op, dt, M, N, K):
     s = x.xtc_default_schedule(op, dt, M, N, K)
     assert x.xtc_sched_check(op, dt, s) == 0
