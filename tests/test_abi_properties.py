@@ -4,7 +4,7 @@ one of the documented status codes, a schedule the check accepts is one of
 the compiled instances, and invalid calls are refused before any device
 work (dummy pointers that a kernel would fault on)."""
 import pytest
-from hypothesis import HealthCheck, given, settings
+from hypothesis import HealthCheck, example, given, settings
 from hypothesis import strategies as st
 
 I32 = st.one_of(st.integers(-2 ** 31, 2 ** 31 - 1), st.sampled_from([0, 1, 2, 4, 8, 16, 32, 64, 128, 256, 512, -1]))
@@ -36,6 +36,7 @@ def test_sched_check_total_and_sound(x, vals, op, dt):
 @given(M=st.integers(-5, 2 ** 63 - 1), N=st.integers(-5, 2 ** 63 - 1), K=st.integers(-5, 2 ** 63 - 1),
        pads=st.tuples(*[st.one_of(st.just(0), st.integers(0, 2 ** 63 - 1))] * 3),
        dt=st.sampled_from([0, 1]))
+@example(M=(1 << 62) + 1, N=4, K=4, pads=(0, 0, 0), dt=0)   # (M - 1) * ld wraps to 0
 def test_huge_or_negative_shapes_refused_before_launch(x, M, N, K, pads, dt):
     # leading dimensions at least the extents, up to 2^63 - 1 (products of
     # such sizes overflow 64 bits); pointers are dummies, so only the no-op
@@ -69,3 +70,38 @@ def test_huge_or_negative_shapes_refused_before_launch(x, M, N, K, pads, dt):
 def test_default_schedule_is_always_compiled(x, op, dt, M, N, K):
     s = x.xtc_default_schedule(op, dt, M, N, K)
     assert x.xtc_sched_check(op, dt, s) == 0
+
+
+SIZE = st.one_of(st.integers(-2, 9), st.integers(-2, 2 ** 63 - 1))
+
+
+@settings(max_examples=400, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
+@given(dims=st.tuples(*[SIZE] * 11), dt=st.sampled_from([0, 1]))
+@example(dims=(1 << 61, 1, 4, 4, 1, 3, 3, 1, 1, 0, 0), dt=0)   # X and Y spans wrap to 0
+@example(dims=(1, 1 << 62, 4, 4, 1, 3, 3, 1, 1, 0, 0), dt=1)   # C * R * S wraps
+def test_conv_invalid_or_huge_refused_before_launch(x, dims, dt):
+    # The conv checks in their order: shape signs, strides / pads / padded
+    # extents above 2^30, a kernel larger than the padded input, the no-op
+    # (N or OC == 0), then the operand spans (2^31-byte limit).  Pointers
+    # are dummies, so only calls that one of these decides are made: a
+    # valid call of modest size is skipped (it would launch).
+    N, C, H, W, OC, R, S, sh, sw, ph, pw = dims
+    BAD = 0x10
+    lim = 2 ** 30
+    if (N < 0 or OC < 0 or C < 1 or H < 1 or W < 1 or R < 1 or S < 1 or sh < 1 or sw < 1
+            or ph < 0 or pw < 0):
+        expected = 2
+    elif max(sh, sw, ph, pw, H, W) > lim or H + 2 * ph > lim or W + 2 * pw > lim:
+        expected = 7
+    elif H + 2 * ph < R or W + 2 * pw < S:
+        expected = 2
+    elif N == 0 or OC == 0:
+        expected = 0
+    else:
+        OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+        elt = 4 if dt == 0 else 2
+        spans = [N * C * H * W * elt, OC * C * R * S * elt, N * OC * OH * OW * 4]
+        if max(spans) * 2 < 2 ** 32:
+            return
+        expected = 7
+    assert x.xtc_conv2d_nchw(N, C, H, W, OC, R, S, sh, sw, ph, pw, BAD, BAD, BAD, dt) == expected
