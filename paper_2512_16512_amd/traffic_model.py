@@ -36,6 +36,12 @@ Convolutions (``conv_grid``, ``predict_conv``) follow the same L2 rule with
 the launchers' own tile grids; a workgroup's footprint is the weights of its
 output-channel tile and the input rows its output rows reach.
 
+The level above.  ``predict_l2_reads`` models what the workgroups of a
+matmul read from L2 (TCC_READ_SECTORS): each tile's operand panels, one
+K-stage at a time, in whole cache lines, with lines that consecutive stages
+share kept only when the resident workgroups' stage blocks fit in half the
+CU's L1 (``correlate-l2``).
+
 Usage (the measurement step runs under rocprofv3; see ``run``)::
 
     rocprofv3 --pmc FETCH_SIZE -f csv -d OUT -o run -- \\
@@ -46,6 +52,9 @@ Usage (the measurement step runs under rocprofv3; see ``run``)::
         python3 -m paper_2512_16512_amd.traffic_model run-conv f32 32 64 56 56 64 3 3 1 1 --order ORDER.json
     python -m paper_2512_16512_amd.traffic_model correlate-conv ORDER.json OUT/run_counter_collection.csv \\
         --fetch-scale 2.0
+    rocprofv3 --pmc TCC_READ_SECTORS_sum -f csv -d OUT -o run -- \\
+        python3 -m paper_2512_16512_amd.traffic_model run f32 1000 1000 1000 --order ORDER.json --rasters 0,1
+    python -m paper_2512_16512_amd.traffic_model correlate-l2 ORDER.json OUT/run_counter_collection.csv
 """
 from __future__ import annotations
 
@@ -344,6 +353,111 @@ def correlate(order_path: str, fetch_csv: str, fetch_scale: float):
     return table, pearson(x, y), spearman(x, y)
 
 
+# ------------------------------------------------ L2 reads (the CU side)
+
+SECTOR = 32            # bytes per L2 read sector (the unit of TCC_READ_SECTORS)
+LINE = 128             # bytes per cache line
+L1_KEEP = 16 << 10     # half the CU's 32 KiB vector L1 (see ``predict_l2_reads``)
+
+
+def _block_lines(starts, length: int, line: int = LINE) -> int:
+    """Distinct lines of ``line`` bytes touched by byte runs of ``length``
+    at the increasing, non-overlapping offsets ``starts`` (a run can share
+    a line only with its neighbours)."""
+    import numpy as np
+    st = np.asarray(starts, dtype=np.int64)
+    if length <= 0 or st.size == 0:
+        return 0
+    first, last = st // line, (st + length - 1) // line
+    return int((last - first + 1).sum() - (last[:-1] >= first[1:]).sum())
+
+
+def gemm_tile(dtype: str, s: dict, M: int, N: int, K: int):
+    """(block_m, block_n, block_k) of the kernel a matmul instance runs on
+    this shape (contiguous operands, 16-byte aligned bases): the fp32
+    256x256 direct-to-LDS instances fall back to the register-staged
+    128x128x32 kernel when K or N is not a whole number of 16-byte chunks;
+    every other instance keeps its tile."""
+    elt = 4 if dtype == "f32" else 2
+    whole = (K * elt) % 16 == 0 and (N * elt) % 16 == 0
+    if dtype == "f32" and s["lds_pad"] == -1 and s["block_m"] == 256 and s["block_n"] == 256 and not whole:
+        return 128, 128, 32
+    return s["block_m"], s["block_n"], s["block_k"]
+
+
+def predict_l2_reads(M: int, N: int, K: int, elt: int, block_m: int, block_n: int, block_k: int,
+                     occupancy: int = 1, lda: int = None, ldb: int = None, l1_keep: int = L1_KEEP,
+                     line: int = LINE) -> int:
+    """Bytes the workgroups of one matmul launch read from L2, for the
+    kernels that stage their operands through LDS (the level above the one
+    ``predict`` models).
+
+    Every output tile reads the in-range part of its A row-panel and B
+    column-panel one K-stage at a time: per stage an A block (rows x
+    block_k) and a B block (block_k rows x columns), each fetched as the
+    distinct cache lines its rows touch.  A line that two consecutive
+    stages share (a stage's A rows are half a line for fp32 with block_k 16
+    or bf16 with block_k 32; rows not aligned to a line) is fetched again
+    unless it survives in the CU's L1 from one stage to the next, which the
+    model takes to happen when the stage blocks of the workgroups resident
+    on a CU (min(occupancy, tiles per CU)) fit in half the L1; the panel's
+    distinct lines are then fetched once.  Reuse between workgroups is not
+    modelled.  Out-of-range elements (ragged edges) are not read."""
+    import numpy as np
+    if M <= 0 or N <= 0 or K <= 0:
+        return 0
+    lda = K if lda is None else lda
+    ldb = N if ldb is None else ldb
+    tiles_m, tiles_n = _cdiv(M, block_m), _cdiv(N, block_n)
+    resident = min(max(1, occupancy), _cdiv(tiles_m * tiles_n, XCDS * CUS_PER_XCD))
+    keep = resident * (min(block_m, M) + min(block_n, N)) * block_k * elt <= l1_keep
+    stages = [(k0, min(block_k, K - k0)) for k0 in range(0, K, block_k)]
+    a = b = 0
+    for t in range(tiles_m):
+        rows = np.arange(t * block_m, min(M, (t + 1) * block_m), dtype=np.int64) * lda * elt
+        if keep:
+            a += _block_lines(rows, K * elt, line)
+        else:
+            a += sum(_block_lines(rows + k0 * elt, kk * elt, line) for k0, kk in stages)
+    for t in range(tiles_n):
+        n0, cols = t * block_n, min(block_n, N - t * block_n)
+        if keep:
+            b += _block_lines(np.arange(K, dtype=np.int64) * ldb * elt + n0 * elt, cols * elt, line)
+        else:
+            b += sum(_block_lines(np.arange(k0, k0 + kk, dtype=np.int64) * ldb * elt + n0 * elt,
+                                  cols * elt, line) for k0, kk in stages)
+    return (a * tiles_n + b * tiles_m) * line
+
+
+def correlate_l2(order_path: str, csv_path: str):
+    """Predicted (``predict_l2_reads``) vs measured (TCC_READ_SECTORS x 32)
+    L2 read bytes per matmul schedule of a ``run`` order file.  The
+    register-fed reduction-split kernels (no LDS stages), which read their
+    MFMA fragments straight from memory, are not modelled (predicted None);
+    the statistics are over the modelled schedules."""
+    o = json.load(open(order_path))
+    vals = _counter_rows(csv_path, "TCC_READ_SECTORS_sum")
+    reps = o["reps"]
+    if len(vals) != reps * len(o["schedules"]):
+        raise ValueError("%d counter rows for %d schedules x %d launches"
+                         % (len(vals), len(o["schedules"]), reps))
+    M, N, K = o["M"], o["N"], o["K"]
+    elt = 4 if o["dtype"] == "f32" else 2
+    table = []
+    for i, e in enumerate(o["schedules"]):
+        s = e["sched"]
+        meas = sum(vals[i * reps:(i + 1) * reps]) / reps * SECTOR
+        pred = None
+        if s["lds_stages"] > 0:
+            bm, bn, bk = gemm_tile(o["dtype"], s, M, N, K)
+            pred = predict_l2_reads(M, N, K, elt, bm, bn, bk, e["occupancy"])
+        table.append({"sched": s, "occupancy": e["occupancy"], "predicted": pred, "measured": meas})
+    mod = [t for t in table if t["predicted"] is not None]
+    x = [t["predicted"] for t in mod]
+    y = [t["measured"] for t in mod]
+    return table, pearson(x, y), spearman(x, y)
+
+
 # ------------------------------------------------------------------- conv
 
 def _cdiv(a: int, b: int) -> int:
@@ -545,6 +659,7 @@ def main(argv=None):
     r.add_argument("K", type=int)
     r.add_argument("--order", required=True)
     r.add_argument("--reps", type=int, default=2)
+    r.add_argument("--rasters", default="0,1,4,8,16", help="tile orders, comma-separated")
     w = sub.add_parser("orders")
     w.add_argument("dtype", choices=["f32", "bf16"])
     w.add_argument("M", type=int)
@@ -566,6 +681,10 @@ def main(argv=None):
     rc.add_argument("dims", type=int, nargs=9, help="N C H W OC R S stride pad")
     rc.add_argument("--order", required=True)
     rc.add_argument("--reps", type=int, default=2)
+    cl = sub.add_parser("correlate-l2")
+    cl.add_argument("order")
+    cl.add_argument("csv")
+    cl.add_argument("--json", default=None)
     cc = sub.add_parser("correlate-conv")
     cc.add_argument("order")
     cc.add_argument("fetch_csv")
@@ -573,10 +692,19 @@ def main(argv=None):
     cc.add_argument("--json", default=None)
     a = ap.parse_args(argv)
     if a.cmd == "run":
-        run(a.dtype, a.M, a.N, a.K, a.order, a.reps)
+        run(a.dtype, a.M, a.N, a.K, a.order, a.reps, tuple(int(v) for v in a.rasters.split(",")))
         return 0
     if a.cmd == "run-conv":
         run_conv(a.dtype, tuple(a.dims), a.order, a.reps)
+        return 0
+    if a.cmd == "correlate-l2":
+        table, r_, rho = correlate_l2(a.order, a.csv)
+        ratio = sorted(t["predicted"] / t["measured"] for t in table if t["predicted"] is not None)
+        print("schedules %d (modelled %d)  Pearson r = %.4f  Spearman rho = %.4f  "
+              "predicted/measured %.3f .. %.3f" % (len(table), len(ratio), r_, rho, ratio[0], ratio[-1]))
+        if a.json:
+            with open(a.json, "w") as f:
+                json.dump({"pearson": r_, "spearman": rho, "rows": table}, f, indent=1)
         return 0
     if a.cmd == "correlate-conv":
         table, r_, rho = correlate_conv(a.order, a.fetch_csv, a.fetch_scale)

@@ -191,3 +191,80 @@ MEASURED_CONV = [
 def test_conv_model_against_counters(dtype, dims, fields, raster, remap, occ, measured):
     r, _ = tm.predict_conv(dtype, _sched(raster=raster, xcd_remap=remap, **fields), dims, occ)
     assert 0.9 <= r / measured <= 1.0
+
+
+# ------------------------------------------------ L2 reads (the CU side)
+
+
+def _l2_brute(M, N, K, elt, bm, bn, bk, keep):
+    """Lines (A and B kept apart) of every in-range element a tile reads,
+    per stage, or per tile when lines survive from stage to stage: sets of
+    line numbers, one element at a time."""
+    total = 0
+    for tm_ in range(-(-M // bm)):
+        for tn in range(-(-N // bn)):
+            ms = range(tm_ * bm, min(M, (tm_ + 1) * bm))
+            ns = range(tn * bn, min(N, (tn + 1) * bn))
+            groups = [range(0, K)] if keep else [range(k0, min(K, k0 + bk)) for k0 in range(0, K, bk)]
+            for ks in groups:
+                a = {(m * K + k) * elt // 128 for m in ms for k in ks}
+                b = {(k * N + n) * elt // 128 for k in ks for n in ns}
+                total += len(a) + len(b)
+    return total * 128
+
+
+@pytest.mark.parametrize("M,N,K,elt,bm,bn,bk", [
+    (5, 24, 40, 4, 4, 16, 8),       # 160-byte rows: runs straddle lines
+    (7, 40, 33, 2, 4, 16, 16),      # ragged K and N, bf16
+    (16, 16, 64, 4, 8, 8, 16),      # 64-byte B rows: neighbouring rows share a line
+    (3, 100, 24, 4, 2, 32, 4),      # 16-byte A runs, ragged column tile
+])
+def test_l2_reads_match_line_sets(M, N, K, elt, bm, bn, bk):
+    for keep in (False, True):
+        pred = tm.predict_l2_reads(M, N, K, elt, bm, bn, bk, l1_keep=1 << 40 if keep else 0)
+        assert pred == _l2_brute(M, N, K, elt, bm, bn, bk, keep)
+
+
+def test_l2_reads_closed_forms():
+    M = N = K = 4096
+    # whole-line stages (128-byte A runs): each tile reads its panels once
+    assert tm.predict_l2_reads(M, N, K, 4, 256, 256, 32) == (M * K * 16 + K * N * 16) * 4
+    # half-line A runs (block_k 16) and a stage too large for the L1: every A line twice
+    assert tm.predict_l2_reads(M, N, K, 4, 256, 128, 16) == (2 * M * K * 32 + K * N * 16) * 4
+    # the same tile alone on its CU with a stage that fits: A lines once
+    assert tm.predict_l2_reads(128, 128, K, 4, 128, 128, 16) == (128 * K + K * 128) * 4
+    # 1024 tiles: with two resident workgroups per CU the footprint passes the limit
+    two = tm.predict_l2_reads(M, N, K, 4, 128, 128, 16, occupancy=2)
+    assert two == tm.predict_l2_reads(M, N, K, 4, 128, 128, 16, l1_keep=0) == (2 * M * K * 32 + K * N * 32) * 4
+    assert tm.predict_l2_reads(M, N, K, 4, 128, 128, 16, occupancy=1) == (M * K * 32 + K * N * 32) * 4
+    # a launch of 16 tiles leaves one workgroup per CU whatever the occupancy
+    assert tm.predict_l2_reads(512, 512, K, 4, 128, 128, 16, occupancy=2) == (512 * K * 4 + K * 512 * 4) * 4
+    assert tm.predict_l2_reads(0, N, K, 4, 64, 64, 32) == 0
+
+
+def test_l2_tile_follows_the_fallback():
+    s = _sched(block_m=256, block_n=256, block_k=32, lds_pad=-1)
+    assert tm.gemm_tile("f32", s, 256, 258, 512) == (128, 128, 32)    # N = 258: rows not whole chunks
+    assert tm.gemm_tile("f32", s, 4096, 4096, 4096) == (256, 256, 32)
+    assert tm.gemm_tile("bf16", s, 1000, 1000, 1000) == (256, 256, 32)
+
+
+# TCC_READ_SECTORS_sum x 32 bytes per launch (mean of two), one counter
+# pass per shape (a plain 256 MiB copy reads 1.0008 x its bytes):
+# (dtype, M, N, K, block_m, block_n, block_k, lds_pad, occupancy) -> bytes
+MEASURED_L2 = [
+    ("f32", 4096, 4096, 4096, 256, 256, 32, -1, 1, 2150091776),   # whole-line stages
+    ("f32", 4096, 4096, 4096, 256, 128, 16, -1, 1, 5361601024),   # A lines twice
+    ("f32", 1000, 1000, 1000, 64, 64, 32, -1, 5, 157319104),      # 4000-byte rows, lines kept
+    ("f32", 256, 258, 512, 256, 256, 32, -1, 1, 3096192),         # the 128x128 fallback
+    ("f32", 32768, 16, 4096, 256, 256, 32, -1, 1, 571819328),     # one 16-column panel
+    ("bf16", 2048, 2048, 2048, 256, 256, 32, -1, 1, 201325120),   # bf16 half-line A runs
+]
+
+
+@pytest.mark.parametrize("dtype,M,N,K,bm,bn,bk,pad,occ,measured", MEASURED_L2)
+def test_l2_model_against_counters(dtype, M, N, K, bm, bn, bk, pad, occ, measured):
+    s = _sched(block_m=bm, block_n=bn, block_k=bk, lds_pad=pad)
+    tile = tm.gemm_tile(dtype, s, M, N, K)
+    pred = tm.predict_l2_reads(M, N, K, 4 if dtype == "f32" else 2, *tile, occupancy=occ)
+    assert 0.95 <= pred / measured <= 1.02
