@@ -702,26 +702,142 @@ def conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw, vec=None)
     return per_image.scaled(_cdiv(OC, 16) * N)
 
 
+# ------------------------------------------------ fp32 conv: gather kernels
+
+def _ktab_build(K: int, NW: int, base: int) -> LdsCost:
+    """Building the k-offset table at kernel start: thread t writes entries
+    t, t + NT, ... (8 bytes each), one ds_write_b64 per wave and pass in
+    which the wave has an entry."""
+    NT = 64 * NW
+    cost = LdsCost()
+    n = sum(1 for i in range(_cdiv(K, NT)) for w in range(NW) if w * 64 + i * NT < K)
+    cost.add("ds_write_b64", [base + 8 * lane for lane in range(64)], times=n)
+    return cost
+
+
+def conv_f32_gather_dma_launch(BM, BN, WM, WN, STAGES, N, C, H, W, OC, R, S, sh, sw, ph, pw,
+                               tap: bool) -> LdsCost:
+    """The fp32 direct-to-LDS gather conv kernels (block_k 32, 32x32x2
+    instructions): the tap-major kernel (``tap``) and the k-table kernel.
+    Both read fragments as the direct-to-LDS GEMM does (weight chunks
+    swizzled by (m ^ m >> 3) & 7, pixel columns XOR 32 on odd groups of four
+    k rows), K-stages x block_k / 8 fragment sets per workgroup.  The
+    k-table kernel also builds its table and reads one entry (the same for
+    every lane of a wave) per k row a wave gathers, in every stage it
+    prepares: the STAGES of the prologue and one per K-stage."""
+    BK, MI = 32, 32
+    OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    K, NW = C * R * S, (BM // WM) * (BN // WN)
+    KT = _cdiv(K, BK)
+    tile = gemm_f32_dma_stage(BM, BN, BK, WM, WN, MI,
+                              swz_a=lambda ca, row: (row ^ (row >> 3)) & 7).scaled(KT)
+    if not tap:
+        base = STAGES * (BM + BN) * BK * 4
+        tile += _ktab_build(K, NW, base)
+        tile.add("ds_read_b64", [base] * 64, times=(STAGES + KT) * BK)
+    return tile.scaled(_cdiv(OC, BM) * _cdiv(N * OH * OW, BN))
+
+
+def conv_f32_reg_launch(BM, BN, BK, WM, WN, MI, PAD, N, C, H, W, OC, R, S, sh, sw, ph, pw,
+                        vec: bool) -> LdsCost:
+    """The fp32 register-staged gather conv kernel: per K-stage the weight
+    tile's 16-byte (``vec``) or 4-byte stores, one 4-byte store per gathered
+    element (thread t owns pixel column t % BN), and the register-staged
+    GEMM's fragment reads; at kernel start the k-offset table.  A wave reads
+    the table entry of each k row it gathers (every lane the same entry, as
+    two 4-byte reads) when one of its lanes has a pixel and k < K."""
+    OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    K, Ng = C * R * S, N * OH * OW
+    NW = (BM // WM) * (BN // WN)
+    NT = 64 * NW
+    KT = _cdiv(K, BK)
+    AS, BS = BK + PAD, BN + (8 if MI == 32 else 4)
+    WA = 4 if vec else 1
+    _, stage = gemm_f32_reg_stage(BM, BN, BK, WM, WN, MI, PAD)
+    for w in range(NW):
+        for i in range(BM * BK // (WA * NT)):
+            addrs = []
+            for lane in range(64):
+                idx = w * 64 + lane + i * NT
+                r, c = idx // (BK // WA), (idx % (BK // WA)) * WA
+                addrs.append((r * AS + c) * 4)
+            stage.add("ds_write_b128" if vec else "ds_write_b32", addrs)
+    brpp = NT // BN                       # gathered k rows per pass
+    for w in range(NW):
+        for i in range(BK // brpp):
+            stage.add("ds_write_b32", [(((w * 64 + lane) // BN + i * brpp) * BS + (w * 64 + lane) % BN) * 4
+                                       for lane in range(64)])
+    tiles_m, tiles_n = _cdiv(OC, BM), _cdiv(Ng, BN)
+    total = stage.scaled(KT * tiles_m * tiles_n)
+    base = 2 * (BM * AS + BK * BS) * 4
+    total += _ktab_build(K, NW, base).scaled(tiles_m * tiles_n)
+    reads = 0
+    for tn in range(tiles_n):
+        for w in range(NW):
+            if tn * BN + (w * 64) % BN >= Ng:
+                continue                  # no lane of the wave has a pixel
+            brow0 = (w * 64) // BN
+            reads += sum(1 for k0 in range(0, KT * BK, BK) for i in range(BK // brpp)
+                         if k0 + brow0 + i * brpp < K)
+    total.add("ds_read_b32", [base] * 64, times=2 * reads * tiles_m)
+    return total
+
+
+# the tap-major instances' stages and their k-table fallback's stages
+_TAP_FALLBACK = {(64, 256): 2, (64, 128): 3, (64, 64): 4, (128, 128): 3}
+
+
+def _conv_f32_gather(s: dict, k_order: int, stages: int, dims) -> LdsCost:
+    """The launchers' chain below the halo kernels: tap-major when C % 32 ==
+    0, else the k-table direct-to-LDS kernel with the fallback stages, else
+    (C*R*S not a multiple of 4) the register-staged kernel with 4-float
+    padded rows."""
+    N, C, H, W, OC, R, S, sh, sw, ph, pw = dims
+    BM, BN, WM, WN = s["block_m"], s["block_n"], s["wave_m"], s["wave_n"]
+    K = C * R * S
+    if k_order == 1:
+        if C % 32 == 0:
+            return conv_f32_gather_dma_launch(BM, BN, WM, WN, stages, *dims, tap=True)
+        stages = _TAP_FALLBACK[(BM, BN)]
+    if K % 4 == 0:
+        return conv_f32_gather_dma_launch(BM, BN, WM, WN, stages, *dims, tap=False)
+    return conv_f32_reg_launch(BM, BN, 32, WM, WN, 32, 4, *dims, vec=False)
+
+
 def conv_launch(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
     """LDS cost of one conv launch of instance ``s``, or None when the kernel
-    it runs for this shape is not modelled (the gather, channel-major
-    direct-to-LDS, tap-major and 64x256 halo kernels)."""
+    it runs for this shape is not modelled (the 64x256 halo kernel and the
+    bf16 gather kernel)."""
     sh, sw = (stride, stride) if isinstance(stride, int) else stride
     ph, pw = (pad, pad) if isinstance(pad, int) else pad
     OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
     halo_class = R == 3 and S == 3 and sh == 1 and sw == 1
+    dims = (N, C, H, W, OC, R, S, sh, sw, ph, pw)
+    if dtype == "f32" and s["block_m"] == 16 and s["lds_stages"] == 0:
+        return conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw)
     if dtype == "f32" and s["k_order"] == 2 and s["block_n"] in (208, 416):
         nh = 1 if s["block_n"] == 208 else 2
-        if not (halo_class and C % 8 == 0 and pw <= 4 and OW - pw + 5 <= 63):
-            return None
-        # the launcher's pixel tile: the fewest tiles per image of at most 208*nh
-        ohw = OH * OW
-        t = _cdiv(ohw, 208 * nh)
-        pt = _cdiv(ohw, t)
-        span = (pt - 1 + OW - 1) // OW + 1
-        if span + 2 > (8 if nh == 1 else 10):
-            return None
-        return conv_f32_halo16_launch(N, C, H, W, OC, ph, pw, nh=nh, a_swizzle=True, tile_px=pt)
+        if halo_class and C % 8 == 0 and pw <= 4 and OW - pw + 5 <= 63:
+            # the launcher's pixel tile: the fewest tiles per image of at most 208*nh
+            ohw = OH * OW
+            t = _cdiv(ohw, 208 * nh)
+            pt = _cdiv(ohw, t)
+            span = (pt - 1 + OW - 1) // OW + 1
+            if span + 2 <= (8 if nh == 1 else 10):
+                return conv_f32_halo16_launch(N, C, H, W, OC, ph, pw, nh=nh, a_swizzle=True, tile_px=pt)
+        s = dict(s, block_n=256, wave_m=64, wave_n=64)   # falls back to the 64x256 halo kernel
+    if dtype == "f32" and s["k_order"] == 2:
+        span = (256 - 1 + OW - 1) // OW + 1
+        if halo_class and C % 16 == 0 and pw <= 4 and OW - pw + 5 <= 63 and span + 2 <= 8:
+            return None                   # the 64x256 halo kernel: not modelled
+        return _conv_f32_gather(dict(s, block_m=64, block_n=256, wave_m=64, wave_n=64), 1, 2, dims)
+    if dtype == "f32" and s["k_order"] == 1:
+        return _conv_f32_gather(s, 1, s["lds_stages"], dims)
+    if dtype == "f32" and s["k_order"] == 0 and s["lds_pad"] < 0:
+        return _conv_f32_gather(s, 0, s["lds_stages"], dims)
+    if dtype == "f32" and s["k_order"] == 0:
+        return conv_f32_reg_launch(s["block_m"], s["block_n"], s["block_k"], s["wave_m"], s["wave_n"],
+                                   s["mfma_m"], s["lds_pad"], *dims, vec=(C * R * S) % 4 == 0)
     if dtype == "bf16" and s["k_order"] == 3:
         if halo_class and C == 64 and W % 2 == 0 and pw <= 2 and OW % 4 == 0 and OW <= 64 and OW + 1 - pw + 2 <= 63:
             return conv_bf16_rows_launch(N, C, H, W, OC, ph, pw)
@@ -732,8 +848,6 @@ def conv_launch(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
             return conv_bf16_halo_launch(N, C, H, W, OC, ph, pw, a_swizzle=True, rotate=True,
                                          store_order=True)
         return None
-    if dtype == "f32" and s["block_m"] == 16 and s["lds_stages"] == 0:
-        return conv_f32_smallm_patch_launch(N, C, H, W, OC, R, S, sh, sw, ph, pw)
     return None
 
 

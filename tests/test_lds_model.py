@@ -146,9 +146,63 @@ def test_small_channel_conv_matches_counters():
 
 
 def test_unmodelled_kernels_return_none():
-    # the tap-major conv kernel is not modelled
-    s = dict(k_order=1, block_n=256, block_m=64, lds_stages=2)
+    # the fp32 64x256 halo kernel, where its class applies, is not modelled
+    s = dict(k_order=2, block_m=64, block_n=256, block_k=8, wave_m=64, wave_n=64, mfma_m=32,
+             lds_stages=2, lds_pad=-1)
     assert L.conv_launch("f32", s, 32, 64, 56, 56, 64, 3, 3, 1, 1) is None
+    # outside it the launcher falls back to the tap-major kernel, which is
+    assert L.conv_launch("f32", s, 8, 128, 28, 28, 256, 3, 3, 1, 1).active == 1382400
+
+
+def _conv_inst(bm, bn, wm, wn, mi, stages, pad, k_order, bk=32):
+    return dict(block_m=bm, block_n=bn, block_k=bk, wave_m=wm, wave_n=wn, mfma_m=mi,
+                lds_stages=stages, lds_pad=pad, k_order=k_order)
+
+
+# SQ_LDS_IDX_ACTIVE and SQ_LDS_BANK_CONFLICT per launch, measured (mean of
+# two launches, equal): the fp32 gather conv kernels as the launchers chain
+# them (tap-major for C % 32 == 0, else the k-table direct-to-LDS kernel with
+# the fallback's stages, else the register-staged kernel)
+MEASURED_GATHER = [
+    ((32, 64, 56, 56, 64, 3, 3, 1, 1), _conv_inst(64, 128, 32, 64, 32, 2, -1, 1), 4515840, 0),
+    ((32, 64, 56, 56, 64, 3, 3, 1, 1), _conv_inst(128, 128, 64, 64, 32, 3, -1, 0), 6500928, 0),
+    ((32, 64, 56, 56, 64, 3, 3, 1, 1), _conv_inst(64, 128, 32, 64, 16, 2, 4, 0), 11769408, 903168),
+    ((32, 64, 56, 56, 64, 3, 3, 1, 1), _conv_inst(128, 128, 64, 64, 32, 2, 4, 0), 12672576, 0),
+    ((8, 128, 28, 28, 256, 3, 3, 1, 1), _conv_inst(128, 128, 64, 64, 32, 2, -1, 1), 1354752, 0),
+    ((4, 16, 56, 56, 16, 3, 3, 1, 1), _conv_inst(64, 256, 64, 64, 32, 2, -1, 1), 116620, 0),
+    ((4, 16, 56, 56, 16, 3, 3, 1, 1), _conv_inst(64, 128, 32, 64, 32, 2, 4, 0), 364952, 0),
+    ((2, 24, 30, 30, 40, 5, 5, 2, 2), _conv_inst(64, 128, 32, 64, 32, 3, -1, 0), 30112, 0),
+    ((2, 24, 30, 30, 40, 5, 5, 2, 2), _conv_inst(128, 128, 64, 64, 32, 2, -1, 1), 34976, 0),
+]
+
+
+@pytest.mark.parametrize("dims,s,active,conflict", MEASURED_GATHER)
+def test_gather_conv_kernels_match_counters(dims, s, active, conflict):
+    c = L.conv_launch("f32", s, *dims)
+    assert c.active == active and c.conflict == conflict
+
+
+def test_gather_conv_fallbacks_match_counters():
+    # C*R*S = 147 and 45 are not multiples of 4: every gather instance runs
+    # the register-staged kernel (measured 367010 and 11074 for 64x128 tiles;
+    # the model is within 0.3%)
+    for dims, meas in (((1, 3, 224, 224, 16, 7, 7, 2, 3), 367010), ((3, 5, 17, 19, 33, 3, 3, 1, 1), 11074)):
+        for s in (_conv_inst(64, 128, 32, 64, 32, 2, -1, 1), _conv_inst(64, 128, 32, 64, 32, 3, -1, 0),
+                  _conv_inst(64, 128, 32, 64, 32, 2, 4, 0)):
+            assert L.conv_launch("f32", s, *dims).active == pytest.approx(meas, rel=3e-3)
+    # the 64x64 k-table tile: the compiler skips one table read per stage
+    # past the end of K, which the model counts (measured 7545216)
+    c = L.conv_launch("f32", _conv_inst(64, 64, 32, 32, 32, 3, -1, 0), 32, 64, 56, 56, 64, 3, 3, 1, 1)
+    assert 1.0 < c.active / 7545216 < 1.01
+
+
+def test_tap_major_is_the_fragment_reads_only():
+    # no table: K-stages x four fragment sets of the direct-to-LDS GEMM's
+    # reads (with the conv's weight swizzle) per workgroup
+    s = _conv_inst(64, 128, 32, 64, 32, 2, -1, 1)
+    c = L.conv_launch("f32", s, 32, 64, 56, 56, 64, 3, 3, 1, 1)
+    stage = L.gemm_f32_dma_stage(64, 128, 32, 32, 64, 32, swz_a=lambda ca, row: (row ^ (row >> 3)) & 7)
+    assert c.active == stage.active * (576 // 32) * (32 * 56 * 56 // 128)
 
 
 def test_staged_k_split_matches_counters():
