@@ -50,20 +50,21 @@ PHASES = {
     "ds_write_b128": [list(range(8 * i, 8 * i + 8)) for i in range(8)],
     "ds_write_b64": [list(range(16 * i, 16 * i + 16)) for i in range(4)],
     "ds_write_b32": [list(range(32)), list(range(32, 64))],
+    "ds_write_b16": [list(range(32)), list(range(32, 64))],
 }
 WIDTH = {"ds_read_b128": 16, "ds_read_b64": 8, "ds_read_b64_tr_b16": 8, "ds_read_b32": 4,
-         "ds_write_b128": 16, "ds_write_b64": 8, "ds_write_b32": 4}
+         "ds_write_b128": 16, "ds_write_b64": 8, "ds_write_b32": 4, "ds_write_b16": 2}
 # Banks a phase of the instruction sees: two lanes of one phase conflict when
 # their dword addresses differ by a multiple of this (measured by scanning
 # the address distance of two lanes of one phase).
 PERIOD = {"ds_read_b128": 64, "ds_read_b64": 64, "ds_read_b64_tr_b16": 64, "ds_read_b32": 32,
-          "ds_write_b128": 32, "ds_write_b64": 32, "ds_write_b32": 32}
+          "ds_write_b128": 32, "ds_write_b64": 32, "ds_write_b32": 32, "ds_write_b16": 32}
 
 
 def cycles(op: str, addrs) -> int:
     """LDS cycles of one wave instruction: ``addrs`` holds each lane's byte
     address (None for an inactive lane)."""
-    words = WIDTH[op] // 4
+    words = max(1, WIDTH[op] // 4)       # a 2-byte access uses the bank of its dword
     nbanks = PERIOD.get(op, BANKS)
     total = 0
     for phase in PHASES[op]:
@@ -771,16 +772,77 @@ def conv_f32_reg_launch(BM, BN, BK, WM, WN, MI, PAD, N, C, H, W, OC, R, S, sh, s
     total = stage.scaled(KT * tiles_m * tiles_n)
     base = 2 * (BM * AS + BK * BS) * 4
     total += _ktab_build(K, NW, base).scaled(tiles_m * tiles_n)
-    reads = 0
-    for tn in range(tiles_n):
-        for w in range(NW):
-            if tn * BN + (w * 64) % BN >= Ng:
-                continue                  # no lane of the wave has a pixel
-            brow0 = (w * 64) // BN
-            reads += sum(1 for k0 in range(0, KT * BK, BK) for i in range(BK // brpp)
-                         if k0 + brow0 + i * brpp < K)
-    total.add("ds_read_b32", [base] * 64, times=2 * reads * tiles_m)
+    total.add("ds_read_b32", [base] * 64,
+              times=_reg_table_reads(N, C, H, W, R, S, sh, sw, ph, pw, BN, NW, BK) * tiles_m)
     return total
+
+
+def conv_bf16_gather_launch(BM, BN, BK, WM, WN, MI, PAD, N, C, H, W, OC, R, S, sh, sw, ph, pw) -> LdsCost:
+    """The bf16 register-staged gather conv kernel: per K-stage the weight
+    tile's 16-byte stores (2-byte ones when C*R*S is not a multiple of 8),
+    one 2-byte store per gathered element, and the bf16 register-staged
+    GEMM's fragment reads (transpose reads for the pixel operand); the
+    k-offset table and its reads as in the fp32 kernel."""
+    OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    K, Ng = C * R * S, N * OH * OW
+    NW = (BM // WM) * (BN // WN)
+    NT = 64 * NW
+    KT = _cdiv(K, BK)
+    AS, BS = BK + PAD, BN + 32
+    vec = K % 8 == 0
+    WA = 8 if vec else 1
+    _, stage = gemm_bf16_reg_stage(BM, BN, BK, WM, WN, MI, PAD)
+    for w in range(NW):
+        for i in range(BM * BK // (WA * NT)):
+            addrs = []
+            for lane in range(64):
+                idx = w * 64 + lane + i * NT
+                r, c = idx // (BK // WA), (idx % (BK // WA)) * WA
+                addrs.append((r * AS + c) * 2)
+            stage.add("ds_write_b128" if vec else "ds_write_b16", addrs)
+    brpp = NT // BN
+    for w in range(NW):
+        for i in range(BK // brpp):
+            stage.add("ds_write_b16", [(((w * 64 + lane) // BN + i * brpp) * BS + (w * 64 + lane) % BN) * 2
+                                       for lane in range(64)])
+    tiles_m, tiles_n = _cdiv(OC, BM), _cdiv(Ng, BN)
+    total = stage.scaled(KT * tiles_m * tiles_n)
+    base = 2 * (BM * AS + BK * BS) * 2
+    total += _ktab_build(K, NW, base).scaled(tiles_m * tiles_n)
+    total.add("ds_read_b32", [base] * 64,
+              times=_reg_table_reads(N, C, H, W, R, S, sh, sw, ph, pw, BN, NW, BK) * tiles_m)
+    return total
+
+
+def _reg_table_reads(N, C, H, W, R, S, sh, sw, ph, pw, BN, NW, BK) -> int:
+    """Table reads of the register-staged gather conv kernels per output-
+    channel tile row: a wave reads the entry of each k row it gathers (every
+    lane the same entry) as two 4-byte reads, the first when one of its lanes
+    has a pixel and k < K, the second (the input offset) only when the tap
+    of k also falls inside the image for one of those lanes."""
+    import numpy as np
+    OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
+    K, Ng = C * R * S, N * OH * OW
+    brpp = 64 * NW // BN
+    ks = np.arange(K)
+    kh, kw = (ks % (R * S)) // S, ks % S
+    reads = 0
+    for tn in range(_cdiv(Ng, BN)):
+        for w in range(NW):
+            cols = (w * 64 + np.arange(64)) % BN + tn * BN
+            cols = cols[cols < Ng]
+            if cols.size == 0:
+                continue                  # no lane of the wave has a pixel
+            pix = cols % (OH * OW)
+            ih0, iw0 = (pix // OW) * sh - ph, (pix % OW) * sw - pw
+            rin = ((ih0[None, :] + np.arange(R)[:, None] >= 0) &
+                   (ih0[None, :] + np.arange(R)[:, None] < H))
+            cin = ((iw0[None, :] + np.arange(S)[:, None] >= 0) &
+                   (iw0[None, :] + np.arange(S)[:, None] < W))
+            tap_in = (rin[:, None, :] & cin[None, :, :]).any(axis=2)      # [R][S]
+            mine = ks[(ks % BK) % brpp == ((w * 64) // BN) % brpp]         # the k rows the wave gathers
+            reads += mine.size + int(tap_in[kh[mine], kw[mine]].sum())
+    return reads
 
 
 # the tap-major instances' stages and their k-table fallback's stages
@@ -806,8 +868,8 @@ def _conv_f32_gather(s: dict, k_order: int, stages: int, dims) -> LdsCost:
 
 def conv_launch(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
     """LDS cost of one conv launch of instance ``s``, or None when the kernel
-    it runs for this shape is not modelled (the 64x256 halo kernel and the
-    bf16 gather kernel)."""
+    it runs for this shape is not modelled (the fp32 64x256 halo kernel and
+    the few-channel kernel's gather form)."""
     sh, sw = (stride, stride) if isinstance(stride, int) else stride
     ph, pw = (pad, pad) if isinstance(pad, int) else pad
     OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
@@ -847,7 +909,12 @@ def conv_launch(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
         if halo_class and C % 16 == 0 and W % 2 == 0 and pw <= 2 and OW - pw + 3 <= 63 and span + 2 <= 8:
             return conv_bf16_halo_launch(N, C, H, W, OC, ph, pw, a_swizzle=True, rotate=True,
                                          store_order=True)
-        return None
+        # the halo launcher falls back to the gather kernel's 64x128 tiles
+        s = dict(s, k_order=0, block_m=64, block_n=128, block_k=32, wave_m=32, wave_n=64, mfma_m=32,
+                 lds_pad=8)
+    if dtype == "bf16" and s["k_order"] == 0:
+        return conv_bf16_gather_launch(s["block_m"], s["block_n"], s["block_k"], s["wave_m"], s["wave_n"],
+                                       s["mfma_m"], s["lds_pad"], *dims)
     return None
 
 
