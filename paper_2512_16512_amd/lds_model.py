@@ -845,6 +845,51 @@ def _reg_table_reads(N, C, H, W, R, S, sh, sw, ph, pw, BN, NW, BK) -> int:
     return reads
 
 
+def conv_f32_halo256_launch(N, C, H, W, OC, ph, pw) -> LdsCost:
+    """The fp32 64x256 halo kernel (k_order 2 with 64x256 tiles): four 64x64
+    waves of 32x32x2 instructions, one MFMA k-step per tap of an 8-channel
+    stage.  Per tap a wave reads two weight fragments (ds_read_b128 of
+    [tap][oc][8 channels] cells) and, per 32-pixel block, four ds_read_b32 of
+    the patch at the lane's pixel plus the tap's offset (planes of 8 rows x
+    64 columns + 8 floats).  Each workgroup reads C / 8 stages of nine taps
+    plus the first tap of the stage after its last."""
+    BM, BN, WN, MI, CC, PR, CO = 64, 256, 64, 32, 8, 8, 4
+    PLANE = PR * 64 + 8
+    A_BYTES = 9 * BM * CC * 4
+    OH, OW = H + 2 * ph - 2, W + 2 * pw - 2
+    OHW = OH * OW
+
+    def tap_cost(p0, tap):
+        oh0 = p0 // OW
+        kh, kw = divmod(tap, 3)
+        cost = LdsCost()
+        for w in range(BN // WN):
+            for i in range(BM // MI):
+                cost.add("ds_read_b128", [((lane % 32) * CC + 4 * (lane // 32)) * 4 +
+                                          (tap * BM * CC + i * MI * CC) * 4 for lane in range(64)])
+            for j in range(WN // MI):
+                base = []
+                for lane in range(64):
+                    pix = p0 + w * WN + j * MI + lane % 32
+                    off = 0                       # past the image: patch position 0
+                    if pix < OHW:
+                        oh, ow = divmod(pix, OW)
+                        off = (oh - oh0) * 64 + ow - pw + CO
+                    base.append((4 * (lane // 32) * PLANE + off) * 4)
+                for sub in range(4):
+                    cost.add("ds_read_b32", [A_BYTES + b + (sub * PLANE + kh * 64 + kw) * 4 for b in base])
+        return cost
+
+    total = LdsCost()
+    for chunk in range(_cdiv(OHW, BN)):
+        stage = LdsCost()
+        for tap in range(9):
+            stage += tap_cost(chunk * BN, tap)
+        total += stage.scaled(C // CC)
+        total += tap_cost(chunk * BN, 0)
+    return total.scaled(N * _cdiv(OC, BM))
+
+
 # the tap-major instances' stages and their k-table fallback's stages
 _TAP_FALLBACK = {(64, 256): 2, (64, 128): 3, (64, 64): 4, (128, 128): 3}
 
@@ -868,8 +913,8 @@ def _conv_f32_gather(s: dict, k_order: int, stages: int, dims) -> LdsCost:
 
 def conv_launch(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
     """LDS cost of one conv launch of instance ``s``, or None when the kernel
-    it runs for this shape is not modelled (the fp32 64x256 halo kernel and
-    the few-channel kernel's gather form)."""
+    it runs for this shape is not modelled (the few-channel kernel's gather
+    form, when the patch does not fit)."""
     sh, sw = (stride, stride) if isinstance(stride, int) else stride
     ph, pw = (pad, pad) if isinstance(pad, int) else pad
     OH, OW = (H + 2 * ph - R) // sh + 1, (W + 2 * pw - S) // sw + 1
@@ -891,7 +936,7 @@ def conv_launch(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
     if dtype == "f32" and s["k_order"] == 2:
         span = (256 - 1 + OW - 1) // OW + 1
         if halo_class and C % 16 == 0 and pw <= 4 and OW - pw + 5 <= 63 and span + 2 <= 8:
-            return None                   # the 64x256 halo kernel: not modelled
+            return conv_f32_halo256_launch(N, C, H, W, OC, ph, pw)
         return _conv_f32_gather(dict(s, block_m=64, block_n=256, wave_m=64, wave_n=64), 1, 2, dims)
     if dtype == "f32" and s["k_order"] == 1:
         return _conv_f32_gather(s, 1, s["lds_stages"], dims)

@@ -145,13 +145,21 @@ def test_small_channel_conv_matches_counters():
     assert c.conflict == 18816
 
 
-def test_unmodelled_kernels_return_none():
-    # the fp32 64x256 halo kernel, where its class applies, is not modelled
+def test_f32_64x256_halo_conv_matches_counters():
+    # measured SQ_LDS_IDX_ACTIVE / SQ_LDS_BANK_CONFLICT per launch, with
+    # conflicts (this kernel is not a default): 4672000 / 1756672 and
+    # 152000 / 57152
     s = dict(k_order=2, block_m=64, block_n=256, block_k=8, wave_m=64, wave_n=64, mfma_m=32,
              lds_stages=2, lds_pad=-1)
-    assert L.conv_launch("f32", s, 32, 64, 56, 56, 64, 3, 3, 1, 1) is None
-    # outside it the launcher falls back to the tap-major kernel, which is
+    c = L.conv_launch("f32", s, 32, 64, 56, 56, 64, 3, 3, 1, 1)
+    assert (c.active, c.conflict) == (4672000, 1756672)
+    c = L.conv_launch("f32", s, 4, 16, 56, 56, 16, 3, 3, 1, 1)
+    assert (c.active, c.conflict) == (152000, 57152)
+    # outside its class the launcher falls back to the tap-major kernel
     assert L.conv_launch("f32", s, 8, 128, 28, 28, 256, 3, 3, 1, 1).active == 1382400
+    # the few-channel kernel's gather form (the patch does not fit) is not modelled
+    few = dict(k_order=0, block_m=16, block_n=64, lds_stages=0)
+    assert L.conv_launch("f32", few, 32, 64, 56, 56, 64, 3, 3, 1, 1) is None
 
 
 def _conv_inst(bm, bn, wm, wn, mi, stages, pad, k_order, bk=32):
