@@ -547,7 +547,29 @@ def conv_grid(dtype: str, s: dict, N, C, H, W, OC, R, S, stride, pad):
         tn, seg = flattened(256)                       # the tap-major 64x256 fallback
         return 64, _cdiv(OC, 64), tn, seg, None
     if bm == 16:
-        return None                                    # patch-staged or gather: not modelled
+        # few output channels: 64-pixel tiles; the patch-staged form loads, per
+        # tile, its patch rows of every channel (rows outside the image read
+        # nothing); the gather form (the patch does not fit) is not modelled
+        bn = 64
+        span = (bn - 1 + OW - 1) // OW + 1
+        PR = (span - 1) * sh + R
+        vec = W % 4 == 0
+        padl = (pw + 3) // 4 * 4 if vec else pw
+        WP = (OW - 1) * sw + S - pw + padl
+        if vec:
+            WP = (WP + 3) // 4 * 4
+        K = C * R * S
+        kp = _cdiv(K, 32) * 32
+        area = max(C * PR * WP, 32 * bn)
+        if not (4 * (area + 16 * (kp + 2)) + 4 * kp <= 48 * 1024 and WP <= 256 and kp <= 256):
+            return None
+        chunks = _cdiv(OHW, bn)
+
+        def seg(tn):
+            img, c = divmod(tn, chunks)
+            lo = (c * bn // OW) * sh - ph
+            return [(img, max(0, lo), min(H - 1, lo + PR - 1))]
+        return 16, _cdiv(OC, 16), N * chunks, seg, None
     tn, seg = flattened(s["block_n"])
     return bm, _cdiv(OC, bm), tn, seg, None
 

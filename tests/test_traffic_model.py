@@ -268,3 +268,20 @@ def test_l2_model_against_counters(dtype, M, N, K, bm, bn, bk, pad, occ, measure
     tile = tm.gemm_tile(dtype, s, M, N, K)
     pred = tm.predict_l2_reads(M, N, K, 4 if dtype == "f32" else 2, *tile, occupancy=occ)
     assert 0.95 <= pred / measured <= 1.02
+
+
+def test_few_channel_conv_grid_and_counters():
+    # the patch-staged few-channel kernel: 64-pixel tiles, each reading its
+    # 9 patch rows (7x7 stride 2) of every channel; FETCH_SIZE x 1024 x
+    # 1.9998 measured 943650 bytes per launch on the paper's 7x7 layer
+    s = _sched(block_m=16, block_n=64, block_k=128, wave_m=16, wave_n=16, mfma_m=16, lds_stages=0, lds_pad=0)
+    dims = (1, 3, 224, 224, 16, 7, 7, 2, 3)
+    bm, tmm, tn, seg, force = tm.conv_grid("f32", s, *dims)
+    assert (bm, tmm, tn) == (16, 1, 112 * 112 // 64)
+    assert seg(1) == [(0, 0, 5)]        # pixels 64..127: output rows 0..1, patch rows -3..5
+    assert seg(2) == [(0, 0, 7)]        # pixels 128..191 start on output row 1: patch rows -1..7
+    assert seg(195) == [(0, 219, 223)]  # the last tile: patch rows 219..227, the image ends at 223
+    r, w = tm.predict_conv("f32", s, dims, 1)
+    assert w == 4 * 16 * 112 * 112 and 0.85 <= r / 943650 <= 0.95
+    # the gather form (the patch does not fit) is not modelled
+    assert tm.conv_grid("f32", s, 32, 64, 56, 56, 64, 3, 3, 1, 1) is None
