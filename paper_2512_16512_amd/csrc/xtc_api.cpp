@@ -293,7 +293,7 @@ xtc_status xtc_default_schedule(xtc_op op, xtc_dtype dt, int64_t M, int64_t N, i
     const int64_t t = tiles(out->block_m, out->block_n);
     out->raster = (mid || big) ? 4 : (t >= 64 ? 8 : 0);
     // The register-fed reduction-split tiles: column-major order (graph
-    // replays interleaved on one box: 256^3 3.36 -> 3.25 us, 256x258x512
+    // replays interleaved on one machine: 256^3 3.36 -> 3.25 us, 256x258x512
     // 5.77 -> 5.57 us, the 256x1024x128 matmul+relu 4.91 -> 4.78 us)
     if (out->k_split > 1 && out->lds_stages == 0) out->raster = 1;
     if (dt == XTC_BF16 && out->block_m == 256 && out->block_n == 256) {
