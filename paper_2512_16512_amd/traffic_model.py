@@ -620,6 +620,74 @@ def predict_conv(dtype: str, s: dict, dims, occupancy: int, l2_bytes: int = L2_B
     return read, 4 * N * OC * OH * OW
 
 
+def predict_conv_l2(dtype: str, s: dict, dims, line: int = LINE):
+    """Bytes the workgroups of one conv launch read from L2, for the kernels
+    that stage whole input rows (None for the others, whose gathers re-read
+    inputs through the L1 tap by tap): every workgroup reads, per channel
+    it stages, its patch or band rows inside the image as one contiguous
+    run, and its weights, each run in whole cache lines, with no reuse
+    between stages or workgroups.
+      - fp32 halo kernel (k_order 2, 64x208 or 64x416 tiles): per 8-channel
+        stage, 8 (one pixel half) or 10 (two) patch rows from the tile's
+        first output row less the padding, and the stage's 64 x 8 x 9
+        weights (one 288-byte run per output channel);
+      - bf16 row-streaming kernel (k_order 3): the band's input rows of all
+        64 channels and the 64 output channels' 576 weights each;
+      - few-channel kernel (block_m 16, patch-staged): its patch rows of
+        every channel and its 16 output channels' weights."""
+    import numpy as np
+    N, C, H, W, OC, R, S, stride, pad = dims
+    g = conv_grid(dtype, s, *dims)
+    if g is None:
+        return None
+    bm, tiles_m, tiles_n, seg, force = g
+    elt = 4 if dtype == "f32" else 2
+    OH, OW = (H + 2 * pad - R) // stride + 1, (W + 2 * pad - S) // stride + 1
+    K = C * R * S
+
+    def rows_run(img, c, lo, hi):
+        # each input row is its own load (its own instructions, at its own
+        # time), so a line two neighbouring rows share is fetched for each
+        if hi < lo:
+            return 0
+        starts = (((img * C + c) * H + np.arange(lo, hi + 1, dtype=np.int64)) * W * elt)
+        return int(((starts + W * elt - 1) // line - starts // line + 1).sum())
+
+    def weights(m, width):
+        rows = np.arange(m * bm, min(OC, (m + 1) * bm), dtype=np.int64)
+        return _block_lines(rows * K * elt, width * elt, line) if rows.size else 0
+
+    total = 0
+    halo16 = (dtype == "f32" and s["k_order"] == 2 and s["block_n"] in (208, 416) and R == 3 and S == 3
+              and stride == 1 and C % 8 == 0 and pad <= 4 and OW - pad + 5 <= 63 and tiles_n % N == 0
+              and tiles_n // N == _cdiv(OH * OW, 208 * (1 if s["block_n"] == 208 else 2)))
+    if halo16:
+        PR = 8 if s["block_n"] == 208 else 10
+        ohw = OH * OW
+        chunks = tiles_n // N
+        pt = _cdiv(ohw, chunks)
+        rows_total = 0
+        for img in range(N):
+            for ch in range(chunks):
+                lo = (ch * pt) // OW - pad
+                a, b = max(0, lo), min(H - 1, lo + PR - 1)
+                rows_total += sum(rows_run(img, c, a, b) for c in range(C))
+        for m in range(tiles_m):
+            oc = np.arange(m * bm, min(OC, (m + 1) * bm), dtype=np.int64)
+            w = sum(_block_lines(oc * K * 4 + c0 * 9 * 4, 8 * 9 * 4, line) for c0 in range(0, C, 8))
+            total += rows_total + w * tiles_n
+        return total * line
+    if (dtype == "bf16" and s["k_order"] == 3 and force == 1) or bm == 16:
+        per_tile_rows = 0
+        for tn in range(tiles_n):
+            for img, lo, hi in seg(tn):
+                per_tile_rows += sum(rows_run(img, c, lo, hi) for c in range(C))
+        for m in range(tiles_m):
+            total += per_tile_rows + weights(m, K) * tiles_n
+        return total * line
+    return None
+
+
 CONV_ORDERS = ((0, 1), (0, 0), (1, 1), (1, 0), (8, 1))
 
 
@@ -671,6 +739,27 @@ def correlate_conv(order_path: str, fetch_csv: str, fetch_scale: float):
     return table, pearson(x, y), spearman(x, y)
 
 
+def correlate_conv_l2(order_path: str, csv_path: str):
+    """Predicted (``predict_conv_l2``) vs measured (TCC_READ_SECTORS x 32)
+    L2 read bytes per conv schedule of a ``run-conv`` order file; the
+    statistics are over the modelled schedules."""
+    o = json.load(open(order_path))
+    vals = _counter_rows(csv_path, "TCC_READ_SECTORS_sum")
+    reps = o["reps"]
+    if len(vals) != reps * len(o["schedules"]):
+        raise ValueError("%d counter rows for %d schedules x %d launches"
+                         % (len(vals), len(o["schedules"]), reps))
+    table = []
+    for i, e in enumerate(o["schedules"]):
+        meas = sum(vals[i * reps:(i + 1) * reps]) / reps * SECTOR
+        pred = predict_conv_l2(o["dtype"], e["sched"], tuple(o["dims"]))
+        table.append({"sched": e["sched"], "predicted": pred, "measured": meas})
+    mod = [t for t in table if t["predicted"] is not None]
+    x = [t["predicted"] for t in mod]
+    y = [t["measured"] for t in mod]
+    return table, pearson(x, y), spearman(x, y)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -707,6 +796,9 @@ def main(argv=None):
     cl.add_argument("order")
     cl.add_argument("csv")
     cl.add_argument("--json", default=None)
+    cv = sub.add_parser("correlate-conv-l2")
+    cv.add_argument("order")
+    cv.add_argument("csv")
     cc = sub.add_parser("correlate-conv")
     cc.add_argument("order")
     cc.add_argument("fetch_csv")
@@ -727,6 +819,14 @@ def main(argv=None):
         if a.json:
             with open(a.json, "w") as f:
                 json.dump({"pearson": r_, "spearman": rho, "rows": table}, f, indent=1)
+        return 0
+    if a.cmd == "correlate-conv-l2":
+        table, r_, rho = correlate_conv_l2(a.order, a.csv)
+        for t in table:
+            if t["predicted"] is not None:
+                print("%s  predicted %.4g  measured %.4g  %.3f" % (
+                    {k: t["sched"][k] for k in ("block_m", "block_n", "k_order", "raster", "xcd_remap")},
+                    t["predicted"], t["measured"], t["predicted"] / t["measured"]))
         return 0
     if a.cmd == "correlate-conv":
         table, r_, rho = correlate_conv(a.order, a.fetch_csv, a.fetch_scale)

@@ -285,3 +285,26 @@ def test_few_channel_conv_grid_and_counters():
     assert w == 4 * 16 * 112 * 112 and 0.85 <= r / 943650 <= 0.95
     # the gather form (the patch does not fit) is not modelled
     assert tm.conv_grid("f32", s, 32, 64, 56, 56, 64, 3, 3, 1, 1) is None
+
+
+def test_conv_l2_reads_row_loads_and_weights():
+    # bf16 row-streaming kernel, 32x64x56x56 -> 64: 224 workgroups, each
+    # reading its band's 10 input rows (8 for the first and last bands, which
+    # start or end in the padding) of 64 channels, each 112-byte row as whole
+    # lines of its own, and 64 x 576 weights (72 KiB, 576 lines)
+    s = _sched(block_n=64, block_m=64, block_k=16, k_order=3)
+    dims = (32, 64, 56, 56, 64, 3, 3, 1, 1)
+    got = tm.predict_conv_l2("bf16", s, dims)
+    rows = 0
+    for img in range(32):
+        for band in range(7):
+            lo, hi = max(0, band * 8 - 1), min(55, band * 8 + 8)
+            for c in range(64):
+                for r in range(lo, hi + 1):
+                    st = ((img * 64 + c) * 56 + r) * 112
+                    rows += (st + 111) // 128 - st // 128 + 1
+    assert got == (rows + 224 * 576) * 128
+    # measured TCC_READ_SECTORS x 32: 39.65e6 bytes (raster 0, XCD remap)
+    assert 1.1 <= got / 39.65e6 <= 1.2
+    # the gather kernels are not modelled
+    assert tm.predict_conv_l2("f32", _sched(block_n=128, k_order=0, lds_stages=3), dims) is None
