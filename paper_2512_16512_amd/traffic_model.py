@@ -40,7 +40,8 @@ The level above.  ``predict_l2_reads`` models what the workgroups of a
 matmul read from L2 (TCC_READ_SECTORS): each tile's operand panels, one
 K-stage at a time, in whole cache lines, with lines that consecutive stages
 share kept only when the resident workgroups' stage blocks fit in half the
-CU's L1 (``correlate-l2``).
+CU's L1 (``correlate-l2``).  ``predict_conv_l2`` does the same for the conv
+kernels that stage whole input rows (``correlate-conv-l2``).
 
 Usage (the measurement step runs under rocprofv3; see ``run``)::
 
@@ -55,6 +56,9 @@ Usage (the measurement step runs under rocprofv3; see ``run``)::
     rocprofv3 --pmc TCC_READ_SECTORS_sum -f csv -d OUT -o run -- \\
         python3 -m paper_2512_16512_amd.traffic_model run f32 1000 1000 1000 --order ORDER.json --rasters 0,1
     python -m paper_2512_16512_amd.traffic_model correlate-l2 ORDER.json OUT/run_counter_collection.csv
+    rocprofv3 --pmc TCC_READ_SECTORS_sum -f csv -d OUT -o run -- \\
+        python3 -m paper_2512_16512_amd.traffic_model run-conv bf16 32 64 56 56 64 3 3 1 1 --order ORDER.json
+    python -m paper_2512_16512_amd.traffic_model correlate-conv-l2 ORDER.json OUT/run_counter_collection.csv
 """
 from __future__ import annotations
 
